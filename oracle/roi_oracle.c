@@ -1,0 +1,465 @@
+/*
+ * roi_oracle.c -- plain, slow, single-threaded CPU oracle of the RoI
+ * differentiable N:M mask sampler (arxiv 2608.23048, "Reservoir of Importance").
+ *
+ * TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT.  Only the test suite, the
+ * smoke check and the benchmark's CPU-baseline leg may load this library.  It
+ * shares no code, header, table or constant with the HIP library; the two
+ * agree only because both follow the same written definitions below.
+ *
+ * What is computed, per group of m consecutive weights (§4.1: a mask keeps
+ * exactly n of every m contiguous parameters):
+ *
+ *   1. noise      u_j ~ U(0,1) from a counter-based generator, g_j = -log(-log u_j)
+ *                 (Appendix, Algorithm 1: Gumbel noise);
+ *   2. keys       kappa_j = phi_j / lambda + g_j
+ *                 (§3.2 / §4.2.2 key equation; §4.2.3: the Gumbel trick is
+ *                 applied to the scaled logits phi / lambda);
+ *   3. hard mask  the n largest keys, i.e. arg-top-n (§3.2 Gumbel-Top-K; the
+ *                 straight-through variant of the appendix emits this mask in
+ *                 the forward pass), so W_masked = W (.) hard (§4.1);
+ *   4. relaxation alpha^(1) = kappa, mu^(k) = softmax(alpha^(k)/tau),
+ *                 alpha^(k+1) = alpha^(k) + log(1 - mu^(k)),  S = sum_k mu^(k)
+ *                 (§3.2 recursion, §4.2.2, Algorithm 1);
+ *   5. backward   reverse-mode derivative of S with respect to phi, with the
+ *                 upstream gradient of S equal to dL/dW_masked (.) W (the
+ *                 straight-through estimator: backward through the relaxation).
+ *
+ * Readings of points the paper leaves open (each also listed in the design
+ * notes):
+ *   - u comes from Philox4x32-10 (Salmon et al., SC'11) keyed by the seed,
+ *     with counter (element/4, step) and word element%4; u is the odd 23-bit
+ *     grid point (2*(x>>9)+1) * 2^-24, never 0 or 1.
+ *   - "log" in the noise is the deterministic fp32 logarithm oracle_log()
+ *     below, so that the keys, and therefore the hard selection, are one
+ *     well-defined fp32 value for every input.
+ *   - keys are fp32: kappa = fl(fl(phi / lambda) + g).
+ *   - ties between keys go to the lower index; the returned indices are in
+ *     selection order (descending key).
+ *   - the relaxation and its derivative run in fp64 from the fp32 keys;
+ *     1 - mu_i is evaluated as sum_{j != i} mu_j (same value, no cancellation)
+ *     and log(1 - mu) is floored at log(FLT_MIN) with zero derivative there.
+ *   - pruned weights are +0.0 (bf16 bits 0x0000).
+ */
+#include "roi_oracle.h"
+
+#include <float.h>
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_MAX_M 64
+
+/* ------------------------------------------------------------------------- *
+ * 1. Counter-based uniform source: Philox4x32-10 as published by Salmon,
+ *    Moraes, Dror and Shaw ("Parallel random numbers: as easy as 1, 2, 3",
+ *    SC'11).  Round: two 32x32->64 products of the even words with the two
+ *    Philox multipliers, the high halves xor-ed with the odd words and the
+ *    round key; the key advances by the two Weyl increments between rounds.
+ * ------------------------------------------------------------------------- */
+static const uint32_t PHILOX_MULT_A = 0xD2511F53u;
+static const uint32_t PHILOX_MULT_B = 0xCD9E8D57u;
+static const uint32_t WEYL_A = 0x9E3779B9u; /* golden ratio */
+static const uint32_t WEYL_B = 0xBB67AE85u; /* sqrt(3) - 1 */
+
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += WEYL_A;
+            k1 += WEYL_B;
+        }
+        uint64_t pa = (uint64_t)PHILOX_MULT_A * (uint64_t)c0;
+        uint64_t pb = (uint64_t)PHILOX_MULT_B * (uint64_t)c2;
+        uint32_t pa_hi = (uint32_t)(pa >> 32), pa_lo = (uint32_t)pa;
+        uint32_t pb_hi = (uint32_t)(pb >> 32), pb_lo = (uint32_t)pb;
+        uint32_t n0 = pb_hi ^ c1 ^ k0;
+        uint32_t n1 = pb_lo;
+        uint32_t n2 = pa_hi ^ c3 ^ k1;
+        uint32_t n3 = pa_lo;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Word for global element `elem` at training step `step`. */
+uint32_t oracle_philox_word(uint64_t seed, uint64_t step, uint64_t elem)
+{
+    uint64_t block = elem / 4u;
+    uint32_t ctr[4] = {(uint32_t)block, (uint32_t)(block >> 32), (uint32_t)step,
+                       (uint32_t)(step >> 32)};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t out[4];
+    oracle_philox4x32_10(ctr, key, out);
+    return out[elem % 4u];
+}
+
+/* u ~ U(0,1): the odd points of the 2^-24 grid, (2k+1) 2^-24 for the top 23
+ * bits k of the word.  Exact in fp32; the extreme values are 2^-24 and
+ * 1 - 2^-24. */
+float oracle_uniform(uint32_t word)
+{
+    uint32_t k = word >> 9;
+    double u = ((double)k * 2.0 + 1.0) / 16777216.0; /* exact */
+    return (float)u;                                    /* exact */
+}
+
+/* ------------------------------------------------------------------------- *
+ * 2. Deterministic fp32 natural logarithm.  Written from the mathematics:
+ *    x = m 2^E with m in [sqrt(1/2), sqrt(2)), ln x = E ln 2 + ln m, and
+ *    ln m = 2 atanh(s) with s = (m-1)/(m+1) = f/(f+2), f = m-1, expanded as
+ *    2s + s^3 (2/3 + (2/5) s^2 + (2/7) s^4 + (2/9) s^6) (the first terms of
+ *    the atanh series; |s| <= 0.1716, the dropped terms are below 1e-9
+ *    relative).  ln 2 is split Cody-Waite style into a 16-bit head (so that
+ *    E * head is exact) and an fp32 tail.  Every operation is one IEEE fp32
+ *    operation (add, multiply, divide, or fused multiply-add), in the order
+ *    written, so the result is a single well-defined fp32 value.
+ *    Valid for finite normal x > 0, which covers every value the noise
+ *    definition feeds it (u in [2^-24, 1-2^-24] and -ln u in [5.9e-8, 16.7]).
+ * ------------------------------------------------------------------------- */
+static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+
+float oracle_log(float x)
+{
+    /* Series coefficients 2/k rounded to fp32, and ln 2 = head + tail. */
+    const float c3 = (float)(2.0 / 3.0);
+    const float c5 = (float)(2.0 / 5.0);
+    const float c7 = (float)(2.0 / 7.0);
+    const float c9 = (float)(2.0 / 9.0);
+    const double ln2 = 0.69314718055994530941723212145818;
+    const float ln2_head = (float)(floor(ln2 * 65536.0) / 65536.0); /* 16 significant bits */
+    const float ln2_tail = (float)(ln2 - (double)ln2_head);
+
+    uint32_t bits = f2u(x);
+    int e = (int)(bits >> 23) - 127;
+    uint32_t frac = bits & 0x7FFFFFu;
+    float m = u2f(frac | 0x3F800000u); /* m in [1, 2) */
+    /* Bring m into [sqrt(1/2), sqrt(2)): halve it when m > sqrt(2).  The
+     * smallest fp32 above sqrt(2) is 0x3FB504F4. */
+    if ((frac | 0x3F800000u) >= 0x3FB504F4u) {
+        m = m * 0.5f;
+        e = e + 1;
+    }
+    float f = m - 1.0f;          /* exact */
+    float s = f / (f + 2.0f);
+    float z = s * s;
+    float p = fmaf(c9, z, c7);
+    p = fmaf(p, z, c5);
+    p = fmaf(p, z, c3);
+    float t = s * z;
+    float r = fmaf(t, p, s + s); /* ln m */
+    float ef = (float)e;
+    float lo = fmaf(ef, ln2_tail, r);
+    return fmaf(ef, ln2_head, lo);
+}
+
+void oracle_log_array(const float* x, int64_t n, float* out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_log(x[i]);
+}
+
+/* Algorithm 1: g = -log(-log u). */
+float oracle_gumbel(float u)
+{
+    float y = -oracle_log(u);
+    return -oracle_log(y);
+}
+
+void oracle_gumbel_from_words(const uint32_t* words, int64_t n, float* g)
+{
+    for (int64_t i = 0; i < n; ++i) g[i] = oracle_gumbel(oracle_uniform(words[i]));
+}
+
+/* §3.2 / §4.2.2: kappa = phi_bar + g with phi_bar = phi / lambda (§4.2.3). */
+static float key_of(float phi, float lambda, uint64_t seed, uint64_t step, uint64_t elem)
+{
+    float g = oracle_gumbel(oracle_uniform(oracle_philox_word(seed, step, elem)));
+    float phi_bar = phi / lambda;
+    return phi_bar + g;
+}
+
+void oracle_keys(const float* phi, int64_t numel, float lambda, uint64_t seed, uint64_t step,
+                 uint64_t elem_offset, float* kappa)
+{
+    for (int64_t i = 0; i < numel; ++i)
+        kappa[i] = key_of(phi[i], lambda, seed, step, elem_offset + (uint64_t)i);
+}
+
+/* ------------------------------------------------------------------------- *
+ * 3. Hard Gumbel-Top-K (§3.2): pick the largest key, then the largest of the
+ *    rest, n times.  A strict '>' keeps the lowest index among equal keys
+ *    (fp32 -0 and +0 compare equal).  order[k] is the k-th selected index.
+ * ------------------------------------------------------------------------- */
+int oracle_topn(const float* kappa, int m, int n, uint8_t* order, uint8_t* hard)
+{
+    if (m < 1 || m > ORACLE_MAX_M || n < 1 || n > m) return -1;
+    int taken[ORACLE_MAX_M];
+    for (int j = 0; j < m; ++j) taken[j] = 0;
+    for (int k = 0; k < n; ++k) {
+        int best = -1;
+        for (int j = 0; j < m; ++j) {
+            if (taken[j]) continue;
+            if (best < 0 || kappa[j] > kappa[best]) best = j;
+        }
+        taken[best] = 1;
+        if (order) order[k] = (uint8_t)best;
+    }
+    if (hard)
+        for (int j = 0; j < m; ++j) hard[j] = (uint8_t)taken[j];
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- *
+ * 4. Relaxation (§3.2 recursion, §4.2.2, Algorithm 1), fp64.
+ *    One step: mu = softmax(alpha / tau), evaluated with the largest alpha
+ *    subtracted first; omega_i = 1 - mu_i evaluated as sum_{j != i} mu_j;
+ *    alpha <- alpha + log(max(omega, FLT_MIN)).  The step record keeps mu,
+ *    omega and whether the floor was hit, for the backward.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    double mu[ORACLE_MAX_M];
+    double omega[ORACLE_MAX_M];
+    int floored[ORACLE_MAX_M];
+} relax_step;
+
+static void softmax_step(const double* alpha, int m, double tau, relax_step* st)
+{
+    double amax = alpha[0];
+    for (int j = 1; j < m; ++j)
+        if (alpha[j] > amax) amax = alpha[j];
+    double e[ORACLE_MAX_M];
+    double total = 0.0;
+    for (int j = 0; j < m; ++j) {
+        e[j] = exp((alpha[j] - amax) / tau);
+        total += e[j];
+    }
+    for (int i = 0; i < m; ++i) {
+        st->mu[i] = e[i] / total;
+        double others = 0.0;
+        for (int j = 0; j < m; ++j)
+            if (j != i) others += e[j];
+        st->omega[i] = others / total;
+        st->floored[i] = st->omega[i] < (double)FLT_MIN;
+    }
+}
+
+static void relax_forward(const double* kappa, int m, int n, double tau, relax_step* steps,
+                          double* S)
+{
+    double alpha[ORACLE_MAX_M];
+    for (int j = 0; j < m; ++j) {
+        alpha[j] = kappa[j]; /* alpha^(1) = kappa */
+        if (S) S[j] = 0.0;
+    }
+    for (int k = 0; k < n; ++k) {
+        softmax_step(alpha, m, tau, &steps[k]);
+        for (int j = 0; j < m; ++j) {
+            if (S) S[j] += steps[k].mu[j];
+            double om = steps[k].floored[j] ? (double)FLT_MIN : steps[k].omega[j];
+            alpha[j] += log(om);
+        }
+    }
+}
+
+int oracle_relax_fwd(const double* kappa, int m, int n, double tau, double* S)
+{
+    if (m < 1 || m > ORACLE_MAX_M || n < 1 || n > m || !(tau > 0.0)) return -1;
+    relax_step* steps = (relax_step*)malloc(sizeof(relax_step) * (size_t)n);
+    if (!steps) return -2;
+    relax_forward(kappa, m, n, tau, steps, S);
+    free(steps);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- *
+ * 5. Backward of S = sum_k mu^(k) with respect to kappa (reverse mode).
+ *    The paper writes no backward; this is the chain rule through the
+ *    recursion of §3.2.  With sbar = dL/dS and a = dL/dalpha^(k+1) carried
+ *    down from the later steps (a = 0 above the last step):
+ *      mubar_i   = sbar_i - a_i / omega_i         (d log(omega_i)/d mu_i = -1/omega_i;
+ *                                                   0 where the floor was hit)
+ *      dL/dalpha^(k)_i = a_i + (mu_i / tau) (mubar_i - sum_j mu_j mubar_j)
+ *    Because 1 - mu_i = omega_i, the softmax term equals
+ *      (mu_i / tau) (omega_i mubar_i - sum_{j != i} mu_j mubar_j),
+ *    and omega_i mubar_i = omega_i sbar_i - a_i exactly, so
+ *      dL/dalpha^(k)_i = a_i (1 - mu_i / tau) + (mu_i / tau) (omega_i sbar_i - sum_{j != i} mu_j mubar_j)
+ *    with 1 - mu_i / tau = (omega_i + (tau - 1)) / tau.  This form never
+ *    subtracts two large nearly equal numbers when mu_i is close to 1.
+ *    Finally dL/dkappa = dL/dalpha^(1).
+ * ------------------------------------------------------------------------- */
+static void relax_backward(const relax_step* steps, int m, int n, double tau, const double* sbar,
+                           double* dkappa)
+{
+    double a[ORACLE_MAX_M];
+    for (int j = 0; j < m; ++j) a[j] = 0.0;
+    for (int k = n - 1; k >= 0; --k) {
+        const relax_step* st = &steps[k];
+        int has_next = (k < n - 1); /* alpha^(k+1) feeds a later step */
+        double mubar[ORACLE_MAX_M];
+        for (int j = 0; j < m; ++j) {
+            double via_log = (has_next && !st->floored[j]) ? a[j] / st->omega[j] : 0.0;
+            mubar[j] = sbar[j] - via_log;
+        }
+        double a_new[ORACLE_MAX_M];
+        for (int i = 0; i < m; ++i) {
+            double others = 0.0;
+            for (int j = 0; j < m; ++j)
+                if (j != i) others += st->mu[j] * mubar[j];
+            double soft = (st->mu[i] / tau) * (st->omega[i] * sbar[i] - others);
+            double carried = 0.0;
+            if (has_next) {
+                /* (omega - 1 + tau) / tau, grouped so that tau == 1 gives omega exactly */
+                double keep = st->floored[i] ? 1.0 : (st->omega[i] + (tau - 1.0)) / tau;
+                carried = a[i] * keep;
+            }
+            a_new[i] = carried + soft;
+        }
+        for (int j = 0; j < m; ++j) a[j] = a_new[j];
+    }
+    for (int j = 0; j < m; ++j) dkappa[j] = a[j];
+}
+
+int oracle_relax_bwd(const double* kappa, int m, int n, double tau, const double* sbar,
+                     double* dkappa)
+{
+    if (m < 1 || m > ORACLE_MAX_M || n < 1 || n > m || !(tau > 0.0)) return -1;
+    relax_step* steps = (relax_step*)malloc(sizeof(relax_step) * (size_t)n);
+    if (!steps) return -2;
+    relax_forward(kappa, m, n, tau, steps, NULL);
+    relax_backward(steps, m, n, tau, sbar, dkappa);
+    free(steps);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- *
+ * 6. Whole groups.
+ * ------------------------------------------------------------------------- */
+static float bf16_to_float(uint16_t h)
+{
+    return u2f((uint32_t)h << 16);
+}
+
+static int check_args(int64_t count, int n, int m, float tau, float lambda)
+{
+    if (count < 0) return -1;
+    if (m < 1 || m > ORACLE_MAX_M || n < 1 || n > m) return -1;
+    if (!(tau > 0.0f) || !(lambda > 0.0f)) return -1;
+    if (!isfinite(tau) || !isfinite(lambda)) return -1;
+    return 0;
+}
+
+static void group_fwd(const uint16_t* W, const float* phi, int n, int m, float tau,
+                      float lambda, uint64_t seed, uint64_t step, uint64_t elem0,
+                      uint16_t* Wm, double* S, uint8_t* idx, relax_step* steps)
+{
+    float kappa[ORACLE_MAX_M] = {0};
+    uint8_t order[ORACLE_MAX_M], hard[ORACLE_MAX_M];
+    for (int j = 0; j < m; ++j) kappa[j] = key_of(phi[j], lambda, seed, step, elem0 + (uint64_t)j);
+    oracle_topn(kappa, m, n, order, hard);
+    for (int j = 0; j < m; ++j) Wm[j] = hard[j] ? W[j] : (uint16_t)0x0000u;
+    if (idx)
+        for (int k = 0; k < n; ++k) idx[k] = order[k];
+    if (S) {
+        double kd[ORACLE_MAX_M];
+        for (int j = 0; j < m; ++j) kd[j] = (double)kappa[j];
+        relax_forward(kd, m, n, (double)tau, steps, S);
+    }
+}
+
+static void group_bwd(const uint16_t* G, const uint16_t* W, const float* phi, int n, int m,
+                      float tau, float lambda, uint64_t seed, uint64_t step, uint64_t elem0,
+                      double* dphi, relax_step* steps)
+{
+    double kd[ORACLE_MAX_M] = {0}, sbar[ORACLE_MAX_M] = {0}, dk[ORACLE_MAX_M] = {0};
+    for (int j = 0; j < m; ++j) {
+        kd[j] = (double)key_of(phi[j], lambda, seed, step, elem0 + (uint64_t)j);
+        /* Straight-through: W_masked is used as W (.) S in the backward, so
+         * dL/dS = dL/dW_masked (.) W. */
+        sbar[j] = (double)bf16_to_float(G[j]) * (double)bf16_to_float(W[j]);
+    }
+    relax_forward(kd, m, n, (double)tau, steps, NULL);
+    relax_backward(steps, m, n, (double)tau, sbar, dk);
+    /* kappa = phi / lambda + g, so dL/dphi = dL/dkappa / lambda. */
+    for (int j = 0; j < m; ++j) dphi[j] = dk[j] / (double)lambda;
+}
+
+int roi_oracle_fwd(const uint16_t* W, const float* logits, int64_t numel, int n, int m,
+                   float tau, float lambda, uint64_t seed, uint64_t step, uint64_t elem_offset,
+                   uint16_t* W_masked, double* soft_mask, uint8_t* sel_idx)
+{
+    if (check_args(numel, n, m, tau, lambda) || numel % m != 0) return -1;
+    relax_step* steps = (relax_step*)malloc(sizeof(relax_step) * (size_t)n);
+    if (!steps) return -2;
+    for (int64_t q = 0; q < numel / m; ++q) {
+        int64_t base = q * m;
+        group_fwd(W + base, logits + base, n, m, tau, lambda, seed, step,
+                  elem_offset + (uint64_t)base, W_masked + base,
+                  soft_mask ? soft_mask + base : NULL, sel_idx ? sel_idx + q * n : NULL, steps);
+    }
+    free(steps);
+    return 0;
+}
+
+int roi_oracle_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
+                   int64_t numel, int n, int m, float tau, float lambda, uint64_t seed,
+                   uint64_t step, uint64_t elem_offset, double* grad_logits)
+{
+    if (check_args(numel, n, m, tau, lambda) || numel % m != 0) return -1;
+    relax_step* steps = (relax_step*)malloc(sizeof(relax_step) * (size_t)n);
+    if (!steps) return -2;
+    for (int64_t q = 0; q < numel / m; ++q) {
+        int64_t base = q * m;
+        group_bwd(grad_W_masked + base, W + base, logits + base, n, m, tau, lambda, seed, step,
+                  elem_offset + (uint64_t)base, grad_logits + base, steps);
+    }
+    free(steps);
+    return 0;
+}
+
+int roi_oracle_fwd_groups(const uint16_t* W, const float* logits, int64_t ngroups,
+                          const uint64_t* group_elem, int n, int m, float tau, float lambda,
+                          uint64_t seed, uint64_t step, uint16_t* W_masked, double* soft_mask,
+                          uint8_t* sel_idx)
+{
+    if (check_args(ngroups, n, m, tau, lambda)) return -1;
+    relax_step* steps = (relax_step*)malloc(sizeof(relax_step) * (size_t)n);
+    if (!steps) return -2;
+    for (int64_t q = 0; q < ngroups; ++q) {
+        int64_t base = q * m;
+        group_fwd(W + base, logits + base, n, m, tau, lambda, seed, step, group_elem[q],
+                  W_masked + base, soft_mask ? soft_mask + base : NULL,
+                  sel_idx ? sel_idx + q * n : NULL, steps);
+    }
+    free(steps);
+    return 0;
+}
+
+int roi_oracle_bwd_groups(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
+                          int64_t ngroups, const uint64_t* group_elem, int n, int m, float tau,
+                          float lambda, uint64_t seed, uint64_t step, double* grad_logits)
+{
+    if (check_args(ngroups, n, m, tau, lambda)) return -1;
+    relax_step* steps = (relax_step*)malloc(sizeof(relax_step) * (size_t)n);
+    if (!steps) return -2;
+    for (int64_t q = 0; q < ngroups; ++q) {
+        int64_t base = q * m;
+        group_bwd(grad_W_masked + base, W + base, logits + base, n, m, tau, lambda, seed, step,
+                  group_elem[q], grad_logits + base, steps);
+    }
+    free(steps);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- *
+ * 7. §4.2.3, exponential annealing:
+ *    v_t = max{ v_end, v_init (v_end / v_init)^(t / T_anneal) }.
+ * ------------------------------------------------------------------------- */
+double oracle_anneal(double v_init, double v_end, double t, double t_anneal)
+{
+    double v = v_init * pow(v_end / v_init, t / t_anneal);
+    return v > v_end ? v : v_end;
+}

@@ -1,0 +1,564 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: an
+independent library implementation (rocRAND's Philox4x32-10, numpy/scipy
+log and softmax, torch autograd, mpmath), a closed form derived from the
+paper's recursion, exact rational arithmetic, brute-force enumeration of the
+Weighted-Reservoir-Sampling law (Eq. 1, §3.1), or an invariant.  No GPU.
+"""
+from __future__ import annotations
+
+import itertools
+import json
+import math
+import os
+import shutil
+import subprocess
+from fractions import Fraction
+
+import numpy as np
+import pytest
+from scipy import special, stats
+
+import oracle
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def ulp32(x: np.ndarray) -> np.ndarray:
+    x = np.abs(np.asarray(x, dtype=np.float32))
+    return np.spacing(x).astype(np.float64)
+
+
+# --------------------------------------------------------------------------- Philox
+@pytest.fixture(scope="module")
+def rocrand_ref(tmp_path_factory):
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available for the rocRAND reference")
+    exe = str(tmp_path_factory.mktemp("rr") / "philox_ref")
+    subprocess.run([hipcc, "-O1", "-w", "-o", exe, os.path.join(HERE, "rocrand_philox_ref.cpp")],
+                   check=True, capture_output=True)
+    return exe
+
+
+def test_philox_matches_rocrand(rocrand_ref):
+    """Philox4x32-10 (Salmon et al., SC'11) with counter (elem/4, step), key
+    seed and word elem%4 equals rocRAND's engine at (seed, subsequence=step,
+    offset=elem), an independent implementation of the same generator."""
+    cases = [
+        (0, 0, 0, 64),
+        (1, 0, 0, 16),
+        (0, 1, 0, 16),
+        (0x0123456789ABCDEF, 9, 1000003, 37),
+        (0xFFFFFFFF00000001, (1 << 32) + 5, (1 << 34) - 6, 40),  # counter crosses 2^32 blocks
+        (42, 7, 6525288448 - 13, 29),  # near the end of the 7B-class stack
+        (2**64 - 1, 2**64 - 1, 2**63 + 1, 11),
+    ]
+    text = "".join(f"{s} {st} {o} {c}\n" for s, st, o, c in cases)
+    out = subprocess.run([rocrand_ref], input=text, capture_output=True, text=True, check=True)
+    ref = [int(w, 16) for w in out.stdout.split()]
+    mine = []
+    for s, st, o, c in cases:
+        mine += [oracle.philox_word(s, st, o + i) for i in range(c)]
+    assert mine == ref
+
+
+def test_philox_block_structure():
+    """The four words of one call are the four elements of one block."""
+    out = oracle.philox4x32_10([5, 0, 3, 0], [11, 0])
+    assert [oracle.philox_word(11, 3, 20 + i) for i in range(4)] == list(out)
+
+
+def test_philox_bit_balance():
+    words = np.array([oracle.philox_word(0, 0, e) for e in range(1 << 16)], dtype=np.uint32)
+    bits = np.unpackbits(words.view(np.uint8))
+    # 2^21 fair bits: mean within 5 sigma of 1/2
+    assert abs(bits.mean() - 0.5) < 5 * 0.5 / math.sqrt(bits.size)
+    hist = np.bincount(words >> 24, minlength=256)
+    chi2 = ((hist - hist.mean()) ** 2 / hist.mean()).sum()
+    assert stats.chi2.sf(chi2, 255) > 1e-4
+
+
+# --------------------------------------------------------------------------- uniform
+def test_uniform_grid_exact_and_open():
+    assert oracle.uniform(0) == 2.0 ** -24
+    assert oracle.uniform(0xFFFFFFFF) == 1.0 - 2.0 ** -24
+    rng = np.random.default_rng(1)
+    for w in rng.integers(0, 2**32, 2000, dtype=np.uint64):
+        u = oracle.uniform(int(w))
+        k = int(w) >> 9
+        assert u * 2**24 == 2 * k + 1
+        assert 0.0 < u < 1.0
+
+
+# --------------------------------------------------------------------------- deterministic log
+def test_log_accuracy_every_mantissa():
+    """Every fp32 mantissa in four binades (all 2^23 values each): the fp32
+    result is within 2 ulp of numpy's fp64 log (error measured in ulp of the
+    correctly rounded fp32 value, or absolutely near ln x = 0)."""
+    mant = np.arange(1 << 23, dtype=np.uint32)
+    for exp_bits in (126, 127, 100, 131):  # [0.5,1), [1,2), tiny, [16,32)
+        x = ((np.uint32(exp_bits) << 23) | mant).view(np.float32)
+        got = oracle.log32_array(x).astype(np.float64)
+        ref = np.log(x.astype(np.float64))
+        err = np.abs(got - ref) / np.maximum(ulp32(ref.astype(np.float32)), 2.0 ** -149)
+        # near x = 1 the value is tiny; there the error is bounded relative to |ln x| by
+        # the same 2 ulp (the reduction leaves m - 1 exact), so the ulp measure applies.
+        assert err.max() <= 2.0, (exp_bits, err.max(), x[err.argmax()])
+
+
+def test_log_special_values():
+    assert oracle.log32(1.0) == 0.0
+    for k in range(-24, 8):
+        got = float(oracle.log32(2.0 ** k))
+        assert abs(got - k * math.log(2)) <= float(ulp32(np.float32(k * math.log(2)))) + 1e-30
+
+
+# --------------------------------------------------------------------------- Gumbel noise
+@pytest.fixture(scope="module")
+def gumbel_grid():
+    k = np.arange(1 << 23, dtype=np.uint32)
+    words = k << np.uint32(9)
+    u = (2.0 * k.astype(np.float64) + 1.0) * 2.0 ** -24
+    g = oracle.gumbel_from_words(words).astype(np.float64)
+    return u, g
+
+
+def test_gumbel_is_inverse_cdf(gumbel_grid):
+    """Algorithm 1: g = -log(-log u) is the inverse of the Gumbel(0,1) CDF
+    F(g) = exp(-exp(-g)).  Over all 2^23 grid values, g matches the fp64
+    inverse CDF within the fp32 error budget of the two logarithms."""
+    u, g = gumbel_grid
+    ref = -np.log(-np.log(u))
+    # inner log relative error (<= 2 ulp) becomes an absolute error in g; the
+    # outer log adds <= 2 ulp of g.
+    tol = 2.5 * 2.0 ** -23 + 2.5 * ulp32(ref.astype(np.float32))
+    assert np.all(np.abs(g - ref) <= tol)
+    assert np.all(np.abs(np.exp(-np.exp(-g)) - u) <= 4e-6 * np.maximum(u, 1e-3))
+
+
+def test_gumbel_monotone_and_moments(gumbel_grid):
+    u, g = gumbel_grid
+    assert np.all(np.diff(g) >= 0)
+    assert g.min() > -3.0 and g.max() < 17.0
+    # midpoint rule over the full grid: E[g] = Euler-Mascheroni, Var[g] = pi^2/6
+    assert abs(g.mean() - np.euler_gamma) < 2e-6
+    assert abs(g.var() - math.pi ** 2 / 6) < 2e-5
+
+
+def test_keys_use_scaled_logits():
+    """§4.2.3: the trick is applied to phi / lambda; with the noise fixed the
+    keys move by exactly the change of phi / lambda (up to fp32 rounding)."""
+    phi = np.linspace(-3, 3, 64).astype(np.float32)
+    k1 = oracle.keys(phi, 1.0, 3, 4, 128).astype(np.float64)
+    k0 = oracle.keys(np.zeros_like(phi), 1.0, 3, 4, 128).astype(np.float64)
+    k2 = oracle.keys(phi, 2.0, 3, 4, 128).astype(np.float64)
+    assert np.allclose(k1 - k0, phi, atol=4e-6)
+    assert np.allclose(k2 - k0, phi / 2.0, atol=4e-6)
+
+
+# --------------------------------------------------------------------------- hard top-N
+def test_topn_matches_sort_with_ties():
+    rng = np.random.default_rng(7)
+    for trial in range(3000):
+        m = int(rng.choice([4, 8, 16, 32, 5, 3]))
+        n = int(rng.integers(1, m + 1))
+        kappa = rng.normal(size=m).astype(np.float32)
+        if trial % 3 == 0:  # heavy ties, including -0 and +0
+            kappa = rng.choice(np.array([0.0, -0.0, 1.0, -1.0], dtype=np.float32), size=m)
+        order, hard = oracle.topn(kappa, n)
+        ref = sorted(range(m), key=lambda j: (-float(kappa[j]), j))[:n]
+        assert list(order) == ref
+        assert hard.sum() == n and all(hard[j] for j in ref)
+
+
+def test_minus_zero_ties_plus_zero():
+    order, _ = oracle.topn(np.array([-0.0, 0.0, -1.0, -2.0], dtype=np.float32), 1)
+    assert order[0] == 0
+    order, _ = oracle.topn(np.array([-1.0, 0.0, -0.0, -2.0], dtype=np.float32), 2)
+    assert list(order) == [1, 2]
+
+
+# --------------------------------------------------------------------------- WRS law (Eq. 1)
+def wrs_ordered_prob(w, order):
+    """Eq. 1 (§3.1): product of w_{y_i} / (W - sum_{j<i} w_{y_j})."""
+    total = sum(w)
+    p = Fraction(1)
+    used = Fraction(0)
+    for y in order:
+        p *= w[y] / (total - used)
+        used += w[y]
+    return p
+
+
+def sample_selection(w, n, groups, lam=1.0, seed=0, step=0):
+    m = len(w)
+    phi = np.tile((lam * np.log(np.array([float(x) for x in w]))).astype(np.float32), groups)
+    W = np.ones(phi.size, dtype=np.uint16) * 0x3F80
+    _, _, idx = oracle.mask_fwd(W, phi, n, m, 1.0, lam, seed, step, 0, want_soft=False)
+    return idx
+
+
+@pytest.mark.parametrize("w,n,groups,ordered,lam", [
+    ((Fraction(4, 10), Fraction(3, 10), Fraction(2, 10), Fraction(1, 10)), 2, 400_000, True, 1.0),
+    ((Fraction(4, 10), Fraction(3, 10), Fraction(2, 10), Fraction(1, 10)), 2, 200_000, True, 0.5),
+    ((Fraction(5), Fraction(1), Fraction(3), Fraction(1)), 1, 200_000, True, 1.0),
+    ((Fraction(5), Fraction(1), Fraction(3), Fraction(1)), 3, 200_000, True, 1.0),
+    (tuple(Fraction(k) for k in (8, 1, 2, 7, 3, 1, 5, 4)), 2, 200_000, True, 1.0),
+    (tuple(Fraction(k) for k in (8, 1, 2, 7, 3, 1, 5, 4)), 4, 200_000, False, 1.0),
+])
+def test_selection_law_is_wrs(w, n, groups, ordered, lam):
+    """Selection frequencies of the hard top-n equal brute-force enumeration
+    of the WRS law: ordered tuples against Eq. 1 directly, unordered subsets
+    against Eq. 1 summed over orderings (the mask distribution of §4.2.1)."""
+    m = len(w)
+    idx = sample_selection(w, n, groups, lam=lam, seed=12345, step=3)
+    if ordered:
+        outcomes = list(itertools.permutations(range(m), n))
+        probs = np.array([float(wrs_ordered_prob(w, o)) for o in outcomes])
+        code = np.zeros(idx.shape[0], dtype=np.int64)
+        for k in range(n):
+            code = code * m + idx[:, k]
+        keys = [sum(o[k] * m ** (n - 1 - k) for k in range(n)) for o in outcomes]
+    else:
+        outcomes = list(itertools.combinations(range(m), n))
+        probs = np.array([float(sum(wrs_ordered_prob(w, p) for p in itertools.permutations(c)))
+                          for c in outcomes])
+        code = np.zeros(idx.shape[0], dtype=np.int64)
+        for k in range(n):
+            code |= np.int64(1) << idx[:, k].astype(np.int64)
+        keys = [sum(1 << j for j in c) for c in outcomes]
+    assert abs(probs.sum() - 1.0) < 1e-12
+    lookup = {kk: i for i, kk in enumerate(keys)}
+    counts = np.zeros(len(outcomes))
+    vals, cnt = np.unique(code, return_counts=True)
+    for v, c in zip(vals, cnt):
+        counts[lookup[int(v)]] += c
+    expected = probs * idx.shape[0]
+    keep = expected >= 5
+    obs = np.append(counts[keep], counts[~keep].sum())
+    exp_ = np.append(expected[keep], expected[~keep].sum())
+    if exp_[-1] == 0:
+        obs, exp_ = obs[:-1], exp_[:-1]
+    chi2 = ((obs - exp_) ** 2 / exp_).sum()
+    assert stats.chi2.sf(chi2, len(obs) - 1) > 1e-4, (chi2, len(obs))
+
+
+def test_inclusion_probabilities_2of4():
+    """Worked example derived from Eq. 1: w = (0.4, 0.3, 0.2, 0.1), 2:4.
+    Inclusion probabilities sum to N."""
+    w = (Fraction(4, 10), Fraction(3, 10), Fraction(2, 10), Fraction(1, 10))
+    incl = [sum(wrs_ordered_prob(w, o) for o in itertools.permutations(range(4), 2) if j in o)
+            for j in range(4)]
+    assert sum(incl) == 2
+    idx = sample_selection(w, 2, 400_000, seed=99)
+    freq = np.array([(idx == j).any(axis=1).mean() for j in range(4)])
+    assert np.allclose(freq, [float(x) for x in incl], atol=5 * 0.5 / math.sqrt(400_000))
+
+
+# --------------------------------------------------------------------------- relaxation
+def exact_relaxation_tau1(w, n):
+    """S at tau = 1 in exact rational arithmetic.  With e = exp(alpha), the
+    recursion of §3.2 reads mu = e / sum(e), e <- e (1 - mu): every quantity
+    stays rational when the initial weights exp(kappa) are rational."""
+    e = [Fraction(x) for x in w]
+    S = [Fraction(0)] * len(e)
+    for _ in range(n):
+        t = sum(e)
+        mu = [x / t for x in e]
+        S = [s + x for s, x in zip(S, mu)]
+        e = [x * (1 - y) for x, y in zip(e, mu)]
+    return S
+
+
+def test_relaxation_worked_example_exact():
+    w = (Fraction(4, 10), Fraction(3, 10), Fraction(2, 10), Fraction(1, 10))
+    S = oracle.relax_fwd(np.log([0.4, 0.3, 0.2, 0.1]), 2, 1.0)
+    assert exact_relaxation_tau1(w, 2) == [Fraction(26, 35), Fraction(3, 5), Fraction(3, 7),
+                                           Fraction(8, 35)]
+    assert np.allclose(S, [26 / 35, 3 / 5, 3 / 7, 8 / 35], rtol=1e-14, atol=0)
+    # S_j may exceed 1: M = 2, N = 2, p = (0.9, 0.1) gives (1.4, 0.6)
+    assert np.allclose(oracle.relax_fwd(np.log([0.9, 0.1]), 2, 1.0), [1.4, 0.6], rtol=1e-14)
+
+
+@pytest.mark.parametrize("m,n", [(4, 1), (4, 2), (4, 3), (4, 4), (8, 4), (8, 7), (16, 8), (32, 4),
+                                 (5, 3)])
+def test_relaxation_exact_rational_tau1(m, n):
+    rng = np.random.default_rng(m * 100 + n)
+    for _ in range(20):
+        w = [Fraction(int(x), 64) for x in rng.integers(1, 256, size=m)]
+        ref = exact_relaxation_tau1(w, n)
+        S = oracle.relax_fwd(np.log([float(x) for x in w]), n, 1.0)
+        assert np.allclose(S, [float(x) for x in ref], rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("tau", [0.1, 0.5, 1.0, 2.0])
+def test_relaxation_closed_forms_n1_n2(tau):
+    """N = 1: S = softmax(kappa / tau) (the Gumbel-softmax).  N = 2:
+    S = p + p (1-p)^(1/tau) / sum(p (1-p)^(1/tau)), p = softmax(kappa/tau)
+    (one step of the §3.2 recursion in closed form)."""
+    rng = np.random.default_rng(int(tau * 100))
+    for m in (4, 8, 16):
+        for _ in range(30):
+            kappa = rng.normal(scale=2.0, size=m)
+            p = special.softmax(kappa / tau)
+            assert np.allclose(oracle.relax_fwd(kappa, 1, tau), p, rtol=1e-12, atol=1e-300)
+            q = p * (1.0 - p) ** (1.0 / tau)
+            assert np.allclose(oracle.relax_fwd(kappa, 2, tau), p + q / q.sum(), rtol=1e-11,
+                               atol=1e-300)
+
+
+def test_relaxation_invariants():
+    rng = np.random.default_rng(3)
+    for _ in range(500):
+        m = int(rng.choice([4, 8, 16, 32]))
+        n = int(rng.integers(1, m + 1))
+        tau = float(rng.choice([0.1, 0.3, 1.0, 3.0]))
+        kappa = rng.normal(scale=3.0, size=m)
+        S = oracle.relax_fwd(kappa, n, tau)
+        assert abs(S.sum() - n) < 1e-12 * n * m
+        assert np.all(S >= 0) and np.all(S <= n)
+        perm = rng.permutation(m)
+        assert np.allclose(oracle.relax_fwd(kappa[perm], n, tau), S[perm], rtol=1e-12, atol=1e-300)
+        assert np.allclose(oracle.relax_fwd(kappa + 5.25, n, tau), S, rtol=1e-12, atol=1e-300)
+
+
+def test_relaxation_zero_temperature_limit_is_hard_topn():
+    """tau -> 0: every softmax becomes the one-hot of the current maximum and
+    log(1 - mu) removes it, so S tends to the hard top-n mask."""
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        m = int(rng.choice([4, 8, 16]))
+        n = int(rng.integers(1, m + 1))
+        kappa = rng.permutation(np.arange(m, dtype=np.float64)) * 0.5  # gaps >= 0.5
+        _, hard = oracle.topn(kappa.astype(np.float32), n)
+        S = oracle.relax_fwd(kappa, n, 1e-3)
+        assert np.allclose(S, hard, atol=1e-12)
+
+
+def test_relaxation_large_temperature_is_uniform():
+    kappa = np.array([3.0, -1.0, 0.5, 2.0, 0.0, 1.0, -2.0, 4.0])
+    assert np.allclose(oracle.relax_fwd(kappa, 3, 1e9), 3 / 8, atol=1e-8)
+
+
+# --------------------------------------------------------------------------- backward
+def test_backward_n1_closed_form():
+    """N = 1: the softmax Jacobian, dkappa = (1/tau) p (sbar - <p, sbar>)."""
+    rng = np.random.default_rng(11)
+    for _ in range(200):
+        m = int(rng.choice([4, 8, 16]))
+        tau = float(rng.choice([0.2, 1.0, 2.5]))
+        kappa = rng.normal(scale=2, size=m)
+        sbar = rng.normal(size=m)
+        p = special.softmax(kappa / tau)
+        ref = p * (sbar - p @ sbar) / tau
+        assert np.allclose(oracle.relax_bwd(kappa, 1, tau, sbar), ref, rtol=1e-11, atol=1e-14)
+
+
+@pytest.mark.parametrize("m,n", [(4, 2), (4, 3), (4, 4), (8, 4), (16, 8), (5, 3), (32, 16)])
+@pytest.mark.parametrize("tau", [1.0, 0.5, 0.3, 2.0])
+def test_backward_matches_finite_differences(m, n, tau):
+    rng = np.random.default_rng(m * 1000 + n * 10 + int(tau * 10))
+    for _ in range(4):
+        kappa = rng.normal(scale=1.5, size=m)
+        sbar = rng.normal(size=m)
+        got = oracle.relax_bwd(kappa, n, tau, sbar)
+        h = 1e-6
+        fd = np.empty(m)
+        for j in range(m):
+            kp, km = kappa.copy(), kappa.copy()
+            kp[j] += h
+            km[j] -= h
+            fd[j] = (oracle.relax_fwd(kp, n, tau) - oracle.relax_fwd(km, n, tau)) @ sbar / (2 * h)
+        assert np.allclose(got, fd, rtol=1e-6, atol=1e-8 * np.abs(sbar).max()), (got, fd)
+
+
+def torch_relaxation(kappa, n, tau):
+    """The §3.2 recursion written literally with torch ops, for autograd."""
+    import torch
+    alpha = kappa
+    S = torch.zeros_like(kappa)
+    for _ in range(n):
+        mu = torch.softmax(alpha / tau, dim=-1)
+        S = S + mu
+        alpha = alpha + torch.log1p(-mu)
+    return S
+
+
+@pytest.mark.parametrize("m,n", [(4, 2), (8, 4), (8, 7), (16, 8), (32, 16)])
+def test_backward_matches_torch_autograd(m, n):
+    import torch
+    rng = np.random.default_rng(m + 31 * n)
+    for tau in (1.0, 0.5, 2.0):
+        for _ in range(10):
+            kappa = rng.normal(scale=1.0, size=m)
+            sbar = rng.normal(size=m)
+            k = torch.tensor(kappa, dtype=torch.float64, requires_grad=True)
+            S = torch_relaxation(k, n, tau)
+            (S * torch.tensor(sbar, dtype=torch.float64)).sum().backward()
+            ref = k.grad.numpy()
+            got = oracle.relax_bwd(kappa, n, tau, sbar)
+            assert np.allclose(got, ref, rtol=1e-8, atol=1e-11)
+            assert np.allclose(oracle.relax_fwd(kappa, n, tau), S.detach().numpy(), rtol=1e-12)
+
+
+def mp_relaxation(kappa, n, tau):
+    import mpmath as mp
+    alpha = list(kappa)
+    S = [mp.mpf(0)] * len(alpha)
+    for _ in range(n):
+        a_max = max(alpha)
+        e = [mp.exp((a - a_max) / tau) for a in alpha]
+        t = mp.fsum(e)
+        mu = [x / t for x in e]
+        S = [s + x for s, x in zip(S, mu)]
+        alpha = [a + mp.log(mp.fsum(mu[:j] + mu[j + 1:])) for j, a in enumerate(alpha)]
+    return S
+
+
+@pytest.mark.parametrize("kappa,n,tau", [
+    ([30.0, 0.0, 0.5, -1.0], 2, 1.0),     # first pick nearly certain: 1 - mu ~ 1e-13
+    ([30.0, 0.0, 0.5, -1.0], 3, 1.0),
+    ([25.0, 24.0, 0.0, -3.0], 3, 1.0),
+    ([12.0, 0.0, 0.3, -1.0], 2, 2.0),      # tau > 1
+    ([12.0, 0.0, 0.3, -1.0, 1.0, 2.0, -0.5, 0.7], 4, 0.5),
+    ([8.0, 0.0, 0.3, -1.0], 2, 0.3),       # omega^(1/tau) tiny but no floor
+])
+def test_backward_extreme_keys_mpmath(kappa, n, tau):
+    """Keys with a dominant entry, where a naive reverse sweep cancels
+    catastrophically: compare with 60-digit finite differences of the
+    recursion evaluated in mpmath."""
+    import mpmath as mp
+    mp.mp.dps = 60
+    m = len(kappa)
+    rng = np.random.default_rng(17)
+    sbar = rng.normal(size=m)
+    got = oracle.relax_bwd(np.array(kappa), n, tau, sbar)
+    h = mp.mpf("1e-25")
+    ref = []
+    for j in range(m):
+        kp = [mp.mpf(x) for x in kappa]
+        km = [mp.mpf(x) for x in kappa]
+        kp[j] += h
+        km[j] -= h
+        sp, sm = mp_relaxation(kp, n, mp.mpf(tau)), mp_relaxation(km, n, mp.mpf(tau))
+        ref.append(float(mp.fsum((a - b) * mp.mpf(float(s)) for a, b, s in zip(sp, sm, sbar))
+                         / (2 * h)))
+    ref = np.array(ref)
+    assert np.allclose(got, ref, rtol=1e-9, atol=1e-12 * np.abs(sbar).max()), (got, ref)
+    S = oracle.relax_fwd(np.array(kappa), n, tau)
+    Smp = np.array([float(x) for x in mp_relaxation([mp.mpf(x) for x in kappa], n, mp.mpf(tau))])
+    assert np.allclose(S, Smp, rtol=1e-12, atol=1e-300)
+
+
+def test_backward_uniform_upstream_is_zero():
+    """sum_j S_j = N for every kappa, so a constant upstream gradient has zero
+    derivative."""
+    rng = np.random.default_rng(23)
+    for _ in range(300):
+        m = int(rng.choice([4, 8, 16, 32]))
+        n = int(rng.integers(1, m + 1))
+        tau = float(rng.choice([0.1, 0.5, 1.0]))
+        kappa = rng.normal(scale=2, size=m)
+        c = float(rng.normal())
+        d = oracle.relax_bwd(kappa, n, tau, np.full(m, c))
+        assert np.abs(d).max() <= 1e-12 * abs(c) * m / tau
+
+
+# --------------------------------------------------------------------------- whole arrays
+def test_fwd_outputs_consistent():
+    rng = np.random.default_rng(29)
+    m, n = 4, 2
+    numel = 4096
+    W = (rng.normal(scale=0.02, size=numel).astype(np.float32).view(np.uint32) >> 16).astype(
+        np.uint16)
+    W[::7] = 0x8000  # some -0.0 weights
+    phi = rng.normal(size=numel).astype(np.float32)
+    Wm, S, idx = oracle.mask_fwd(W, phi, n, m, 0.5, 1.0, 1, 2, 64)
+    hard = np.zeros((numel // m, m), dtype=bool)
+    np.put_along_axis(hard, idx.astype(np.int64), True, axis=1)
+    assert np.all(hard.sum(1) == n)
+    assert np.array_equal(Wm, np.where(hard.reshape(-1), W, np.uint16(0)))
+    assert np.allclose(S.reshape(-1, m).sum(1), n, atol=1e-12)
+    kappa = oracle.keys(phi, 1.0, 1, 2, 64).reshape(-1, m)
+    for q in range(0, numel // m, 97):
+        order, _ = oracle.topn(kappa[q], n)
+        assert list(order) == list(idx[q])
+        assert np.allclose(S.reshape(-1, m)[q], oracle.relax_fwd(kappa[q].astype(np.float64), n,
+                                                                 0.5), rtol=1e-15)
+
+
+def test_groups_entry_matches_contiguous():
+    rng = np.random.default_rng(31)
+    m, n, numel = 8, 4, 8 * 300
+    W = rng.integers(0, 65536, numel).astype(np.uint16)
+    W = np.where((W & 0x7F80) == 0x7F80, np.uint16(0x3F80), W)  # no inf/nan patterns
+    phi = rng.normal(size=numel).astype(np.float32)
+    G = rng.integers(0, 65536, numel).astype(np.uint16)
+    G = np.where((G & 0x7F80) == 0x7F80, np.uint16(0x3F80), G)
+    off = 4 * 12345
+    Wm, S, idx = oracle.mask_fwd(W, phi, n, m, 0.7, 1.3, 5, 6, off)
+    d = oracle.mask_bwd(G, W, phi, n, m, 0.7, 1.3, 5, 6, off)
+    sel = np.array([3, 0, 299, 150])
+    ge = off + sel * m
+    Wg, Sg, ig = oracle.mask_fwd_groups(W.reshape(-1, m)[sel], phi.reshape(-1, m)[sel], ge, n, m,
+                                        0.7, 1.3, 5, 6)
+    dg = oracle.mask_bwd_groups(G.reshape(-1, m)[sel], W.reshape(-1, m)[sel],
+                                phi.reshape(-1, m)[sel], ge, n, m, 0.7, 1.3, 5, 6)
+    assert np.array_equal(Wg, Wm.reshape(-1, m)[sel])
+    assert np.array_equal(ig, idx[sel])
+    assert np.array_equal(Sg, S.reshape(-1, m)[sel])
+    assert np.array_equal(dg, d.reshape(-1, m)[sel])
+
+
+def test_bwd_chains_straight_through_and_lambda():
+    """dL/dphi = (1/lambda) dS/dkappa^T (G (.) W): the straight-through backward
+    treats W_masked as W (.) S."""
+    rng = np.random.default_rng(37)
+    m, n, numel = 4, 2, 64
+    Wf = rng.normal(scale=0.5, size=numel).astype(np.float32)
+    Gf = rng.normal(size=numel).astype(np.float32)
+    W = (Wf.view(np.uint32) >> 16).astype(np.uint16)
+    G = (Gf.view(np.uint32) >> 16).astype(np.uint16)
+    phi = rng.normal(size=numel).astype(np.float32)
+    lam = float(np.float32(0.8))  # the oracle takes fp32 temperatures
+    tau = float(np.float32(0.9))
+    d = oracle.mask_bwd(G, W, phi, n, m, tau, lam, 2, 3, 0)
+    kappa = oracle.keys(phi, lam, 2, 3, 0).astype(np.float64).reshape(-1, m)
+    Wd = (W.astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1, m)
+    Gd = (G.astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1, m)
+    for q in range(numel // m):
+        ref = oracle.relax_bwd(kappa[q], n, tau, Gd[q] * Wd[q]) / lam
+        assert np.allclose(d.reshape(-1, m)[q], ref, rtol=1e-15, atol=0)
+
+
+def test_argument_checks():
+    W = np.zeros(8, dtype=np.uint16)
+    phi = np.zeros(8, dtype=np.float32)
+    for bad in [dict(n=0, m=4), dict(n=5, m=4), dict(n=2, m=3)]:
+        with pytest.raises(ValueError):
+            oracle.mask_fwd(W, phi, bad["n"], bad["m"], 1.0, 1.0, 0, 0)
+    with pytest.raises(ValueError):
+        oracle.mask_fwd(W, phi, 2, 4, 0.0, 1.0, 0, 0)
+    with pytest.raises(ValueError):
+        oracle.mask_fwd(W, phi, 2, 4, 1.0, -1.0, 0, 0)
+
+
+# --------------------------------------------------------------------------- annealing
+def test_anneal_schedule_paper_hyperparameters():
+    """§4.2.3 exponential annealing with the appendix's settings: starts at
+    the initial value, reaches the final value at T_anneal, stays there, and
+    decays by a constant ratio per step."""
+    hp = json.load(open(os.path.join(HERE, "golden", "hyperparameters.json")))
+    T = hp["t_anneal"]
+    for a, b in ((hp["tau_init"], hp["tau_end"]), (hp["lambda_init"], hp["lambda_end"])):
+        vals = np.array([oracle.anneal(a, b, t, T) for t in range(hp["training_steps"] + 1)])
+        assert vals[0] == a
+        assert math.isclose(vals[T], b, rel_tol=1e-12)
+        assert np.all(vals[T:] == b) or np.allclose(vals[T:], b, rtol=1e-12)
+        ratios = vals[1:T] / vals[: T - 1]
+        assert np.allclose(ratios, (b / a) ** (1.0 / T), rtol=1e-10)
+    # 10-step schedule from 1.0 to 0.1 reaching 0.1 at the last step
+    taus = [oracle.anneal(1.0, 0.1, t, 9) for t in range(10)]
+    assert taus[0] == 1.0 and math.isclose(taus[9], 0.1, rel_tol=1e-12)
