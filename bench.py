@@ -1,0 +1,185 @@
+"""Benchmark of the RoI N:M mask sampler step (mask forward + backward) on one GPU.
+
+A step is one forward (hard top-n sample, masked weights and selected
+indices) and one backward (grad_logits from grad_W_masked) over the whole
+synthetic stack, with every input already resident in HBM.  The default
+workload is the 7B-class full stack at 2:4 (28 layers x 7 linears, 196
+tensors, 6.53e9 masked weights) with tau annealed from 1.0 to 0.1 over 10
+steps (§4.2.3 exponential schedule); the stack is one back-to-back slab, so
+each direction is one kernel launch.
+
+Prints one JSON line (rank 0).  Kernel durations come from HIP events
+recorded on the stream the kernels are launched on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "masked weights/sec (mask fwd+bwd) and achieved HBM GB/s vs peak, 7B-class 2:4"
+HBM_PEAK_GBPS = 8000.0
+
+
+def algorithmic_bytes(n: int, m: int) -> tuple[float, float]:
+    """Bytes per weight the method must move: forward reads W (bf16) and the
+    logits (fp32) and writes W_masked (bf16) and n/m index bytes; backward
+    reads grad_W_masked and W (bf16) and the logits, and writes grad_logits."""
+    return 2 + 4 + 2 + n / m, 2 + 2 + 4 + 4
+
+
+def cpu_baseline(W, L, G, work, n, m, tau):
+    """The CPU oracle, as it is, on a bounded sample of the same workload: the
+    q, k, v and o projections of layer 0, one forward + backward."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    sample = [t for t in work.tensors[:4]]
+    end = sample[-1].offset + sample[-1].numel
+    bits = lambda t: t[:end].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    Wb, Gb, Lf = bits(W), bits(G), L[:end].cpu().numpy()
+    t0 = time.perf_counter()
+    oracle.mask_fwd(Wb, Lf, n, m, tau, 1.0, 0, 0, 0, want_soft=False)
+    oracle.mask_bwd(Gb, Wb, Lf, n, m, tau, 1.0, 0, 0, 0)
+    dt = time.perf_counter() - t0
+    names = "+".join(t.name.split(".")[-1] for t in sample)
+    return {"value": end / dt, "unit": "masked weights/s", "cores": 1, "kind": "oracle",
+            "sample": f"layer 0 {names} ({end} weights), one mask fwd+bwd, {dt:.1f} s on 1 thread"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="qwen2.5-7b-stack-2:4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the sampler needs no collectives, and this build "
+              "runs and reports a single MI355X (pass --gpus 1).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2608_23048_amd as roi
+    from paper_2608_23048_amd import workloads as wl
+
+    roi.lib()  # raises if the HIP library is not built
+    work = wl.WORKLOADS[args.workload]
+    n, m = work.n, work.m
+    dev = torch.device("cuda:0")
+    numel = work.numel
+    print(f"# workload {work.name}: {len(work.tensors)} tensors, {numel} weights, {n}:{m}",
+          file=sys.stderr, flush=True)
+    W, L, G = wl.fill_slab(work, dev, step=0)
+    Wm = torch.empty_like(W)
+    idx = torch.empty((numel // m, n), dtype=torch.uint8, device=dev)
+    dphi = torch.empty_like(L)
+    torch.cuda.synchronize()
+
+    def tau_at(t: int) -> float:
+        if work.tau_schedule is None:
+            return work.tau
+        a, b, T = work.tau_schedule
+        return roi.anneal(a, b, t, T)
+
+    def step(t: int, ev=None):
+        tau = tau_at(t)
+        if ev is not None:
+            ev[0].record()
+        roi.mask_fwd(W, L, n, m, tau, 1.0, 0, t, 0, want_soft=False, want_idx=True,
+                     out={"W_masked": Wm, "sel_idx": idx})
+        if ev is not None:
+            ev[1].record()
+        roi.mask_bwd(G, W, L, n, m, tau, 1.0, 0, t, 0, out=dphi)
+        if ev is not None:
+            ev[2].record()
+
+    for i in range(args.warmup):
+        step(1000 + i)
+    torch.cuda.synchronize()
+    print(f"# warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.steps):
+        step(t, events[t])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in events]
+    bwd_ms = [e[1].elapsed_time(e[2]) for e in events]
+    fwd_avg = sum(fwd_ms) / len(fwd_ms)
+    bwd_avg = sum(bwd_ms) / len(bwd_ms)
+    bf, bb = algorithmic_bytes(n, m)
+    fwd_gbps = bf * numel / (fwd_avg * 1e-3) / 1e9
+    bwd_gbps = bb * numel / (bwd_avg * 1e-3) / 1e9
+    dominant = ("roi_mask_bwd", bwd_gbps, bb) if bwd_avg >= fwd_avg else ("roi_mask_fwd", fwd_gbps, bf)
+    value = numel * args.steps / elapsed
+    ms_per_step = elapsed * 1e3 / args.steps
+    print(f"# timed {args.steps} steps: {ms_per_step:.3f} ms/step, fwd {fwd_avg:.3f} ms "
+          f"({fwd_gbps:.0f} GB/s), bwd {bwd_avg:.3f} ms ({bwd_gbps:.0f} GB/s)", file=sys.stderr,
+          flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(W, L, G, work, n, m, tau_at(0))
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "masked weights/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded W~N(0,0.02^2) bf16, logits~N(0,1) fp32, "
+                "grad~N(0,1e-6) bf16; Qwen2.5 shapes only)",
+        "config": {
+            "workload": work.name,
+            "tensors": len(work.tensors),
+            "masked_weights": numel,
+            "pattern": f"{n}:{m}",
+            "tau": (f"{work.tau_schedule[0]}->{work.tau_schedule[1]} exponential over "
+                    f"{work.tau_schedule[2] + 1} steps" if work.tau_schedule else work.tau),
+            "lambda": 1.0,
+            "launches_per_step": 2,
+        },
+        "step_algorithmic_GBps": (bf + bb) * value / 1e9,
+        "kernels": {
+            "roi_mask_fwd": {"avg_ms": fwd_avg, "algorithmic_bytes_per_weight": bf,
+                             "GBps": fwd_gbps},
+            "roi_mask_bwd": {"avg_ms": bwd_avg, "algorithmic_bytes_per_weight": bb,
+                             "GBps": bwd_gbps},
+        },
+        "roofline": {
+            "kernel": dominant[0],
+            "bound": "hbm",
+            "achieved": dominant[1],
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": dominant[1] / HBM_PEAK_GBPS,
+            "traffic": None,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,149 @@
+/*
+ * roi.h -- C ABI of the MI355X (gfx950) RoI differentiable N:M mask sampler.
+ *
+ * The method: "Reservoir of Importance: Learning Semi-Structured Sparsity with
+ * Differentiable Subset Sampling" (arxiv 2608.23048).  Every group of m
+ * consecutive weights carries m logits phi (one per weight, §4.2.1).  Each
+ * training step perturbs them with Gumbel noise into keys (§3.2, §4.2.2),
+ * keeps the n largest keys (hard Gumbel-Top-K, §3.2), and relaxes that
+ * selection into a soft n-hot mask S by n softmax steps (§3.2 recursion,
+ * Appendix Algorithm 1).  The forward emits the hard-masked weights; the
+ * backward differentiates through the relaxation (the straight-through
+ * variant of the appendix, "Comparison with Straight-Through Gumbel-Top-K").
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ *  - Pointers are DEVICE pointers on the current HIP device, 16-byte aligned,
+ *    contiguous; inputs and outputs must not overlap.  The caller owns all
+ *    memory; the library allocates none.
+ *  - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
+ *  - A weight tensor is row-major [rows, cols] (PyTorch Linear: [out, in]);
+ *    groups are m consecutive elements along cols, so cols % m == 0.  Any
+ *    back-to-back stack of such tensors is itself a valid [1, total] input:
+ *    groups never straddle tensors, and the noise depends only on the global
+ *    element index.
+ *  - Calls are asynchronous on `stream` (0 = the null stream).  Argument
+ *    errors are detected on the host and returned before anything is
+ *    launched; nothing is written then.  No exceptions cross the ABI.
+ *  - Return value: ROI_OK or a negative roi_status; roi_last_error() gives a
+ *    thread-local human-readable detail of the last failure.
+ *  - Supported patterns: m in {4, 8} with 1 <= n <= m.
+ *
+ * Noise (the same definition the forward and the backward use):
+ *  - global element index e = elem_offset + (flat index of the element);
+ *  - x = word (e mod 4) of Philox4x32-10 (Salmon et al., SC'11) with key
+ *    (lo32 seed, hi32 seed) and counter (lo32 e/4, hi32 e/4, lo32 step,
+ *    hi32 step);
+ *  - u = (2 (x >> 9) + 1) 2^-24, in (0, 1) (Algorithm 1: u ~ Uniform(0,1));
+ *  - g = -L(-L(u)) with L the library's deterministic fp32 logarithm
+ *    (Algorithm 1: g = -log(-log u)); L(x) = E ln2 + 2 atanh(s) for
+ *    x = m 2^E, m in [sqrt(1/2), sqrt(2)), s = (m-1)/(m+1), evaluated by
+ *    a fixed sequence of IEEE fp32 operations, so the value is reproducible;
+ *  - kappa = fl(fl(phi / lambda) + g) in fp32 (§3.2 key; §4.2.3 applies the
+ *    trick to phi / lambda).
+ *  Given (seed, step, elem_offset) the noise is a pure function, so the
+ *  backward regenerates it instead of storing it, and any split of a stack
+ *  into calls with matching elem_offset gives identical results.
+ */
+#ifndef ROI_H
+#define ROI_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ROI_OK = 0,
+    ROI_E_INVAL = -1,       /* invalid argument (sizes, pattern, temperatures, pointers) */
+    ROI_E_UNSUPPORTED = -2, /* valid for the method but not built: m outside {4, 8} */
+    ROI_E_HIP = -3          /* the HIP runtime reported an error at launch */
+} roi_status;
+
+/*
+ * roi_mask_fwd -- one forward sample of the n:m mask for every group.
+ *
+ * §3.2 / §4.2.2: keys kappa = phi/lambda + g; hard selection = the n largest
+ * keys of each group (ties go to the lower index; -0.0 and +0.0 tie).
+ * §4.1: W_masked = W (.) hard mask (pruned entries are +0.0, bits 0x0000).
+ * §3.2 recursion / Algorithm 1: soft_mask S = sum_{k=1..n} mu^(k) with
+ * alpha^(1) = kappa, mu^(k) = softmax(alpha^(k) / tau),
+ * alpha^(k+1) = alpha^(k) + log(1 - mu^(k)), computed in fp32 (log(1 - mu) is
+ * floored at log(FLT_MIN)).
+ *
+ *  W          bf16 [rows, cols]          frozen weights (read)
+ *  logits     fp32 [rows, cols]          phi (read)
+ *  rows, cols sizes, rows >= 0, cols >= 0, cols % m == 0, rows * cols < 2^62
+ *  n, m       keep n of every m; m in {4, 8}, 1 <= n <= m
+ *  tau        relaxation temperature, finite, > 0 (used only for soft_mask)
+ *  lambda     sampling temperature, finite, > 0 (§4.2.3)
+ *  seed, step Philox key and step counter
+ *  elem_offset global index of element 0; elem_offset % 4 == 0
+ *  W_masked   bf16 [rows, cols]          (written; required)
+ *  soft_mask  fp32 [rows, cols] or NULL  (written when not NULL)
+ *  sel_idx    uint8 [rows*cols/m, n] or NULL: the kept indices of each group in
+ *             selection order (descending key)   (written when not NULL)
+ */
+int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows, int64_t cols, int n,
+                 int m, float tau, float lambda, uint64_t seed, uint64_t step,
+                 uint64_t elem_offset, uint16_t* W_masked, float* soft_mask, uint8_t* sel_idx,
+                 hipStream_t stream);
+
+/*
+ * roi_mask_bwd -- dL/dlogits from dL/dW_masked.
+ *
+ * Straight-through (Appendix, Comparison with Straight-Through Gumbel-Top-K):
+ * the forward value is the hard mask, the backward goes through the
+ * relaxation as if W_masked = W (.) S.  So dL/dS = grad_W_masked (.) W (exact
+ * in fp32), dL/dkappa is the reverse-mode derivative of the §3.2 recursion,
+ * and dL/dphi = dL/dkappa / lambda.  The keys are regenerated from
+ * (seed, step, elem_offset) and must match the forward call's arguments.
+ *
+ *  grad_W_masked bf16 [rows, cols]       (read)
+ *  W, logits, rows, cols, n, m, tau, lambda, seed, step, elem_offset: as in
+ *             roi_mask_fwd
+ *  grad_logits fp32 [rows, cols]         (overwritten)
+ */
+int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
+                 int64_t rows, int64_t cols, int n, int m, float tau, float lambda, uint64_t seed,
+                 uint64_t step, uint64_t elem_offset, float* grad_logits, hipStream_t stream);
+
+/*
+ * roi_gumbel_noise -- the noise of `count` consecutive elements starting at
+ * global index elem_offset (elem_offset % 4 == 0): the raw Philox words
+ * and/or g = -L(-L(u)) (Algorithm 1).  Either output may be NULL, not both.
+ *  words  uint32 [count] or NULL; gumbel fp32 [count] or NULL
+ */
+int roi_gumbel_noise(uint64_t seed, uint64_t step, uint64_t elem_offset, int64_t count,
+                     uint32_t* words, float* gumbel, hipStream_t stream);
+
+/*
+ * roi_gumbel_from_words -- g = -L(-L(u(x))) for caller-given 32-bit words x
+ * (Algorithm 1 applied to explicit uniforms; exposes the deterministic noise
+ * transform on its own).  words uint32 [count] (read), gumbel fp32 [count]
+ * (written).
+ */
+int roi_gumbel_from_words(const uint32_t* words, int64_t count, float* gumbel,
+                          hipStream_t stream);
+
+/*
+ * roi_anneal -- §4.2.3 exponential annealing, host-side:
+ * v_t = max{ v_end, v_init (v_end / v_init)^(t / t_anneal) }, evaluated in
+ * fp64 and rounded to fp32.  Requires v_init > 0, v_end > 0, t >= 0,
+ * t_anneal > 0; returns NaN otherwise.
+ */
+float roi_anneal(float v_init, float v_end, int64_t t, int64_t t_anneal);
+
+/* Static description of a status code. */
+const char* roi_status_string(int status);
+/* Thread-local detail of the last failed call on this thread ("" if none). */
+const char* roi_last_error(void);
+/* ABI version, currently 1. */
+int roi_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ROI_H */

@@ -1,0 +1,170 @@
+"""MI355X (gfx950) RoI differentiable N:M mask sampler.
+
+Thin ctypes binding of ``libroi.so`` (declared in ``include/roi.h``): argument
+marshalling only.  Every step of the sampler runs in the HIP kernels; torch is
+used for device memory and the current stream.  If the library has not been
+built, every call raises -- there is no other implementation behind it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libroi.so")
+
+ROI_OK = 0
+ROI_E_INVAL = -1
+ROI_E_UNSUPPORTED = -2
+ROI_E_HIP = -3
+
+SUPPORTED_M = (4, 8)
+
+
+class RoiError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{detail} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+_vp = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_u64 = ctypes.c_uint64
+_int = ctypes.c_int
+_f32 = ctypes.c_float
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libroi.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_23048_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.roi_mask_fwd.argtypes = [_vp, _vp, _i64, _i64, _int, _int, _f32, _f32, _u64, _u64, _u64,
+                                   _vp, _vp, _vp, _vp]
+        L.roi_mask_fwd.restype = _int
+        L.roi_mask_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _int, _int, _f32, _f32, _u64, _u64,
+                                   _u64, _vp, _vp]
+        L.roi_mask_bwd.restype = _int
+        L.roi_gumbel_noise.argtypes = [_u64, _u64, _u64, _i64, _vp, _vp, _vp]
+        L.roi_gumbel_noise.restype = _int
+        L.roi_gumbel_from_words.argtypes = [_vp, _i64, _vp, _vp]
+        L.roi_gumbel_from_words.restype = _int
+        L.roi_anneal.argtypes = [_f32, _f32, _i64, _i64]
+        L.roi_anneal.restype = _f32
+        L.roi_status_string.argtypes = [_int]
+        L.roi_status_string.restype = ctypes.c_char_p
+        L.roi_last_error.argtypes = []
+        L.roi_last_error.restype = ctypes.c_char_p
+        L.roi_abi_version.argtypes = []
+        L.roi_abi_version.restype = _int
+        _lib = L
+    return _lib
+
+
+def _raise_on(status: int):
+    if status != ROI_OK:
+        raise RoiError(status, lib().roi_last_error().decode() or
+                       lib().roi_status_string(status).decode())
+
+
+def _stream(t) -> int:
+    import torch
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _shape2d(t) -> tuple[int, int]:
+    if t.dim() == 2:
+        return int(t.shape[0]), int(t.shape[1])
+    return 1, int(t.numel())
+
+
+def _check_tensor(t, dtype, name, like=None):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if like is not None and t.shape != like.shape:
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(like.shape)}")
+
+
+# --------------------------------------------------------------------------- tensor API
+def mask_fwd(W, logits, n: int, m: int, tau: float = 1.0, lam: float = 1.0, seed: int = 0,
+             step: int = 0, elem_offset: int = 0, want_soft: bool = False, want_idx: bool = True,
+             out: dict | None = None):
+    """Forward sample.  W: bf16 [rows, cols] (or 1-D), logits: fp32 same shape.
+
+    Returns (W_masked bf16, soft_mask fp32 or None, sel_idx uint8 [groups, n] or
+    None).  ``out`` may hold preallocated "W_masked", "soft_mask", "sel_idx".
+    """
+    import torch
+    _check_tensor(W, torch.bfloat16, "W")
+    _check_tensor(logits, torch.float32, "logits", like=W)
+    rows, cols = _shape2d(W)
+    out = out or {}
+    Wm = out.get("W_masked")
+    if Wm is None:
+        Wm = torch.empty_like(W)
+    S = out.get("soft_mask") if want_soft else None
+    if want_soft and S is None:
+        S = torch.empty_like(logits)
+    idx = out.get("sel_idx") if want_idx else None
+    if want_idx and idx is None:
+        idx = torch.empty((W.numel() // m if m > 0 else 0, n), dtype=torch.uint8, device=W.device)
+    st = lib().roi_mask_fwd(_ptr(W), _ptr(logits), rows, cols, n, m, tau, lam, seed, step,
+                            elem_offset, _ptr(Wm), _ptr(S), _ptr(idx), _stream(W))
+    _raise_on(st)
+    return Wm, S, idx
+
+
+def mask_bwd(grad_W_masked, W, logits, n: int, m: int, tau: float = 1.0, lam: float = 1.0,
+             seed: int = 0, step: int = 0, elem_offset: int = 0, out=None):
+    """dL/dlogits (fp32, same shape as logits) from dL/dW_masked (bf16)."""
+    import torch
+    _check_tensor(grad_W_masked, torch.bfloat16, "grad_W_masked")
+    _check_tensor(W, torch.bfloat16, "W", like=grad_W_masked)
+    _check_tensor(logits, torch.float32, "logits", like=grad_W_masked)
+    rows, cols = _shape2d(W)
+    d = out if out is not None else torch.empty_like(logits)
+    st = lib().roi_mask_bwd(_ptr(grad_W_masked), _ptr(W), _ptr(logits), rows, cols, n, m, tau, lam,
+                            seed, step, elem_offset, _ptr(d), _stream(W))
+    _raise_on(st)
+    return d
+
+
+def gumbel_noise(count: int, seed: int = 0, step: int = 0, elem_offset: int = 0, device="cuda",
+                 want_words: bool = True, want_gumbel: bool = True):
+    """Raw Philox words (as int32 bit patterns) and Gumbel noise of `count` elements."""
+    import torch
+    words = torch.empty(count, dtype=torch.int32, device=device) if want_words else None
+    g = torch.empty(count, dtype=torch.float32, device=device) if want_gumbel else None
+    ref = words if words is not None else g
+    st = lib().roi_gumbel_noise(seed, step, elem_offset, count, _ptr(words), _ptr(g), _stream(ref))
+    _raise_on(st)
+    return words, g
+
+
+def gumbel_from_words(words):
+    """g = -L(-L(u(x))) for int32 tensors holding 32-bit words."""
+    import torch
+    _check_tensor(words, torch.int32, "words")
+    g = torch.empty(words.shape, dtype=torch.float32, device=words.device)
+    _raise_on(lib().roi_gumbel_from_words(_ptr(words), words.numel(), _ptr(g), _stream(words)))
+    return g
+
+
+def anneal(v_init: float, v_end: float, t: int, t_anneal: int) -> float:
+    """§4.2.3 exponential annealing of a temperature (host-side)."""
+    return float(lib().roi_anneal(v_init, v_end, t, t_anneal))

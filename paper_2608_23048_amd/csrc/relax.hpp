@@ -1,0 +1,157 @@
+// relax.hpp -- per-group hard top-n, Gumbel-Top-K relaxation and its reverse
+// sweep, on register arrays of one group (m keys held by one lane).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace roi {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kFltMin = 1.17549435e-38f;
+
+// Hard Gumbel-Top-K (§3.2): rank_j = number of keys that beat key j, where
+// i beats j when kappa_i > kappa_j, or kappa_i == kappa_j and i < j.  The n
+// keys of rank < n are kept; rank is also the selection order.
+template <int M>
+__device__ __forceinline__ void rank_keys(const float (&kappa)[M], int (&rank)[M])
+{
+#pragma unroll
+    for (int j = 0; j < M; ++j) rank[j] = 0;
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+#pragma unroll
+        for (int j = i + 1; j < M; ++j) {
+            const bool i_wins = kappa[i] >= kappa[j];
+            rank[j] += i_wins ? 1 : 0;
+            rank[i] += i_wins ? 0 : 1;
+        }
+    }
+}
+
+// One record per relaxation step, kept for the reverse sweep.
+template <int M>
+struct StepRec {
+    float mu[M];     // mu^(k)
+    float om_star;   // 1 - mu^(k)_{i*}, evaluated as the sum of the others
+    int istar;       // index of the largest adjusted key at step k
+};
+
+// Relaxation (§3.2 recursion, Algorithm 1) in fp32:
+//   alpha^(1) = kappa; mu^(k) = softmax(alpha^(k) / tau);
+//   alpha^(k+1) = alpha^(k) + log(1 - mu^(k));  S = sum_k mu^(k).
+// Internally a = (alpha - max kappa) * log2(e), so the softmax is
+// exp2((a - max a) / tau) and the update is a += log2(1 - mu) (same values,
+// one multiply fewer per step).  Subtracting the group's largest key first
+// keeps the competing entries near 0, where fp32 is densest.
+// 1 - mu_i: for i != i* it is >= 1/2 and 1 - mu_i is exact to rounding; for
+// the current argmax i* it is rest / T with rest = sum of the other
+// exponentials (no cancellation).  log(1 - mu) is floored at log(FLT_MIN).
+template <int M, int N, bool kWantS, bool kKeep>
+__device__ __forceinline__ void relax_forward(const float (&kappa)[M], float inv_tau,
+                                              float (&S)[M], StepRec<M> (&rec)[N])
+{
+    float kmax = kappa[0];
+#pragma unroll
+    for (int j = 1; j < M; ++j) kmax = fmaxf(kmax, kappa[j]);
+    float a[M];
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+        a[j] = (kappa[j] - kmax) * kLog2e;
+        if (kWantS) S[j] = 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        float amax = a[0];
+        int istar = 0;
+#pragma unroll
+        for (int j = 1; j < M; ++j) {
+            const bool gt = a[j] > amax;
+            amax = gt ? a[j] : amax;
+            istar = gt ? j : istar;
+        }
+        float e[M];
+        float rest = 0.0f;
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+            e[j] = __builtin_amdgcn_exp2f((a[j] - amax) * inv_tau); // e[istar] == 1 exactly
+            rest += (j == istar) ? 0.0f : e[j];
+        }
+        const float inv_total = __builtin_amdgcn_rcpf(1.0f + rest);
+        const float om_star = rest * inv_total;
+        float mu[M];
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+            mu[j] = e[j] * inv_total;
+            if (kWantS) S[j] += mu[j];
+            if (kKeep) rec[k].mu[j] = mu[j];
+        }
+        if (kKeep) {
+            rec[k].om_star = om_star;
+            rec[k].istar = istar;
+        }
+        if (k + 1 < N) {
+#pragma unroll
+            for (int j = 0; j < M; ++j) {
+                float om = (j == istar) ? om_star : 1.0f - mu[j];
+                om = fmaxf(om, kFltMin);
+                a[j] += __builtin_amdgcn_logf(om);
+            }
+        }
+    }
+}
+
+// Reverse sweep of relax_forward: given sbar = dL/dS, returns dL/dkappa.
+// Chain rule through the recursion, with a = dL/dalpha^(k+1) (0 above the
+// last step), omega = 1 - mu^(k):
+//   mubar_i = sbar_i - a_i / omega_i          (0 instead where the floor was hit)
+//   dL/dalpha^(k)_i = a_i + (mu_i / tau) (mubar_i - sum_j mu_j mubar_j).
+// For i != i* this is evaluated as written (mu_i <= 1/2, omega_i >= 1/2).  For
+// i* the product mu_i* * (...) may cancel catastrophically when mu_i* ~ 1, so
+// the identity omega_i* mubar_i* = omega_i* sbar_i* - a_i* is used:
+//   dL/dalpha^(k)_i* = a_i* (omega* + tau - 1) / tau
+//                      + (mu_i* / tau) (omega* sbar_i* - sum_{j != i*} mu_j mubar_j).
+template <int M, int N>
+__device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const float (&sbar)[M],
+                                               float tau, float inv_tau, float (&abar)[M])
+{
+#pragma unroll
+    for (int j = 0; j < M; ++j) abar[j] = 0.0f;
+#pragma unroll
+    for (int k = N - 1; k >= 0; --k) {
+        const bool has_next = (k + 1 < N);
+        const int istar = rec[k].istar;
+        const float oms = rec[k].om_star;
+        const bool floored = !(oms >= kFltMin);
+        float mubar[M];
+        float p_excl = 0.0f;
+        float mu_is = 0.0f, mub_is = 0.0f;
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+            const bool is = (j == istar);
+            const float mu = rec[k].mu[j];
+            float r = 0.0f;
+            if (has_next) {
+                const float om = is ? oms : 1.0f - mu;
+                const bool live = !(is && floored);
+                r = live ? abar[j] * __builtin_amdgcn_rcpf(om) : 0.0f;
+            }
+            mubar[j] = sbar[j] - r;
+            p_excl += is ? 0.0f : mu * mubar[j];
+            mu_is = is ? mu : mu_is;
+            mub_is = is ? mubar[j] : mub_is;
+        }
+        const float p_all = p_excl + mu_is * mub_is;
+        const float keep = floored ? 1.0f : (oms + (tau - 1.0f)) * inv_tau;
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+            const bool is = (j == istar);
+            const float mu = rec[k].mu[j];
+            const float carried = has_next ? abar[j] * (is ? keep : 1.0f) : 0.0f;
+            const float inner = is ? (oms * sbar[j] - p_excl) : (mubar[j] - p_all);
+            abar[j] = carried + (mu * inv_tau) * inner;
+        }
+    }
+}
+
+} // namespace roi

@@ -1,0 +1,539 @@
+// roi.hip -- gfx950 kernels and the C ABI of the RoI N:M mask sampler.
+//
+// Work decomposition: one group of m consecutive weights per lane.  A wave of
+// 64 lanes covers 64 consecutive groups, so each load and store instruction of
+// a wave touches one contiguous span (64 * 16 B of logits, 64 * 2m B of bf16
+// weights); blocks walk the tensor in a grid-stride loop.  Everything a group
+// needs stays in registers: the Philox words, the keys, the ranks and, in the
+// backward, the n softmax records of the relaxation.  The path is a stream of
+// elementwise work with per-group reductions, so it is bound by HBM bandwidth
+// or VALU issue, never by a dense contraction; there is no MFMA here.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <utility>
+
+#include "noise.hpp"
+#include "relax.hpp"
+#include "roi.h"
+
+namespace roi {
+namespace {
+
+constexpr int kBlock = 256;
+
+struct FwdArgs {
+    const uint16_t* W;
+    const float* phi;
+    uint16_t* Wm;
+    float* S;
+    uint8_t* idx;
+    int64_t ngroups;
+    uint64_t block0; // elem_offset / 4
+    NoiseKey key;
+    float lambda;
+    float inv_tau;
+};
+
+struct BwdArgs {
+    const uint16_t* G;
+    const uint16_t* W;
+    const float* phi;
+    float* dphi;
+    int64_t ngroups;
+    uint64_t block0;
+    NoiseKey key;
+    float lambda;
+    float inv_lambda;
+    float tau;
+    float inv_tau;
+};
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t b) { return __uint_as_float(b << 16); }
+
+// Loads of one group: m fp32 logits (m/4 16-byte loads) and m bf16 values
+// (one 8-byte load for m = 4, one 16-byte load for m = 8).
+template <int M>
+__device__ __forceinline__ void load_logits(const float* p, float (&phi)[M])
+{
+    const f32x4* p4 = reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+    for (int t = 0; t < M / 4; ++t) {
+        const f32x4 v = __builtin_nontemporal_load(p4 + t);
+        phi[4 * t + 0] = v.x;
+        phi[4 * t + 1] = v.y;
+        phi[4 * t + 2] = v.z;
+        phi[4 * t + 3] = v.w;
+    }
+}
+
+template <int M>
+__device__ __forceinline__ void load_bf16(const uint16_t* p, uint32_t (&w)[M])
+{
+    if constexpr (M == 4) {
+        const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+        w[0] = v.x & 0xFFFFu; w[1] = v.x >> 16; w[2] = v.y & 0xFFFFu; w[3] = v.y >> 16;
+    } else {
+        static_assert(M == 8, "m");
+        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+        w[0] = v.x & 0xFFFFu; w[1] = v.x >> 16; w[2] = v.y & 0xFFFFu; w[3] = v.y >> 16;
+        w[4] = v.z & 0xFFFFu; w[5] = v.z >> 16; w[6] = v.w & 0xFFFFu; w[7] = v.w >> 16;
+    }
+}
+
+// Masked bf16 weights: the kept value, or +0.0 (bits 0x0000).
+template <int M>
+__device__ __forceinline__ void store_masked(uint16_t* p, const uint32_t (&w)[M], const int (&rank)[M],
+                                             int n)
+{
+    uint32_t packed[M / 2];
+#pragma unroll
+    for (int t = 0; t < M / 2; ++t) {
+        const uint32_t lo = rank[2 * t] < n ? w[2 * t] : 0u;
+        const uint32_t hi = rank[2 * t + 1] < n ? w[2 * t + 1] : 0u;
+        packed[t] = lo | (hi << 16);
+    }
+    if constexpr (M == 4) {
+        const u32x2 v = {packed[0], packed[1]};
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x2*>(p));
+    } else {
+        const u32x4 v = {packed[0], packed[1], packed[2], packed[3]};
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+    }
+}
+
+// Selected indices in selection order: byte r holds the index of rank r.
+template <int M, int N>
+__device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
+{
+    uint64_t packed = 0;
+#pragma unroll
+    for (int j = 0; j < M; ++j)
+        packed |= (rank[j] < N) ? ((uint64_t)j << (8 * rank[j])) : 0ull;
+    if constexpr (N == 1) {
+        *p = (uint8_t)packed;
+    } else if constexpr (N == 2) {
+        *reinterpret_cast<uint16_t*>(p) = (uint16_t)packed;
+    } else if constexpr (N == 4) {
+        *reinterpret_cast<uint32_t*>(p) = (uint32_t)packed;
+    } else if constexpr (N == 8) {
+        *reinterpret_cast<uint64_t*>(p) = packed;
+    } else {
+#pragma unroll
+        for (int r = 0; r < N; ++r) p[r] = (uint8_t)(packed >> (8 * r));
+    }
+}
+
+template <int M, bool kLambdaOne>
+__device__ __forceinline__ void group_keys(const float (&phi)[M], uint64_t block, const NoiseKey& key,
+                                           float lambda, float (&kappa)[M])
+{
+#pragma unroll
+    for (int t = 0; t < M / 4; ++t) {
+        const uint4 x = philox_block(block + t, key);
+        kappa[4 * t + 0] = key_of<kLambdaOne>(phi[4 * t + 0], lambda, x.x);
+        kappa[4 * t + 1] = key_of<kLambdaOne>(phi[4 * t + 1], lambda, x.y);
+        kappa[4 * t + 2] = key_of<kLambdaOne>(phi[4 * t + 2], lambda, x.z);
+        kappa[4 * t + 3] = key_of<kLambdaOne>(phi[4 * t + 3], lambda, x.w);
+    }
+}
+
+template <int M, int N, bool kWantS, bool kWantIdx, bool kLambdaOne>
+__global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
+{
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
+        const int64_t base = q * M;
+        float phi[M];
+        uint32_t w[M];
+        load_logits<M>(a.phi + base, phi);
+        load_bf16<M>(a.W + base, w);
+        float kappa[M];
+        group_keys<M, kLambdaOne>(phi, a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda, kappa);
+        int rank[M];
+        rank_keys<M>(kappa, rank);
+        store_masked<M>(a.Wm + base, w, rank, N);
+        if (kWantIdx) store_idx<M, N>(a.idx + q * N, rank);
+        if (kWantS) {
+            float S[M];
+            StepRec<M> unused[N]; // not written when records are not kept
+            relax_forward<M, N, true, false>(kappa, a.inv_tau, S, unused);
+            f32x4* s4 = reinterpret_cast<f32x4*>(a.S + base);
+#pragma unroll
+            for (int t = 0; t < M / 4; ++t) {
+                const f32x4 v = {S[4 * t], S[4 * t + 1], S[4 * t + 2], S[4 * t + 3]};
+                __builtin_nontemporal_store(v, s4 + t);
+            }
+        }
+    }
+}
+
+template <int M, int N, bool kLambdaOne>
+__global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
+{
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
+        const int64_t base = q * M;
+        float phi[M];
+        uint32_t w[M], g[M];
+        load_logits<M>(a.phi + base, phi);
+        load_bf16<M>(a.W + base, w);
+        load_bf16<M>(a.G + base, g);
+        float kappa[M];
+        group_keys<M, kLambdaOne>(phi, a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda, kappa);
+        // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
+        float sbar[M];
+#pragma unroll
+        for (int j = 0; j < M; ++j) sbar[j] = bf16_bits_to_float(g[j]) * bf16_bits_to_float(w[j]);
+        StepRec<M> rec[N];
+        float S_unused[M];
+        relax_forward<M, N, false, true>(kappa, a.inv_tau, S_unused, rec);
+        float abar[M];
+        relax_backward<M, N>(rec, sbar, a.tau, a.inv_tau, abar);
+        f32x4* d4 = reinterpret_cast<f32x4*>(a.dphi + base);
+#pragma unroll
+        for (int t = 0; t < M / 4; ++t) {
+            f32x4 v;
+            v.x = kLambdaOne ? abar[4 * t + 0] : abar[4 * t + 0] * a.inv_lambda;
+            v.y = kLambdaOne ? abar[4 * t + 1] : abar[4 * t + 1] * a.inv_lambda;
+            v.z = kLambdaOne ? abar[4 * t + 2] : abar[4 * t + 2] * a.inv_lambda;
+            v.w = kLambdaOne ? abar[4 * t + 3] : abar[4 * t + 3] * a.inv_lambda;
+            __builtin_nontemporal_store(v, d4 + t);
+        }
+    }
+}
+
+// Noise inspection: one Philox call per 4 consecutive elements.
+__global__ __launch_bounds__(kBlock) void noise_kernel(uint32_t* words, float* gum, int64_t count,
+                                                       uint64_t block0, NoiseKey key)
+{
+    const int64_t nblocks = (count + 3) / 4;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t b = (int64_t)blockIdx.x * kBlock + threadIdx.x; b < nblocks; b += stride) {
+        const uint4 x = philox_block(block0 + (uint64_t)b, key);
+        const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int64_t e = 4 * b + t;
+            if (e < count) {
+                if (words) words[e] = xs[t];
+                if (gum) gum[e] = gumbel_from_word(xs[t]);
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void gumbel_words_kernel(const uint32_t* words, float* gum,
+                                                              int64_t count)
+{
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride)
+        gum[i] = gumbel_from_word(words[i]);
+}
+
+// ----------------------------------------------------------------------------- host side
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return status;
+}
+
+int ok()
+{
+    g_last_error.clear();
+    return ROI_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb)
+{
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// Grid for a grid-stride loop over `items` work items of one thread each:
+// enough blocks to cover the items, capped at a few waves of blocks per CU.
+int grid_for(int64_t items)
+{
+    static thread_local int cap_dev = -1, cap = 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    if (dev != cap_dev) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+        cap = cus * 16;
+        cap_dev = dev;
+    }
+    const int64_t need = (items + kBlock - 1) / kBlock;
+    return (int)(need < cap ? (need > 0 ? need : 1) : cap);
+}
+
+struct Shape {
+    int64_t numel = 0;
+    int64_t ngroups = 0;
+};
+
+int check_shape(int64_t rows, int64_t cols, int n, int m, float tau, float lambda,
+                uint64_t elem_offset, Shape* sh)
+{
+    if (rows < 0 || cols < 0) return fail(ROI_E_INVAL, "rows (%lld) and cols (%lld) must be >= 0",
+                                          (long long)rows, (long long)cols);
+    if (m < 1 || n < 1 || n > m)
+        return fail(ROI_E_INVAL, "pattern n:m = %d:%d needs 1 <= n <= m", n, m);
+    if (m != 4 && m != 8)
+        return fail(ROI_E_UNSUPPORTED, "m = %d is not built (supported: 4, 8)", m);
+    if (cols % m != 0) return fail(ROI_E_INVAL, "cols (%lld) must be a multiple of m (%d)",
+                                   (long long)cols, m);
+    if (rows > 0 && cols > ((int64_t)1 << 62) / rows)
+        return fail(ROI_E_INVAL, "rows * cols must be below 2^62");
+    if (!(tau > 0.0f) || !std::isfinite(tau))
+        return fail(ROI_E_INVAL, "tau must be finite and > 0");
+    if (!(lambda > 0.0f) || !std::isfinite(lambda))
+        return fail(ROI_E_INVAL, "lambda must be finite and > 0");
+    if (elem_offset % 4 != 0)
+        return fail(ROI_E_INVAL, "elem_offset (%llu) must be a multiple of 4",
+                    (unsigned long long)elem_offset);
+    const int64_t numel = rows * cols;
+    if (elem_offset > UINT64_MAX - (uint64_t)numel)
+        return fail(ROI_E_INVAL, "elem_offset + rows * cols overflows 64 bits");
+    sh->numel = numel;
+    sh->ngroups = numel / m;
+    return ROI_OK;
+}
+
+NoiseKey make_key(uint64_t seed, uint64_t step)
+{
+    NoiseKey k;
+    k.k0 = (uint32_t)seed;
+    k.k1 = (uint32_t)(seed >> 32);
+    k.step_lo = (uint32_t)step;
+    k.step_hi = (uint32_t)(step >> 32);
+    return k;
+}
+
+int launch_status(const char* what)
+{
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(ROI_E_HIP, "%s: launch failed: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+// ---- dispatch tables over (m, n) and the boolean variants
+using FwdFn = void (*)(FwdArgs);
+using BwdFn = void (*)(BwdArgs);
+
+template <int M, int N>
+FwdFn pick_fwd(bool want_s, bool want_idx, bool lam1)
+{
+#define ROI_FWD(S, I, L) \
+    if (want_s == S && want_idx == I && lam1 == L) return fwd_lane_kernel<M, N, S, I, L>;
+    ROI_FWD(false, false, false) ROI_FWD(false, false, true) ROI_FWD(false, true, false)
+    ROI_FWD(false, true, true) ROI_FWD(true, false, false) ROI_FWD(true, false, true)
+    ROI_FWD(true, true, false) ROI_FWD(true, true, true)
+#undef ROI_FWD
+    return nullptr;
+}
+
+template <int M, int N>
+BwdFn pick_bwd(bool lam1)
+{
+    return lam1 ? bwd_lane_kernel<M, N, true> : bwd_lane_kernel<M, N, false>;
+}
+
+template <int M, int... Ns>
+FwdFn fwd_for_n(int n, bool s, bool i, bool l, std::integer_sequence<int, Ns...>)
+{
+    FwdFn f = nullptr;
+    ((n == Ns + 1 ? (f = pick_fwd<M, Ns + 1>(s, i, l), 0) : 0), ...);
+    return f;
+}
+
+template <int M, int... Ns>
+BwdFn bwd_for_n(int n, bool l, std::integer_sequence<int, Ns...>)
+{
+    BwdFn f = nullptr;
+    ((n == Ns + 1 ? (f = pick_bwd<M, Ns + 1>(l), 0) : 0), ...);
+    return f;
+}
+
+FwdFn select_fwd(int m, int n, bool s, bool i, bool l)
+{
+    if (m == 4) return fwd_for_n<4>(n, s, i, l, std::make_integer_sequence<int, 4>{});
+    if (m == 8) return fwd_for_n<8>(n, s, i, l, std::make_integer_sequence<int, 8>{});
+    return nullptr;
+}
+
+BwdFn select_bwd(int m, int n, bool l)
+{
+    if (m == 4) return bwd_for_n<4>(n, l, std::make_integer_sequence<int, 4>{});
+    if (m == 8) return bwd_for_n<8>(n, l, std::make_integer_sequence<int, 8>{});
+    return nullptr;
+}
+
+} // namespace
+} // namespace roi
+
+using namespace roi;
+
+extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows, int64_t cols,
+                            int n, int m, float tau, float lambda, uint64_t seed, uint64_t step,
+                            uint64_t elem_offset, uint16_t* W_masked, float* soft_mask,
+                            uint8_t* sel_idx, hipStream_t stream)
+{
+    Shape sh;
+    if (int st = check_shape(rows, cols, n, m, tau, lambda, elem_offset, &sh)) return st;
+    if (sh.numel == 0) return ok();
+    if (!W || !logits || !W_masked)
+        return fail(ROI_E_INVAL, "W, logits and W_masked must not be NULL");
+    if (!aligned16(W) || !aligned16(logits) || !aligned16(W_masked) ||
+        (soft_mask && !aligned16(soft_mask)) || (sel_idx && !aligned16(sel_idx)))
+        return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
+    const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
+    const size_t nbi = (size_t)sh.ngroups * (size_t)n;
+    const void* ins[2] = {W, logits};
+    const size_t in_n[2] = {nb2, nb4};
+    void* outs[3] = {W_masked, soft_mask, sel_idx};
+    const size_t out_n[3] = {nb2, nb4, nbi};
+    for (int i = 0; i < 3; ++i) {
+        for (int j = 0; j < 2; ++j)
+            if (overlap(outs[i], out_n[i], ins[j], in_n[j]))
+                return fail(ROI_E_INVAL, "outputs must not overlap inputs");
+        for (int j = i + 1; j < 3; ++j)
+            if (overlap(outs[i], out_n[i], outs[j], out_n[j]))
+                return fail(ROI_E_INVAL, "outputs must not overlap each other");
+    }
+    FwdFn fn = select_fwd(m, n, soft_mask != nullptr, sel_idx != nullptr, lambda == 1.0f);
+    if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
+    FwdArgs a;
+    a.W = W;
+    a.phi = logits;
+    a.Wm = W_masked;
+    a.S = soft_mask;
+    a.idx = sel_idx;
+    a.ngroups = sh.ngroups;
+    a.block0 = elem_offset / 4;
+    a.key = make_key(seed, step);
+    a.lambda = lambda;
+    a.inv_tau = (float)(1.0 / (double)tau);
+    void* args[] = {&a};
+    if (hipLaunchKernel((const void*)fn, dim3(grid_for(sh.ngroups)), dim3(kBlock), args, 0,
+                        stream) != hipSuccess)
+        return launch_status("roi_mask_fwd");
+    return launch_status("roi_mask_fwd");
+}
+
+extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
+                            int64_t rows, int64_t cols, int n, int m, float tau, float lambda,
+                            uint64_t seed, uint64_t step, uint64_t elem_offset, float* grad_logits,
+                            hipStream_t stream)
+{
+    Shape sh;
+    if (int st = check_shape(rows, cols, n, m, tau, lambda, elem_offset, &sh)) return st;
+    if (sh.numel == 0) return ok();
+    if (!grad_W_masked || !W || !logits || !grad_logits)
+        return fail(ROI_E_INVAL, "grad_W_masked, W, logits and grad_logits must not be NULL");
+    if (!aligned16(grad_W_masked) || !aligned16(W) || !aligned16(logits) || !aligned16(grad_logits))
+        return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
+    const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
+    if (overlap(grad_logits, nb4, grad_W_masked, nb2) || overlap(grad_logits, nb4, W, nb2) ||
+        overlap(grad_logits, nb4, logits, nb4))
+        return fail(ROI_E_INVAL, "grad_logits must not overlap the inputs");
+    BwdFn fn = select_bwd(m, n, lambda == 1.0f);
+    if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
+    BwdArgs a;
+    a.G = grad_W_masked;
+    a.W = W;
+    a.phi = logits;
+    a.dphi = grad_logits;
+    a.ngroups = sh.ngroups;
+    a.block0 = elem_offset / 4;
+    a.key = make_key(seed, step);
+    a.lambda = lambda;
+    a.inv_lambda = (float)(1.0 / (double)lambda);
+    a.tau = tau;
+    a.inv_tau = (float)(1.0 / (double)tau);
+    void* args[] = {&a};
+    if (hipLaunchKernel((const void*)fn, dim3(grid_for(sh.ngroups)), dim3(kBlock), args, 0,
+                        stream) != hipSuccess)
+        return launch_status("roi_mask_bwd");
+    return launch_status("roi_mask_bwd");
+}
+
+extern "C" int roi_gumbel_noise(uint64_t seed, uint64_t step, uint64_t elem_offset, int64_t count,
+                                uint32_t* words, float* gumbel, hipStream_t stream)
+{
+    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
+    if (elem_offset % 4 != 0) return fail(ROI_E_INVAL, "elem_offset must be a multiple of 4");
+    if (count > 0 && elem_offset > UINT64_MAX - (uint64_t)count)
+        return fail(ROI_E_INVAL, "elem_offset + count overflows 64 bits");
+    if (count == 0) return ok();
+    if (!words && !gumbel) return fail(ROI_E_INVAL, "words and gumbel are both NULL");
+    if ((words && !aligned16(words)) || (gumbel && !aligned16(gumbel)))
+        return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
+    if (overlap(words, (size_t)count * 4, gumbel, (size_t)count * 4))
+        return fail(ROI_E_INVAL, "words and gumbel must not overlap");
+    hipLaunchKernelGGL(noise_kernel, dim3(grid_for((count + 3) / 4)), dim3(kBlock), 0, stream,
+                       words, gumbel, count, elem_offset / 4, make_key(seed, step));
+    return launch_status("roi_gumbel_noise");
+}
+
+extern "C" int roi_gumbel_from_words(const uint32_t* words, int64_t count, float* gumbel,
+                                     hipStream_t stream)
+{
+    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
+    if (count == 0) return ok();
+    if (!words || !gumbel) return fail(ROI_E_INVAL, "words and gumbel must not be NULL");
+    if (!aligned16(words) || !aligned16(gumbel))
+        return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
+    if (overlap(words, (size_t)count * 4, gumbel, (size_t)count * 4))
+        return fail(ROI_E_INVAL, "words and gumbel must not overlap");
+    hipLaunchKernelGGL(gumbel_words_kernel, dim3(grid_for(count)), dim3(kBlock), 0, stream, words,
+                       gumbel, count);
+    return launch_status("roi_gumbel_from_words");
+}
+
+extern "C" float roi_anneal(float v_init, float v_end, int64_t t, int64_t t_anneal)
+{
+    if (!(v_init > 0.0f) || !(v_end > 0.0f) || t < 0 || t_anneal <= 0 || !std::isfinite(v_init) ||
+        !std::isfinite(v_end))
+        return NAN;
+    const double vi = v_init, ve = v_end;
+    const double v = vi * std::pow(ve / vi, (double)t / (double)t_anneal);
+    return (float)(v > ve ? v : ve);
+}
+
+extern "C" const char* roi_status_string(int status)
+{
+    switch (status) {
+    case ROI_OK: return "ok";
+    case ROI_E_INVAL: return "invalid argument";
+    case ROI_E_UNSUPPORTED: return "unsupported pattern";
+    case ROI_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+extern "C" const char* roi_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" int roi_abi_version(void) { return 1; }

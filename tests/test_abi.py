@@ -1,0 +1,144 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every entry point that include/roi.h declares, and rejects invalid arguments
+on the host before anything is launched."""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2608_23048_amd as roi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "roi.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(roi_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(roi.LIB_PATH):
+        pytest.fail("libroi.so is not built (run __graft_entry__.build())")
+    return roi.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = header_functions()
+    assert {"roi_mask_fwd", "roi_mask_bwd", "roi_gumbel_noise", "roi_gumbel_from_words",
+            "roi_anneal", "roi_status_string", "roi_last_error", "roi_abi_version"} <= set(names)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_version_and_status_strings(L):
+    assert L.roi_abi_version() == 1
+    for st in (roi.ROI_OK, roi.ROI_E_INVAL, roi.ROI_E_UNSUPPORTED, roi.ROI_E_HIP):
+        assert L.roi_status_string(st)
+    assert L.roi_status_string(12345) == b"unknown status"
+
+
+FAKE = 0x7F0000000000  # 16-byte aligned, never dereferenced: every call below fails validation
+
+
+def fwd(L, **kw):
+    a = dict(W=FAKE, logits=FAKE + (1 << 30), rows=4, cols=8, n=2, m=4, tau=1.0, lam=1.0, seed=0,
+             step=0, off=0, Wm=FAKE + (2 << 30), S=None, idx=None)
+    a.update(kw)
+    return L.roi_mask_fwd(a["W"], a["logits"], a["rows"], a["cols"], a["n"], a["m"], a["tau"],
+                          a["lam"], a["seed"], a["step"], a["off"], a["Wm"], a["S"], a["idx"], None)
+
+
+def bwd(L, **kw):
+    a = dict(G=FAKE, W=FAKE + (1 << 30), logits=FAKE + (2 << 30), rows=4, cols=8, n=2, m=4,
+             tau=1.0, lam=1.0, seed=0, step=0, off=0, d=FAKE + (3 << 30))
+    a.update(kw)
+    return L.roi_mask_bwd(a["G"], a["W"], a["logits"], a["rows"], a["cols"], a["n"], a["m"],
+                          a["tau"], a["lam"], a["seed"], a["step"], a["off"], a["d"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=0), roi.ROI_E_INVAL),
+    (dict(n=5), roi.ROI_E_INVAL),
+    (dict(m=3, n=1, cols=9), roi.ROI_E_UNSUPPORTED),
+    (dict(m=16, n=8, cols=16), roi.ROI_E_UNSUPPORTED),
+    (dict(cols=6), roi.ROI_E_INVAL),
+    (dict(rows=-1), roi.ROI_E_INVAL),
+    (dict(rows=1 << 40, cols=1 << 40), roi.ROI_E_INVAL),
+    (dict(tau=0.0), roi.ROI_E_INVAL),
+    (dict(tau=-1.0), roi.ROI_E_INVAL),
+    (dict(tau=math.inf), roi.ROI_E_INVAL),
+    (dict(tau=math.nan), roi.ROI_E_INVAL),
+    (dict(lam=0.0), roi.ROI_E_INVAL),
+    (dict(lam=math.nan), roi.ROI_E_INVAL),
+    (dict(off=2), roi.ROI_E_INVAL),
+    (dict(off=2**64 - 4), roi.ROI_E_INVAL),
+    (dict(W=None), roi.ROI_E_INVAL),
+    (dict(Wm=None), roi.ROI_E_INVAL),
+    (dict(W=FAKE + 8), roi.ROI_E_INVAL),
+    (dict(S=FAKE + (3 << 30) + 4), roi.ROI_E_INVAL),
+    (dict(Wm=FAKE + 16), roi.ROI_E_INVAL),              # overlaps W
+    (dict(S=FAKE + (1 << 30) + 16), roi.ROI_E_INVAL),   # overlaps logits
+    (dict(idx=FAKE + (2 << 30) + 32), roi.ROI_E_INVAL),  # overlaps W_masked
+])
+def test_fwd_rejects_before_launch(L, kw, status):
+    assert fwd(L, **kw) == status
+    assert L.roi_last_error()
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=0), roi.ROI_E_INVAL),
+    (dict(m=32, n=16, cols=32), roi.ROI_E_UNSUPPORTED),
+    (dict(cols=10), roi.ROI_E_INVAL),
+    (dict(tau=0.0), roi.ROI_E_INVAL),
+    (dict(lam=-2.0), roi.ROI_E_INVAL),
+    (dict(off=6), roi.ROI_E_INVAL),
+    (dict(d=None), roi.ROI_E_INVAL),
+    (dict(G=FAKE + 2), roi.ROI_E_INVAL),
+    (dict(d=FAKE + (2 << 30)), roi.ROI_E_INVAL),  # aliases logits
+])
+def test_bwd_rejects_before_launch(L, kw, status):
+    assert bwd(L, **kw) == status
+
+
+def test_empty_input_is_a_no_op(L):
+    # nothing to do: returns OK without touching the (NULL) pointers or the device
+    assert fwd(L, rows=0, W=None, logits=None, Wm=None) == roi.ROI_OK
+    assert fwd(L, cols=0, W=None, logits=None, Wm=None) == roi.ROI_OK
+    assert bwd(L, rows=0, G=None, W=None, logits=None, d=None) == roi.ROI_OK
+    assert L.roi_gumbel_noise(0, 0, 0, 0, None, None, None) == roi.ROI_OK
+    assert L.roi_gumbel_from_words(None, 0, None, None) == roi.ROI_OK
+
+
+def test_noise_entry_checks(L):
+    assert L.roi_gumbel_noise(0, 0, 2, 16, FAKE, None, None) == roi.ROI_E_INVAL
+    assert L.roi_gumbel_noise(0, 0, 0, 16, None, None, None) == roi.ROI_E_INVAL
+    assert L.roi_gumbel_noise(0, 0, 0, -1, FAKE, None, None) == roi.ROI_E_INVAL
+    assert L.roi_gumbel_noise(0, 0, 0, 16, FAKE, FAKE + 32, None) == roi.ROI_E_INVAL
+    assert L.roi_gumbel_from_words(FAKE, 8, FAKE + 16, None) == roi.ROI_E_INVAL
+    assert L.roi_gumbel_from_words(FAKE + 4, 8, FAKE + 4096, None) == roi.ROI_E_INVAL
+
+
+def test_anneal_matches_oracle(L):
+    """§4.2.3 schedule: the library's host function against the oracle's."""
+    import oracle
+    for (a, b, T) in ((1.0, 0.1, 9), (1.0, 0.05, 1500), (1.0, 0.002, 1500), (0.5, 2.0, 10)):
+        for t in (0, 1, 2, T // 2, T - 1, T, T + 1, 3 * T):
+            ref = oracle.anneal(a, b, t, T)
+            got = roi.anneal(a, b, t, T)
+            assert got == pytest.approx(ref, rel=1e-6), (a, b, T, t)
+    assert math.isnan(roi.anneal(0.0, 0.1, 1, 9))
+    assert math.isnan(roi.anneal(1.0, 0.1, 1, 0))
+    assert math.isnan(roi.anneal(1.0, 0.1, -1, 9))
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(roi, "_lib", None)
+    monkeypatch.setattr(roi, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        roi.lib()

@@ -1,0 +1,286 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Selected indices, hard masks and masked weights must be
+bit-exact; the soft mask and grad_logits must be within 1e-5 relative /
+1e-6 absolute (fp32 against the oracle's fp64)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_23048_amd as roi
+from paper_2608_23048_amd import workloads as wl
+from tests.gpu_helpers import assert_close, bf16_bits, f32, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available()
+    roi.lib()  # raises if the HIP library is missing
+    return torch.device("cuda:0")
+
+
+def run_case(dev, rows, cols, n, m, tau, lam, seed, step, off, case_seed, w_std=wl.W_STD,
+             grad_std=wl.GRAD_STD, logit_std=wl.LOGIT_STD, scale_aware=False):
+    import torch
+    say(f"case rows={rows} cols={cols} {n}:{m} tau={tau} lam={lam} seed={seed} step={step} "
+        f"off={off} case_seed={case_seed}")
+    W, L, G = wl.small_case(rows, cols, case_seed, device=dev, w_std=w_std, logit_std=logit_std,
+                            grad_std=grad_std)
+    Wm, S, idx = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True)
+    d = roi.mask_bwd(G, W, L, n, m, tau, lam, seed, step, off)
+    torch.cuda.synchronize()
+    tau32 = float(np.float32(tau))
+    lam32 = float(np.float32(lam))
+    Wm_o, S_o, idx_o = oracle.mask_fwd(bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
+    d_o = oracle.mask_bwd(bf16_bits(G), bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
+    assert np.array_equal(idx.cpu().numpy(), idx_o), "selected indices differ"
+    assert np.array_equal(bf16_bits(Wm).reshape(-1), Wm_o), "masked weights differ"
+    rs = assert_close(f32(S), S_o, "soft mask")
+    rd = assert_close(f32(d), d_o, "grad_logits", scale_aware=scale_aware)
+    say(f"  ok: soft-mask err/bound {rs:.3f}, grad err/bound {rd:.3f}")
+
+
+# --------------------------------------------------------------------------- noise
+def test_noise_words_and_gumbel_bit_exact(dev):
+    import torch
+    for seed, step, off, count in [(0, 0, 0, (1 << 20) + 3), (0xDEADBEEF12345678, 7, 1 << 34, 4099),
+                                   (1, 2**40 + 3, 6525288448 - 4096, 4096)]:
+        say(f"noise seed={seed} step={step} off={off} count={count}")
+        words, g = roi.gumbel_noise(count, seed, step, off, device=dev)
+        torch.cuda.synchronize()
+        w = words.cpu().numpy().view(np.uint32)
+        pick = np.unique(np.r_[np.arange(min(count, 2048)), np.arange(count - 7, count),
+                               np.random.default_rng(seed % 1000).integers(0, count, 2000)])
+        ref_w = np.array([oracle.philox_word(seed, step, off + int(i)) for i in pick], np.uint32)
+        assert np.array_equal(w[pick], ref_w)
+        ref_g = oracle.gumbel_from_words(w)
+        assert np.array_equal(g.cpu().numpy().view(np.uint32), ref_g.view(np.uint32))
+
+
+def test_gumbel_exhaustive_uniform_grid(dev):
+    """All 2^23 uniforms of the grid (and random full words): bit-exact noise."""
+    import torch
+    say("gumbel grid 2^23")
+    k = np.arange(1 << 23, dtype=np.uint32)
+    rnd = np.random.default_rng(5).integers(0, 2**32, 1 << 20, dtype=np.uint64).astype(np.uint32)
+    words = np.concatenate([k << np.uint32(9), (k << np.uint32(9)) | np.uint32(0x1FF), rnd])
+    t = torch.from_numpy(words.view(np.int32)).to(dev)
+    g = roi.gumbel_from_words(t)
+    torch.cuda.synchronize()
+    ref = oracle.gumbel_from_words(words)
+    got = g.cpu().numpy()
+    bad = np.flatnonzero(got.view(np.uint32) != ref.view(np.uint32))
+    assert bad.size == 0, f"{bad.size} mismatches, first word {words[bad[0]]:#x}: " \
+                          f"{got[bad[0]]!r} vs {ref[bad[0]]!r}"
+
+
+# --------------------------------------------------------------------------- small cases
+SMALL = [
+    # rows, cols, n, m, tau, lam, seed, step, off
+    (1, 4, 2, 4, 1.0, 1.0, 0, 0, 0),
+    (37, 36, 2, 4, 1.0, 1.0, 3, 1, 0),           # 333 groups: ragged tail
+    (64, 256, 2, 4, 0.5, 1.0, 11, 2, 4096),
+    (130, 200, 2, 4, 0.1, 1.0, 5, 9, 8),
+    (33, 64, 1, 4, 0.7, 1.0, 1, 0, 0),
+    (33, 64, 3, 4, 1.3, 0.6, 2, 3, 12),
+    (33, 64, 4, 4, 1.0, 1.0, 2, 3, 0),
+    (48, 96, 4, 8, 0.5, 1.0, 7, 4, 0),
+    (61, 88, 2, 8, 1.0, 2.0, 8, 5, 4),
+    (61, 88, 1, 8, 0.3, 1.0, 8, 5, 4),
+    (61, 88, 7, 8, 1.0, 1.0, 8, 5, 4),
+    (61, 88, 8, 8, 0.9, 1.0, 9, 6, 0),
+    (17, 8, 6, 8, 0.25, 0.5, 4, 2**33, 2**36),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: "x".join(map(str, c[:4])))
+def test_small_config_scale(dev, case):
+    rows, cols, n, m, tau, lam, seed, step, off = case
+    run_case(dev, rows, cols, n, m, tau, lam, seed, step, off, case_seed=rows * 1000 + cols)
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: "x".join(map(str, c[:4])))
+def test_small_unit_scale(dev, case):
+    """Unit-scale W and upstream gradients: grad_logits of order 1, so the
+    absolute 1e-6 term is scaled by the largest |oracle| value instead."""
+    rows, cols, n, m, tau, lam, seed, step, off = case
+    run_case(dev, rows, cols, n, m, tau, lam, seed, step, off, case_seed=7 + rows * cols,
+             w_std=1.0, grad_std=1.0, logit_std=2.0, scale_aware=True)
+
+
+def test_single_layer_896(dev):
+    """One 896x896 linear layer, 2:4, tau = 1, seed 0, step 0: every output."""
+    run_case(dev, 896, 896, 2, 4, 1.0, 1.0, 0, 0, 0, case_seed=0)
+
+
+# --------------------------------------------------------------------------- ties
+def test_ties_go_to_lowest_index(dev):
+    """Logits equal to minus the noise make every key exactly +0.0: all keys
+    tie and the kept entries are the lowest indices, in index order."""
+    import torch
+    for n, m in ((2, 4), (3, 8), (1, 4), (5, 8)):
+        say(f"ties {n}:{m}")
+        rows, cols, seed, step = 16, 64, 21, 4
+        _, g = roi.gumbel_noise(rows * cols, seed, step, 0, device=dev, want_words=False)
+        L = (-g).reshape(rows, cols).contiguous()
+        # half of the groups: raise the last two entries so they win, in index order
+        L2 = L.clone()
+        L2.view(-1, m)[::2, m - 2:] += 1.0
+        W = torch.randn(rows, cols, device=dev).to(torch.bfloat16)
+        for logits in (L, L2):
+            Wm, S, idx = roi.mask_fwd(W, logits, n, m, 1.0, 1.0, seed, step, 0, want_soft=True)
+            torch.cuda.synchronize()
+            Wm_o, S_o, idx_o = oracle.mask_fwd(bf16_bits(W), f32(logits), n, m, 1.0, 1.0, seed,
+                                               step, 0)
+            assert np.array_equal(idx.cpu().numpy(), idx_o)
+            assert np.array_equal(bf16_bits(Wm).reshape(-1), Wm_o)
+            assert_close(f32(S), S_o, "soft mask (ties)")
+        idx0 = roi.mask_fwd(W, L, n, m, 1.0, 1.0, seed, step, 0)[2].cpu().numpy()
+        assert np.all(idx0 == np.arange(n)[None, :])
+
+
+# --------------------------------------------------------------------------- layout properties
+def test_split_calls_equal_one_slab_call(dev):
+    """Per-tensor calls with cumulative elem_offset give exactly the outputs of
+    one call over the back-to-back slab."""
+    import torch
+    shapes = [(128, 96), (32, 96), (32, 96), (128, 96), (200, 96), (96, 200)]
+    offs = np.cumsum([0] + [r * c for r, c in shapes])
+    total = int(offs[-1])
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(3)
+    W = (torch.randn(total, generator=gen) * 0.02).to(torch.bfloat16).to(dev)
+    L = torch.randn(total, generator=gen).to(dev)
+    G = (torch.randn(total, generator=gen) * 1e-3).to(torch.bfloat16).to(dev)
+    for n, m in ((2, 4), (4, 8)):
+        say(f"split vs slab {n}:{m}")
+        Wm, S, idx = roi.mask_fwd(W, L, n, m, 0.5, 1.0, 9, 2, 0, want_soft=True)
+        d = roi.mask_bwd(G, W, L, n, m, 0.5, 1.0, 9, 2, 0)
+        for (r, c), o in zip(shapes, offs[:-1]):
+            o = int(o)
+            sl = slice(o, o + r * c)
+            w_t, l_t, g_t = (W[sl].view(r, c), L[sl].view(r, c), G[sl].view(r, c))
+            Wm_t, S_t, idx_t = roi.mask_fwd(w_t, l_t, n, m, 0.5, 1.0, 9, 2, o, want_soft=True)
+            d_t = roi.mask_bwd(g_t, w_t, l_t, n, m, 0.5, 1.0, 9, 2, o)
+            torch.cuda.synchronize()
+            assert torch.equal(Wm_t.reshape(-1).view(torch.int16), Wm[sl].view(torch.int16))
+            assert torch.equal(S_t.reshape(-1).view(torch.int32), S[sl].view(torch.int32))
+            assert torch.equal(idx_t, idx[o // m:(o + r * c) // m])
+            assert torch.equal(d_t.reshape(-1).view(torch.int32), d[sl].view(torch.int32))
+
+
+def test_every_output_written_and_deterministic(dev):
+    import torch
+    W, L, G = wl.small_case(333, 64, 1, device=dev)
+    for n, m in ((2, 4), (3, 8)):
+        say(f"sentinel/determinism {n}:{m}")
+        outs = []
+        for _ in range(2):
+            Wm = torch.full_like(W, float("nan"))
+            S = torch.full_like(L, float("nan"))
+            idx = torch.full((W.numel() // m, n), 255, dtype=torch.uint8, device=dev)
+            d = torch.full_like(L, float("nan"))
+            roi.mask_fwd(W, L, n, m, 0.8, 1.0, 4, 4, 0, want_soft=True,
+                         out={"W_masked": Wm, "soft_mask": S, "sel_idx": idx})
+            roi.mask_bwd(G, W, L, n, m, 0.8, 1.0, 4, 4, 0, out=d)
+            torch.cuda.synchronize()
+            assert not torch.isnan(Wm.float()).any() and not torch.isnan(S).any()
+            assert not torch.isnan(d).any() and bool((idx < m).all())
+            outs.append((Wm.view(torch.int16).clone(), S.view(torch.int32).clone(), idx.clone(),
+                         d.view(torch.int32).clone()))
+        for a, b in zip(*outs):
+            assert torch.equal(a, b)
+
+
+def test_empty_and_invalid_on_device(dev):
+    import torch
+    W = torch.empty(0, 8, dtype=torch.bfloat16, device=dev)
+    L = torch.empty(0, 8, dtype=torch.float32, device=dev)
+    Wm, S, idx = roi.mask_fwd(W, L, 2, 4, want_soft=True)
+    assert Wm.numel() == 0 and idx.numel() == 0
+    W = torch.zeros(4, 6, dtype=torch.bfloat16, device=dev)
+    L = torch.zeros(4, 6, dtype=torch.float32, device=dev)
+    with pytest.raises(roi.RoiError):
+        roi.mask_fwd(W, L, 2, 4)
+    with pytest.raises(roi.RoiError):
+        roi.mask_fwd(W[:, :4].contiguous(), L[:, :4].contiguous(), 2, 4, tau=0.0, want_soft=True)
+
+
+# --------------------------------------------------------------------------- full-size workloads
+def sample_groups(workload, ngroups, m, rng, count):
+    """Random groups plus the first and last group of every tensor."""
+    edges = []
+    for t in workload.tensors:
+        g0 = t.offset // m
+        g1 = (t.offset + t.numel) // m - 1
+        edges += [g0, g1]
+    picks = np.concatenate([rng.integers(0, ngroups, count), np.array(edges), [0, ngroups - 1]])
+    return np.unique(picks)
+
+
+def full_workload_check(dev, name, n, m, tau, step, count):
+    """The whole stack in one call (the benchmark's launch configuration):
+    sampled groups against the oracle, structural properties on every group."""
+    import torch
+    work = wl.WORKLOADS[name]
+    say(f"full workload {name} {n}:{m} tau={tau} step={step}: allocating {work.numel} weights")
+    W, L, G = wl.fill_slab(work, dev, step=step)
+    Wm, _, idx = roi.mask_fwd(W, L, n, m, tau, 1.0, 0, step, 0, want_soft=False)
+    d = roi.mask_bwd(G, W, L, n, m, tau, 1.0, 0, step, 0)
+    torch.cuda.synchronize()
+    say("  kernels done; checking properties")
+    ng = work.numel // m
+    chunk = 1 << 26
+    ar = torch.arange(m, device=dev, dtype=torch.uint8)
+    for g0 in range(0, ng, chunk):
+        g1 = min(ng, g0 + chunk)
+        ii = idx[g0:g1].long()
+        hard = torch.zeros((g1 - g0, m), dtype=torch.bool, device=dev)
+        hard.scatter_(1, ii, True)
+        assert bool((hard.sum(1) == n).all()), "a group does not keep exactly n entries"
+        w = W[g0 * m:g1 * m].view(-1, m).view(torch.int16)
+        wm = Wm[g0 * m:g1 * m].view(-1, m).view(torch.int16)
+        assert torch.equal(wm, torch.where(hard, w, torch.zeros_like(w))), "W_masked != W (.) hard"
+        assert bool(torch.isfinite(d[g0 * m:g1 * m]).all())
+        del ii, hard, w, wm
+    del ar
+    rng = np.random.default_rng(1234 + step)
+    picks = sample_groups(work, ng, m, rng, count)
+    say(f"  comparing {picks.size} sampled groups with the oracle")
+    pt = torch.from_numpy(picks).to(dev)
+    take = lambda t: t.view(-1, m).index_select(0, pt)
+    Wg, Lg, Gg = take(W), take(L), take(G)
+    tau32 = float(np.float32(tau))
+    ge = picks.astype(np.uint64) * np.uint64(m)
+    Wm_o, _, idx_o = oracle.mask_fwd_groups(bf16_bits(Wg), f32(Lg), ge, n, m, tau32, 1.0, 0, step,
+                                            want_soft=False)
+    d_o = oracle.mask_bwd_groups(bf16_bits(Gg), bf16_bits(Wg), f32(Lg), ge, n, m, tau32, 1.0, 0,
+                                 step)
+    assert np.array_equal(idx.index_select(0, pt).cpu().numpy(), idx_o)
+    assert np.array_equal(bf16_bits(take(Wm)), Wm_o)
+    r = assert_close(f32(take(d)), d_o, f"grad_logits ({name})")
+    say(f"  ok: grad err/bound {r:.3f}")
+    del W, L, G, Wm, idx, d
+    torch.cuda.empty_cache()
+
+
+def test_full_qwen05b_stack_2of4(dev):
+    full_workload_check(dev, "qwen2.5-0.5b-stack-2:4", 2, 4, 1.0, 0, 20000)
+
+
+def test_full_qwen7b_layer_2of4(dev):
+    full_workload_check(dev, "qwen2.5-7b-layer-2:4", 2, 4, 0.5, 0, 20000)
+
+
+def test_full_qwen7b_layer_4of8(dev):
+    full_workload_check(dev, "qwen2.5-7b-layer-4:8", 4, 8, 0.5, 0, 20000)
+
+
+@pytest.mark.parametrize("step", [0, 9])
+def test_full_qwen7b_stack_2of4(dev, step):
+    tau = roi.anneal(1.0, 0.1, step, 9)
+    full_workload_check(dev, "qwen2.5-7b-stack-2:4", 2, 4, tau, step, 30000)
