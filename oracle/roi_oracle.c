@@ -108,53 +108,88 @@ float oracle_uniform(uint32_t word)
 }
 
 /* ------------------------------------------------------------------------- *
- * 2. Deterministic fp32 natural logarithm.  Written from the mathematics:
- *    x = m 2^E with m in [sqrt(1/2), sqrt(2)), ln x = E ln 2 + ln m, and
- *    ln m = 2 atanh(s) with s = (m-1)/(m+1) = f/(f+2), f = m-1, expanded as
- *    2s + s^3 (2/3 + (2/5) s^2 + (2/7) s^4 + (2/9) s^6) (the first terms of
- *    the atanh series; |s| <= 0.1716, the dropped terms are below 1e-9
- *    relative).  ln 2 is split Cody-Waite style into a 16-bit head (so that
- *    E * head is exact) and an fp32 tail.  Every operation is one IEEE fp32
- *    operation (add, multiply, divide, or fused multiply-add), in the order
- *    written, so the result is a single well-defined fp32 value.
- *    Valid for finite normal x > 0, which covers every value the noise
- *    definition feeds it (u in [2^-24, 1-2^-24] and -ln u in [5.9e-8, 16.7]).
+ * 2. Deterministic fp32 natural logarithm (table-driven reduction in the
+ *    manner of Tang, "Table-driven implementation of the logarithm function
+ *    in IEEE floating-point arithmetic", ACM TOMS 1990), written from the
+ *    mathematics:
+ *      x = z 2^k with z in [0.703125, 1.40625)   (bit manipulation, exact)
+ *      z lies in one of 128 cells: 76 cells of width 2^-8 below 1 and 52 of
+ *      width 2^-7 from 1 up; cell i has centre c_i, inv_i = fl32(1/c_i) and
+ *      lg_i = fl32(-ln inv_i), except the two cells touching 1, which use
+ *      inv = 1 and lg = 0 so that r = z - 1 is exact there;
+ *      r = fma(z, inv_i, -1)                      (|r| <= 2^-7)
+ *      ln(1 + r) ~ r + r^2 (-1/2 + r (1/3 - r/4)) (first terms of the series;
+ *                                                  dropped terms < 1e-9 relative)
+ *      ln x = k ln2 + lg_i + ln(1 + r).
+ *    The cell constants are computed in fp64 from a truncated atanh series,
+ *    ln v = 2 sum_j s^(2j+1) / (2j+1), s = (v-1)/(v+1) (15 terms, below fp64
+ *    rounding for |s| < 0.18), then rounded to fp32.  Every fp32 step is one
+ *    IEEE operation (add, multiply or fused multiply-add) in the order
+ *    written, so the result is a single well-defined fp32 value.  Valid for
+ *    finite normal x > 0, which covers every value the noise definition feeds
+ *    it (u in [2^-24, 1-2^-24] and -ln u in [5.9e-8, 16.7]).
  * ------------------------------------------------------------------------- */
 static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
 static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
 
+#define LOG_CELLS 128
+#define LOG_CELLS_BELOW_ONE 76
+#define LOG_Z_BASE_BITS 0x3F340000u /* 0.703125 */
+
+static float log_inv[LOG_CELLS];
+static float log_lg[LOG_CELLS];
+static int log_table_ready = 0;
+
+static double ln_atanh_series(double v)
+{
+    double s = (v - 1.0) / (v + 1.0);
+    double s2 = s * s;
+    double acc = 0.0;
+    for (int j = 14; j >= 0; --j) acc = acc * s2 + 2.0 / (double)(2 * j + 1);
+    return s * acc;
+}
+
+static void build_log_table(void)
+{
+    if (log_table_ready) return;
+    for (int i = 0; i < LOG_CELLS; ++i) {
+        double lo, width;
+        if (i < LOG_CELLS_BELOW_ONE) {
+            lo = 0.703125 + (double)i / 256.0;
+            width = 1.0 / 256.0;
+        } else {
+            lo = 1.0 + (double)(i - LOG_CELLS_BELOW_ONE) / 128.0;
+            width = 1.0 / 128.0;
+        }
+        double centre = lo + width / 2.0;
+        if (i == LOG_CELLS_BELOW_ONE - 1 || i == LOG_CELLS_BELOW_ONE) {
+            log_inv[i] = 1.0f;
+            log_lg[i] = 0.0f;
+        } else {
+            float inv = (float)(1.0 / centre);
+            log_inv[i] = inv;
+            log_lg[i] = (float)(-ln_atanh_series((double)inv));
+        }
+    }
+    log_table_ready = 1;
+}
+
 float oracle_log(float x)
 {
-    /* Series coefficients 2/k rounded to fp32, and ln 2 = head + tail. */
-    const float c3 = (float)(2.0 / 3.0);
-    const float c5 = (float)(2.0 / 5.0);
-    const float c7 = (float)(2.0 / 7.0);
-    const float c9 = (float)(2.0 / 9.0);
-    const double ln2 = 0.69314718055994530941723212145818;
-    const float ln2_head = (float)(floor(ln2 * 65536.0) / 65536.0); /* 16 significant bits */
-    const float ln2_tail = (float)(ln2 - (double)ln2_head);
-
-    uint32_t bits = f2u(x);
-    int e = (int)(bits >> 23) - 127;
-    uint32_t frac = bits & 0x7FFFFFu;
-    float m = u2f(frac | 0x3F800000u); /* m in [1, 2) */
-    /* Bring m into [sqrt(1/2), sqrt(2)): halve it when m > sqrt(2).  The
-     * smallest fp32 above sqrt(2) is 0x3FB504F4. */
-    if ((frac | 0x3F800000u) >= 0x3FB504F4u) {
-        m = m * 0.5f;
-        e = e + 1;
-    }
-    float f = m - 1.0f;          /* exact */
-    float s = f / (f + 2.0f);
-    float z = s * s;
-    float p = fmaf(c9, z, c7);
-    p = fmaf(p, z, c5);
-    p = fmaf(p, z, c3);
-    float t = s * z;
-    float r = fmaf(t, p, s + s); /* ln m */
-    float ef = (float)e;
-    float lo = fmaf(ef, ln2_tail, r);
-    return fmaf(ef, ln2_head, lo);
+    build_log_table();
+    const float ln2 = (float)0.69314718055994530941723212145818;
+    uint32_t ix = f2u(x);
+    uint32_t t = ix - LOG_Z_BASE_BITS;
+    int cell = (int)((t >> 16) & (LOG_CELLS - 1));
+    int k = (int32_t)t >> 23;                 /* x = z 2^k */
+    float z = u2f(ix - (t & 0xFF800000u));
+    float r = fmaf(z, log_inv[cell], -1.0f);
+    float p = fmaf(r, -0.25f, (float)(1.0 / 3.0));
+    p = fmaf(r, p, -0.5f);
+    float r2 = r * r;
+    float l1p = fmaf(r2, p, r);                /* ln(1 + r) */
+    float s = log_lg[cell] + l1p;
+    return fmaf((float)k, ln2, s);
 }
 
 void oracle_log_array(const float* x, int64_t n, float* out)

@@ -24,7 +24,7 @@ constexpr uint32_t kWeyl0 = 0x9E3779B9u;
 constexpr uint32_t kWeyl1 = 0xBB67AE85u;
 
 struct NoiseKey {
-    uint32_t k0, k1;          // lo32 / hi32 of the seed
+    uint32_t k0, k1;           // lo32 / hi32 of the seed
     uint32_t step_lo, step_hi; // counter words 2 and 3
 };
 
@@ -54,66 +54,108 @@ __device__ __forceinline__ uint4 philox_block(uint64_t block, const NoiseKey& ke
                          key.k0, key.k1);
 }
 
-// u = (2 (x >> 9) + 1) 2^-24: odd points of the 2^-24 grid, in (0, 1), exact.
+// u = (2 (x >> 9) + 1) 2^-24: odd points of the 2^-24 grid, in (0, 1).
+// Evaluated as (1 + (x >> 9) 2^-23) - (1 - 2^-24): the first term is the
+// float with mantissa x >> 9, and the difference is exact.
 __device__ __forceinline__ float uniform_from_word(uint32_t x)
 {
-    return (float)(((x >> 9) << 1) | 1u) * 0x1p-24f;
+    return __uint_as_float((x >> 9) | 0x3F800000u) - 0x1.fffffep-1f;
 }
 
-// Deterministic fp32 natural logarithm for finite normal x > 0.
-// x = m 2^E with m in [sqrt(1/2), sqrt(2)); ln m = 2 atanh(s), s = f / (f + 2),
-// f = m - 1 (exact), summed as 2s + s^3 (2/3 + 2/5 s^2 + 2/7 s^4 + 2/9 s^6);
-// ln 2 is split into a 16-bit head (E * head is exact) and an fp32 tail.
-// Each line below is one correctly rounded fp32 operation; the file is
-// compiled with -ffp-contract=off so none is fused or reordered, and '/' is
-// the IEEE division.
-constexpr double kLn2 = 0.69314718055994530941723212145818;
-constexpr float kLn2Head = (float)(45426.0 / 65536.0); // ln 2 truncated to 16 bits
-constexpr float kLn2Tail = (float)(kLn2 - 45426.0 / 65536.0);
-constexpr float kAtanh3 = (float)(2.0 / 3.0);
-constexpr float kAtanh5 = (float)(2.0 / 5.0);
-constexpr float kAtanh7 = (float)(2.0 / 7.0);
-constexpr float kAtanh9 = (float)(2.0 / 9.0);
-static_assert(45426.0 / 65536.0 <= kLn2 && kLn2 < 45427.0 / 65536.0, "ln2 head");
+// Deterministic fp32 natural logarithm for finite normal x > 0, table-driven
+// in the manner of Tang (ACM TOMS 1990):
+//   x = z 2^k, z in [0.703125, 1.40625) (bit manipulation, exact);
+//   z falls in one of 128 cells (76 of width 2^-8 below 1, 52 of width 2^-7
+//   from 1 up); cell i holds inv_i = fl32(1/c_i) for its centre c_i and
+//   lg_i = fl32(-ln inv_i), except the two cells touching 1, which hold
+//   inv = 1 and lg = 0 so that r = z - 1 is exact there;
+//   r = fma(z, inv_i, -1), ln(1 + r) ~ r + r^2 (-1/2 + r (1/3 - r/4));
+//   ln x = k ln2 + lg_i + ln(1 + r).
+// The cell constants come from a 15-term fp64 atanh series rounded to fp32.
+// Every fp32 step is one IEEE operation in the order written (the library is
+// compiled with -ffp-contract=off), so the value is reproducible bit for bit.
+constexpr int kLogCells = 128;
+constexpr int kLogCellsBelowOne = 76;
+constexpr uint32_t kLogZBaseBits = 0x3F340000u; // 0.703125
+constexpr float kLn2f = (float)0.69314718055994530941723212145818;
+constexpr float kThird = (float)(1.0 / 3.0);
 
-__device__ __forceinline__ float det_log(float x)
+// fp64 ln by the atanh series, for the cell constants.
+__device__ __forceinline__ double ln_atanh_series(double v)
 {
-    const uint32_t bits = __float_as_uint(x);
-    int e = (int)(bits >> 23) - 127;
-    const uint32_t mbits = (bits & 0x7FFFFFu) | 0x3F800000u; // m in [1, 2)
-    float m = __uint_as_float(mbits);
-    if (mbits >= 0x3FB504F4u) { // m > sqrt(2): use m/2 and E+1
-        m = m * 0.5f;
-        e = e + 1;
-    }
-    const float f = m - 1.0f;
-    const float s = f / (f + 2.0f);
-    const float z = s * s;
-    float p = __builtin_fmaf(kAtanh9, z, kAtanh7);
-    p = __builtin_fmaf(p, z, kAtanh5);
-    p = __builtin_fmaf(p, z, kAtanh3);
-    const float t = s * z;
-    const float r = __builtin_fmaf(t, p, s + s);
-    const float ef = (float)e;
-    const float lo = __builtin_fmaf(ef, kLn2Tail, r);
-    return __builtin_fmaf(ef, kLn2Head, lo);
+    const double s = (v - 1.0) / (v + 1.0);
+    const double s2 = s * s;
+    double acc = 0.0;
+    for (int j = 14; j >= 0; --j) acc = acc * s2 + 2.0 / (double)(2 * j + 1);
+    return s * acc;
 }
 
-// g = -log(-log u)
-__device__ __forceinline__ float gumbel_from_word(uint32_t x)
+// Fills the 128 (inv, lg) cells; threads 0..127 of the block each write one.
+// The caller synchronises the block before the first lookup.
+__device__ __forceinline__ void fill_log_table(float2* tab)
+{
+    const int i = threadIdx.x;
+    if (i >= kLogCells) return;
+    double lo, width;
+    if (i < kLogCellsBelowOne) {
+        lo = 0.703125 + (double)i / 256.0;
+        width = 1.0 / 256.0;
+    } else {
+        lo = 1.0 + (double)(i - kLogCellsBelowOne) / 128.0;
+        width = 1.0 / 128.0;
+    }
+    const double centre = lo + width / 2.0;
+    float inv = 1.0f, lg = 0.0f;
+    if (i != kLogCellsBelowOne - 1 && i != kLogCellsBelowOne) {
+        inv = (float)(1.0 / centre);
+        lg = (float)(-ln_atanh_series((double)inv));
+    }
+    tab[i] = make_float2(inv, lg);
+}
+
+// ln of the float whose bit pattern is ix.
+__device__ __forceinline__ float det_log_bits(uint32_t ix, const float2* tab)
+{
+    const uint32_t t = ix - kLogZBaseBits;
+    const int cell = (int)((t >> 16) & (kLogCells - 1));
+    const int k = (int)t >> 23;
+    const float z = __uint_as_float(ix - (t & 0xFF800000u));
+    const float2 c = tab[cell];
+    const float r = __builtin_fmaf(z, c.x, -1.0f);
+    float p = __builtin_fmaf(r, -0.25f, kThird);
+    p = __builtin_fmaf(r, p, -0.5f);
+    const float r2 = r * r;
+    const float l1p = __builtin_fmaf(r2, p, r);
+    const float s = c.y + l1p;
+    return __builtin_fmaf((float)k, kLn2f, s);
+}
+
+__device__ __forceinline__ float det_log(float x, const float2* tab)
+{
+    return det_log_bits(__float_as_uint(x), tab);
+}
+
+// Returns ln(-ln u) = -g for the Gumbel noise g = -log(-log u).  ln u < 0, so
+// the bits of -ln u are those of ln u with the sign bit cleared.
+__device__ __forceinline__ float neg_gumbel_from_word(uint32_t x, const float2* tab)
 {
     const float u = uniform_from_word(x);
-    const float y = -det_log(u);
-    return -det_log(y);
+    const float lu = det_log(u, tab);
+    return det_log_bits(__float_as_uint(lu) & 0x7FFFFFFFu, tab);
+}
+
+__device__ __forceinline__ float gumbel_from_word(uint32_t x, const float2* tab)
+{
+    return -neg_gumbel_from_word(x, tab);
 }
 
 // kappa = fl(fl(phi / lambda) + g); for lambda == 1 the quotient is phi exactly.
 template <bool kLambdaOne>
-__device__ __forceinline__ float key_of(float phi, float lambda, uint32_t word)
+__device__ __forceinline__ float key_of(float phi, float lambda, uint32_t word, const float2* tab)
 {
-    const float g = gumbel_from_word(word);
+    const float ng = neg_gumbel_from_word(word, tab);
     const float phi_bar = kLambdaOne ? phi : phi / lambda;
-    return phi_bar + g;
+    return phi_bar - ng;
 }
 
 } // namespace roi

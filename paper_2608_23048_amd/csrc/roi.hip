@@ -135,21 +135,24 @@ __device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
 
 template <int M, bool kLambdaOne>
 __device__ __forceinline__ void group_keys(const float (&phi)[M], uint64_t block, const NoiseKey& key,
-                                           float lambda, float (&kappa)[M])
+                                           float lambda, const float2* tab, float (&kappa)[M])
 {
 #pragma unroll
     for (int t = 0; t < M / 4; ++t) {
         const uint4 x = philox_block(block + t, key);
-        kappa[4 * t + 0] = key_of<kLambdaOne>(phi[4 * t + 0], lambda, x.x);
-        kappa[4 * t + 1] = key_of<kLambdaOne>(phi[4 * t + 1], lambda, x.y);
-        kappa[4 * t + 2] = key_of<kLambdaOne>(phi[4 * t + 2], lambda, x.z);
-        kappa[4 * t + 3] = key_of<kLambdaOne>(phi[4 * t + 3], lambda, x.w);
+        kappa[4 * t + 0] = key_of<kLambdaOne>(phi[4 * t + 0], lambda, x.x, tab);
+        kappa[4 * t + 1] = key_of<kLambdaOne>(phi[4 * t + 1], lambda, x.y, tab);
+        kappa[4 * t + 2] = key_of<kLambdaOne>(phi[4 * t + 2], lambda, x.z, tab);
+        kappa[4 * t + 3] = key_of<kLambdaOne>(phi[4 * t + 3], lambda, x.w, tab);
     }
 }
 
 template <int M, int N, bool kWantS, bool kWantIdx, bool kLambdaOne>
 __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
 {
+    __shared__ float2 tab[kLogCells];
+    fill_log_table(tab);
+    __syncthreads();
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
         const int64_t base = q * M;
@@ -158,7 +161,7 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
         load_logits<M>(a.phi + base, phi);
         load_bf16<M>(a.W + base, w);
         float kappa[M];
-        group_keys<M, kLambdaOne>(phi, a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda, kappa);
+        group_keys<M, kLambdaOne>(phi, a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda, tab, kappa);
         int rank[M];
         rank_keys<M>(kappa, rank);
         store_masked<M>(a.Wm + base, w, rank, N);
@@ -180,6 +183,9 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
 template <int M, int N, bool kLambdaOne>
 __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
 {
+    __shared__ float2 tab[kLogCells];
+    fill_log_table(tab);
+    __syncthreads();
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
         const int64_t base = q * M;
@@ -189,7 +195,7 @@ __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
         load_bf16<M>(a.W + base, w);
         load_bf16<M>(a.G + base, g);
         float kappa[M];
-        group_keys<M, kLambdaOne>(phi, a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda, kappa);
+        group_keys<M, kLambdaOne>(phi, a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda, tab, kappa);
         // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
         float sbar[M];
 #pragma unroll
@@ -216,6 +222,9 @@ __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
 __global__ __launch_bounds__(kBlock) void noise_kernel(uint32_t* words, float* gum, int64_t count,
                                                        uint64_t block0, NoiseKey key)
 {
+    __shared__ float2 tab[kLogCells];
+    fill_log_table(tab);
+    __syncthreads();
     const int64_t nblocks = (count + 3) / 4;
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     for (int64_t b = (int64_t)blockIdx.x * kBlock + threadIdx.x; b < nblocks; b += stride) {
@@ -226,7 +235,7 @@ __global__ __launch_bounds__(kBlock) void noise_kernel(uint32_t* words, float* g
             const int64_t e = 4 * b + t;
             if (e < count) {
                 if (words) words[e] = xs[t];
-                if (gum) gum[e] = gumbel_from_word(xs[t]);
+                if (gum) gum[e] = gumbel_from_word(xs[t], tab);
             }
         }
     }
@@ -235,9 +244,12 @@ __global__ __launch_bounds__(kBlock) void noise_kernel(uint32_t* words, float* g
 __global__ __launch_bounds__(kBlock) void gumbel_words_kernel(const uint32_t* words, float* gum,
                                                               int64_t count)
 {
+    __shared__ float2 tab[kLogCells];
+    fill_log_table(tab);
+    __syncthreads();
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride)
-        gum[i] = gumbel_from_word(words[i]);
+        gum[i] = gumbel_from_word(words[i], tab);
 }
 
 // ----------------------------------------------------------------------------- host side

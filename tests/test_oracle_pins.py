@@ -95,7 +95,7 @@ def test_uniform_grid_exact_and_open():
 # --------------------------------------------------------------------------- deterministic log
 def test_log_accuracy_every_mantissa():
     """Every fp32 mantissa in four binades (all 2^23 values each): the fp32
-    result is within 2 ulp of numpy's fp64 log (error measured in ulp of the
+    result is within 1.5 ulp of numpy's fp64 log (error measured in ulp of the
     correctly rounded fp32 value, or absolutely near ln x = 0)."""
     mant = np.arange(1 << 23, dtype=np.uint32)
     for exp_bits in (126, 127, 100, 131):  # [0.5,1), [1,2), tiny, [16,32)
@@ -105,7 +105,7 @@ def test_log_accuracy_every_mantissa():
         err = np.abs(got - ref) / np.maximum(ulp32(ref.astype(np.float32)), 2.0 ** -149)
         # near x = 1 the value is tiny; there the error is bounded relative to |ln x| by
         # the same 2 ulp (the reduction leaves m - 1 exact), so the ulp measure applies.
-        assert err.max() <= 2.0, (exp_bits, err.max(), x[err.argmax()])
+        assert err.max() <= 1.5, (exp_bits, err.max(), x[err.argmax()])
 
 
 def test_log_special_values():
