@@ -81,7 +81,7 @@ constexpr float kLn2f = (float)0.69314718055994530941723212145818;
 constexpr float kThird = (float)(1.0 / 3.0);
 
 // fp64 ln by the atanh series, for the cell constants.
-__device__ __forceinline__ double ln_atanh_series(double v)
+constexpr double ln_atanh_series(double v)
 {
     const double s = (v - 1.0) / (v + 1.0);
     const double s2 = s * s;
@@ -90,27 +90,43 @@ __device__ __forceinline__ double ln_atanh_series(double v)
     return s * acc;
 }
 
-// Fills the 128 (inv, lg) cells; threads 0..127 of the block each write one.
+struct LogCells {
+    float2 cell[kLogCells]; // (inv, lg)
+};
+
+// The cell constants, evaluated by the compiler (IEEE fp64, round to nearest).
+constexpr LogCells make_log_cells()
+{
+    LogCells t{};
+    for (int i = 0; i < kLogCells; ++i) {
+        double lo = 0.0, width = 0.0;
+        if (i < kLogCellsBelowOne) {
+            lo = 0.703125 + (double)i / 256.0;
+            width = 1.0 / 256.0;
+        } else {
+            lo = 1.0 + (double)(i - kLogCellsBelowOne) / 128.0;
+            width = 1.0 / 128.0;
+        }
+        const double centre = lo + width / 2.0;
+        float inv = 1.0f, lg = 0.0f;
+        if (i != kLogCellsBelowOne - 1 && i != kLogCellsBelowOne) {
+            inv = (float)(1.0 / centre);
+            lg = (float)(-ln_atanh_series((double)inv));
+        }
+        t.cell[i].x = inv;
+        t.cell[i].y = lg;
+    }
+    return t;
+}
+
+__device__ const LogCells kLogCellTable = make_log_cells();
+
+// Copies the cells into the block's LDS copy; threads 0..127 each copy one.
 // The caller synchronises the block before the first lookup.
 __device__ __forceinline__ void fill_log_table(float2* tab)
 {
     const int i = threadIdx.x;
-    if (i >= kLogCells) return;
-    double lo, width;
-    if (i < kLogCellsBelowOne) {
-        lo = 0.703125 + (double)i / 256.0;
-        width = 1.0 / 256.0;
-    } else {
-        lo = 1.0 + (double)(i - kLogCellsBelowOne) / 128.0;
-        width = 1.0 / 128.0;
-    }
-    const double centre = lo + width / 2.0;
-    float inv = 1.0f, lg = 0.0f;
-    if (i != kLogCellsBelowOne - 1 && i != kLogCellsBelowOne) {
-        inv = (float)(1.0 / centre);
-        lg = (float)(-ln_atanh_series((double)inv));
-    }
-    tab[i] = make_float2(inv, lg);
+    if (i < kLogCells) tab[i] = kLogCellTable.cell[i];
 }
 
 // ln of the float whose bit pattern is ix.

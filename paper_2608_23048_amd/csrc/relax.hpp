@@ -32,49 +32,59 @@ __device__ __forceinline__ void rank_keys(const float (&kappa)[M], int (&rank)[M
 // One record per relaxation step, kept for the reverse sweep.
 template <int M>
 struct StepRec {
-    float mu[M];     // mu^(k)
-    float om_star;   // 1 - mu^(k)_{i*}, evaluated as the sum of the others
-    int istar;       // index of the largest adjusted key at step k
+    float mu[M];   // mu^(k)
+    float om_star; // 1 - mu^(k)_{i*}, evaluated as the sum of the other entries
+    int istar;     // index of the largest adjusted key at step k
 };
 
 // Relaxation (§3.2 recursion, Algorithm 1) in fp32:
 //   alpha^(1) = kappa; mu^(k) = softmax(alpha^(k) / tau);
 //   alpha^(k+1) = alpha^(k) + log(1 - mu^(k));  S = sum_k mu^(k).
-// Internally a = (alpha - max kappa) * log2(e), so the softmax is
-// exp2((a - max a) / tau) and the update is a += log2(1 - mu) (same values,
-// one multiply fewer per step).  Subtracting the group's largest key first
-// keeps the competing entries near 0, where fp32 is densest.
-// 1 - mu_i: for i != i* it is >= 1/2 and 1 - mu_i is exact to rounding; for
-// the current argmax i* it is rest / T with rest = sum of the other
+// Internally b = (alpha - max kappa) * log2(e) / tau, so the softmax is
+// exp2(b - max b) and the update is b += log2(1 - mu) / tau: the same values
+// with one multiply fewer per element and step.  Subtracting the group's
+// largest key first keeps the competing entries near 0, where fp32 is
+// densest, and makes b = 0 exactly at the first argmax.
+// 1 - mu_i: for i != i* it is >= 1/2, so 1 - mu_i loses nothing; for the
+// current argmax i* it is rest / T with rest = the sum of the other
 // exponentials (no cancellation).  log(1 - mu) is floored at log(FLT_MIN).
 template <int M, int N, bool kWantS, bool kKeep>
 __device__ __forceinline__ void relax_forward(const float (&kappa)[M], float inv_tau,
                                               float (&S)[M], StepRec<M> (&rec)[N])
 {
     float kmax = kappa[0];
+    int istar = 0;
 #pragma unroll
-    for (int j = 1; j < M; ++j) kmax = fmaxf(kmax, kappa[j]);
-    float a[M];
+    for (int j = 1; j < M; ++j) {
+        const bool gt = kappa[j] > kmax;
+        kmax = gt ? kappa[j] : kmax;
+        istar = gt ? j : istar;
+    }
+    const float c = kLog2e * inv_tau;
+    float b[M];
 #pragma unroll
     for (int j = 0; j < M; ++j) {
-        a[j] = (kappa[j] - kmax) * kLog2e;
+        b[j] = (kappa[j] - kmax) * c;
         if (kWantS) S[j] = 0.0f;
     }
 #pragma unroll
     for (int k = 0; k < N; ++k) {
-        float amax = a[0];
-        int istar = 0;
+        float bmax = 0.0f; // step 1: b[istar] == 0 exactly
+        if (k > 0) {
+            bmax = b[0];
+            istar = 0;
 #pragma unroll
-        for (int j = 1; j < M; ++j) {
-            const bool gt = a[j] > amax;
-            amax = gt ? a[j] : amax;
-            istar = gt ? j : istar;
+            for (int j = 1; j < M; ++j) {
+                const bool gt = b[j] > bmax;
+                bmax = gt ? b[j] : bmax;
+                istar = gt ? j : istar;
+            }
         }
         float e[M];
         float rest = 0.0f;
 #pragma unroll
         for (int j = 0; j < M; ++j) {
-            e[j] = __builtin_amdgcn_exp2f((a[j] - amax) * inv_tau); // e[istar] == 1 exactly
+            e[j] = __builtin_amdgcn_exp2f(k > 0 ? b[j] - bmax : b[j]); // e[istar] == 1 exactly
             rest += (j == istar) ? 0.0f : e[j];
         }
         const float inv_total = __builtin_amdgcn_rcpf(1.0f + rest);
@@ -91,11 +101,11 @@ __device__ __forceinline__ void relax_forward(const float (&kappa)[M], float inv
             rec[k].istar = istar;
         }
         if (k + 1 < N) {
+            const float om_star_f = fmaxf(om_star, kFltMin);
 #pragma unroll
             for (int j = 0; j < M; ++j) {
-                float om = (j == istar) ? om_star : 1.0f - mu[j];
-                om = fmaxf(om, kFltMin);
-                a[j] += __builtin_amdgcn_logf(om);
+                const float om = (j == istar) ? om_star_f : 1.0f - mu[j];
+                b[j] = __builtin_fmaf(__builtin_amdgcn_logf(om), inv_tau, b[j]);
             }
         }
     }
@@ -111,6 +121,7 @@ __device__ __forceinline__ void relax_forward(const float (&kappa)[M], float inv
 // the identity omega_i* mubar_i* = omega_i* sbar_i* - a_i* is used:
 //   dL/dalpha^(k)_i* = a_i* (omega* + tau - 1) / tau
 //                      + (mu_i* / tau) (omega* sbar_i* - sum_{j != i*} mu_j mubar_j).
+// A floored omega* is replaced by +inf, so that a_i* / omega* = 0.
 template <int M, int N>
 __device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const float (&sbar)[M],
                                                float tau, float inv_tau, float (&abar)[M])
@@ -123,33 +134,34 @@ __device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const
         const int istar = rec[k].istar;
         const float oms = rec[k].om_star;
         const bool floored = !(oms >= kFltMin);
+        float t[M];
+        float p_all = 0.0f, p_excl = 0.0f, sbar_is = 0.0f, abar_is = 0.0f;
         float mubar[M];
-        float p_excl = 0.0f;
-        float mu_is = 0.0f, mub_is = 0.0f;
 #pragma unroll
         for (int j = 0; j < M; ++j) {
             const bool is = (j == istar);
             const float mu = rec[k].mu[j];
-            float r = 0.0f;
+            mubar[j] = sbar[j];
             if (has_next) {
-                const float om = is ? oms : 1.0f - mu;
-                const bool live = !(is && floored);
-                r = live ? abar[j] * __builtin_amdgcn_rcpf(om) : 0.0f;
+                const float om = is ? (floored ? __builtin_inff() : oms) : 1.0f - mu;
+                mubar[j] = __builtin_fmaf(-abar[j], __builtin_amdgcn_rcpf(om), sbar[j]);
             }
-            mubar[j] = sbar[j] - r;
-            p_excl += is ? 0.0f : mu * mubar[j];
-            mu_is = is ? mu : mu_is;
-            mub_is = is ? mubar[j] : mub_is;
+            t[j] = mu * mubar[j];
+            p_all += t[j];
+            p_excl += is ? 0.0f : t[j];
+            sbar_is = is ? sbar[j] : sbar_is;
+            if (has_next) abar_is = is ? abar[j] : abar_is;
         }
-        const float p_all = p_excl + mu_is * mub_is;
-        const float keep = floored ? 1.0f : (oms + (tau - 1.0f)) * inv_tau;
+        const float inner_is = __builtin_fmaf(oms, sbar_is, -p_excl);
+        float carry_is = 0.0f;
+        if (has_next) carry_is = abar_is * (floored ? 1.0f : (oms + (tau - 1.0f)) * inv_tau);
 #pragma unroll
         for (int j = 0; j < M; ++j) {
             const bool is = (j == istar);
-            const float mu = rec[k].mu[j];
-            const float carried = has_next ? abar[j] * (is ? keep : 1.0f) : 0.0f;
-            const float inner = is ? (oms * sbar[j] - p_excl) : (mubar[j] - p_all);
-            abar[j] = carried + (mu * inv_tau) * inner;
+            const float m_t = rec[k].mu[j] * inv_tau;
+            const float inner = is ? inner_is : mubar[j] - p_all;
+            const float carry = has_next ? (is ? carry_is : abar[j]) : 0.0f;
+            abar[j] = __builtin_fmaf(m_t, inner, carry);
         }
     }
 }

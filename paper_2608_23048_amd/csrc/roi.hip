@@ -27,6 +27,20 @@ namespace {
 
 constexpr int kBlock = 256;
 
+// Groups each lane loads ahead before computing the first.
+#ifndef ROI_UNROLL_M4
+#define ROI_UNROLL_M4 2
+#endif
+#ifndef ROI_UNROLL_M8
+#define ROI_UNROLL_M8 1
+#endif
+// Non-temporal hints on the HBM streams (each byte is touched once).
+#ifndef ROI_NONTEMPORAL
+#define ROI_NONTEMPORAL 1
+#endif
+template <int M>
+constexpr int kUnroll = M == 4 ? ROI_UNROLL_M4 : ROI_UNROLL_M8;
+
 struct FwdArgs {
     const uint16_t* W;
     const float* phi;
@@ -58,6 +72,26 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+template <typename T>
+__device__ __forceinline__ T stream_load(const T* p)
+{
+#if ROI_NONTEMPORAL
+    return __builtin_nontemporal_load(p);
+#else
+    return *p;
+#endif
+}
+
+template <typename T>
+__device__ __forceinline__ void stream_store(const T& v, T* p)
+{
+#if ROI_NONTEMPORAL
+    __builtin_nontemporal_store(v, p);
+#else
+    *p = v;
+#endif
+}
+
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t b) { return __uint_as_float(b << 16); }
 
 // Loads of one group: m fp32 logits (m/4 16-byte loads) and m bf16 values
@@ -68,7 +102,7 @@ __device__ __forceinline__ void load_logits(const float* p, float (&phi)[M])
     const f32x4* p4 = reinterpret_cast<const f32x4*>(p);
 #pragma unroll
     for (int t = 0; t < M / 4; ++t) {
-        const f32x4 v = __builtin_nontemporal_load(p4 + t);
+        const f32x4 v = stream_load(p4 + t);
         phi[4 * t + 0] = v.x;
         phi[4 * t + 1] = v.y;
         phi[4 * t + 2] = v.z;
@@ -80,11 +114,11 @@ template <int M>
 __device__ __forceinline__ void load_bf16(const uint16_t* p, uint32_t (&w)[M])
 {
     if constexpr (M == 4) {
-        const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+        const u32x2 v = stream_load(reinterpret_cast<const u32x2*>(p));
         w[0] = v.x & 0xFFFFu; w[1] = v.x >> 16; w[2] = v.y & 0xFFFFu; w[3] = v.y >> 16;
     } else {
         static_assert(M == 8, "m");
-        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+        const u32x4 v = stream_load(reinterpret_cast<const u32x4*>(p));
         w[0] = v.x & 0xFFFFu; w[1] = v.x >> 16; w[2] = v.y & 0xFFFFu; w[3] = v.y >> 16;
         w[4] = v.z & 0xFFFFu; w[5] = v.z >> 16; w[6] = v.w & 0xFFFFu; w[7] = v.w >> 16;
     }
@@ -104,10 +138,10 @@ __device__ __forceinline__ void store_masked(uint16_t* p, const uint32_t (&w)[M]
     }
     if constexpr (M == 4) {
         const u32x2 v = {packed[0], packed[1]};
-        __builtin_nontemporal_store(v, reinterpret_cast<u32x2*>(p));
+        stream_store(v, reinterpret_cast<u32x2*>(p));
     } else {
         const u32x4 v = {packed[0], packed[1], packed[2], packed[3]};
-        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+        stream_store(v, reinterpret_cast<u32x4*>(p));
     }
 }
 
@@ -147,34 +181,52 @@ __device__ __forceinline__ void group_keys(const float (&phi)[M], uint64_t block
     }
 }
 
+// Each iteration of a block covers kUnroll * kBlock consecutive groups: lane l
+// of the block takes groups base + u * kBlock + l, u < kUnroll, so every load
+// and store instruction of a wave is one contiguous span, and all of a lane's
+// loads are issued before its first group is computed (more bytes in flight
+// per wave for the HBM stream).
 template <int M, int N, bool kWantS, bool kWantIdx, bool kLambdaOne>
 __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
 {
     __shared__ float2 tab[kLogCells];
     fill_log_table(tab);
     __syncthreads();
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
-        const int64_t base = q * M;
-        float phi[M];
-        uint32_t w[M];
-        load_logits<M>(a.phi + base, phi);
-        load_bf16<M>(a.W + base, w);
-        float kappa[M];
-        group_keys<M, kLambdaOne>(phi, a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda, tab, kappa);
-        int rank[M];
-        rank_keys<M>(kappa, rank);
-        store_masked<M>(a.Wm + base, w, rank, N);
-        if (kWantIdx) store_idx<M, N>(a.idx + q * N, rank);
-        if (kWantS) {
-            float S[M];
-            StepRec<M> unused[N]; // not written when records are not kept
-            relax_forward<M, N, true, false>(kappa, a.inv_tau, S, unused);
-            f32x4* s4 = reinterpret_cast<f32x4*>(a.S + base);
+    constexpr int U = kUnroll<M>;
+    const int64_t chunk = (int64_t)kBlock * U;
+    for (int64_t base = (int64_t)blockIdx.x * chunk; base < a.ngroups;
+         base += (int64_t)gridDim.x * chunk) {
+        float phi[U][M];
+        uint32_t w[U][M];
 #pragma unroll
-            for (int t = 0; t < M / 4; ++t) {
-                const f32x4 v = {S[4 * t], S[4 * t + 1], S[4 * t + 2], S[4 * t + 3]};
-                __builtin_nontemporal_store(v, s4 + t);
+        for (int u = 0; u < U; ++u) {
+            const int64_t q = base + u * kBlock + threadIdx.x;
+            if (q < a.ngroups) {
+                load_logits<M>(a.phi + q * M, phi[u]);
+                load_bf16<M>(a.W + q * M, w[u]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t q = base + u * kBlock + threadIdx.x;
+            if (q >= a.ngroups) continue;
+            float kappa[M];
+            group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda,
+                                      tab, kappa);
+            int rank[M];
+            rank_keys<M>(kappa, rank);
+            store_masked<M>(a.Wm + q * M, w[u], rank, N);
+            if (kWantIdx) store_idx<M, N>(a.idx + q * N, rank);
+            if (kWantS) {
+                float S[M];
+                StepRec<M> unused[N]; // not written when records are not kept
+                relax_forward<M, N, true, false>(kappa, a.inv_tau, S, unused);
+                f32x4* s4 = reinterpret_cast<f32x4*>(a.S + q * M);
+#pragma unroll
+                for (int t = 0; t < M / 4; ++t) {
+                    const f32x4 v = {S[4 * t], S[4 * t + 1], S[4 * t + 2], S[4 * t + 3]};
+                    stream_store(v, s4 + t);
+                }
             }
         }
     }
@@ -186,34 +238,48 @@ __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
     __shared__ float2 tab[kLogCells];
     fill_log_table(tab);
     __syncthreads();
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
-        const int64_t base = q * M;
-        float phi[M];
-        uint32_t w[M], g[M];
-        load_logits<M>(a.phi + base, phi);
-        load_bf16<M>(a.W + base, w);
-        load_bf16<M>(a.G + base, g);
-        float kappa[M];
-        group_keys<M, kLambdaOne>(phi, a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda, tab, kappa);
-        // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
-        float sbar[M];
+    constexpr int U = kUnroll<M>;
+    const int64_t chunk = (int64_t)kBlock * U;
+    for (int64_t base = (int64_t)blockIdx.x * chunk; base < a.ngroups;
+         base += (int64_t)gridDim.x * chunk) {
+        float phi[U][M];
+        uint32_t w[U][M], g[U][M];
 #pragma unroll
-        for (int j = 0; j < M; ++j) sbar[j] = bf16_bits_to_float(g[j]) * bf16_bits_to_float(w[j]);
-        StepRec<M> rec[N];
-        float S_unused[M];
-        relax_forward<M, N, false, true>(kappa, a.inv_tau, S_unused, rec);
-        float abar[M];
-        relax_backward<M, N>(rec, sbar, a.tau, a.inv_tau, abar);
-        f32x4* d4 = reinterpret_cast<f32x4*>(a.dphi + base);
+        for (int u = 0; u < U; ++u) {
+            const int64_t q = base + u * kBlock + threadIdx.x;
+            if (q < a.ngroups) {
+                load_logits<M>(a.phi + q * M, phi[u]);
+                load_bf16<M>(a.W + q * M, w[u]);
+                load_bf16<M>(a.G + q * M, g[u]);
+            }
+        }
 #pragma unroll
-        for (int t = 0; t < M / 4; ++t) {
-            f32x4 v;
-            v.x = kLambdaOne ? abar[4 * t + 0] : abar[4 * t + 0] * a.inv_lambda;
-            v.y = kLambdaOne ? abar[4 * t + 1] : abar[4 * t + 1] * a.inv_lambda;
-            v.z = kLambdaOne ? abar[4 * t + 2] : abar[4 * t + 2] * a.inv_lambda;
-            v.w = kLambdaOne ? abar[4 * t + 3] : abar[4 * t + 3] * a.inv_lambda;
-            __builtin_nontemporal_store(v, d4 + t);
+        for (int u = 0; u < U; ++u) {
+            const int64_t q = base + u * kBlock + threadIdx.x;
+            if (q >= a.ngroups) continue;
+            float kappa[M];
+            group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda,
+                                      tab, kappa);
+            // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
+            float sbar[M];
+#pragma unroll
+            for (int j = 0; j < M; ++j)
+                sbar[j] = bf16_bits_to_float(g[u][j]) * bf16_bits_to_float(w[u][j]);
+            StepRec<M> rec[N];
+            float S_unused[M];
+            relax_forward<M, N, false, true>(kappa, a.inv_tau, S_unused, rec);
+            float abar[M];
+            relax_backward<M, N>(rec, sbar, a.tau, a.inv_tau, abar);
+            f32x4* d4 = reinterpret_cast<f32x4*>(a.dphi + q * M);
+#pragma unroll
+            for (int t = 0; t < M / 4; ++t) {
+                f32x4 v;
+                v.x = kLambdaOne ? abar[4 * t + 0] : abar[4 * t + 0] * a.inv_lambda;
+                v.y = kLambdaOne ? abar[4 * t + 1] : abar[4 * t + 1] * a.inv_lambda;
+                v.z = kLambdaOne ? abar[4 * t + 2] : abar[4 * t + 2] * a.inv_lambda;
+                v.w = kLambdaOne ? abar[4 * t + 3] : abar[4 * t + 3] * a.inv_lambda;
+                stream_store(v, d4 + t);
+            }
         }
     }
 }
@@ -282,24 +348,20 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb)
     return a0 < b0 + nb && b0 < a0 + na;
 }
 
-// Grid for a grid-stride loop over `items` work items of one thread each:
-// enough blocks to cover the items, capped at a few waves of blocks per CU.
+// Grid for `items` work items of one thread each.  One block per kBlock items
+// (a one-shot grid dispatched in address order keeps the set of DRAM pages in
+// use compact; measured on MI355X, a plain copy streams at ~6.3 TB/s this way
+// against ~5 TB/s with a fixed grid looping with a large stride).  Kernels
+// keep a stride loop only for grids beyond kMaxBlocks.
+constexpr int64_t kMaxBlocks = (int64_t)1 << 22;
 int grid_for(int64_t items)
 {
-    static thread_local int cap_dev = -1, cap = 0;
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
-    if (dev != cap_dev) {
-        int cus = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
-            cus = 256;
-        cap = cus * 16;
-        cap_dev = dev;
-    }
     const int64_t need = (items + kBlock - 1) / kBlock;
-    return (int)(need < cap ? (need > 0 ? need : 1) : cap);
+    return (int)(need < 1 ? 1 : (need < kMaxBlocks ? need : kMaxBlocks));
 }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int kUnroll4or8(int m) { return m == 4 ? kUnroll<4> : kUnroll<8>; }
 
 struct Shape {
     int64_t numel = 0;
@@ -449,7 +511,7 @@ extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows
     a.lambda = lambda;
     a.inv_tau = (float)(1.0 / (double)tau);
     void* args[] = {&a};
-    if (hipLaunchKernel((const void*)fn, dim3(grid_for(sh.ngroups)), dim3(kBlock), args, 0,
+    if (hipLaunchKernel((const void*)fn, dim3(grid_for(ceil_div(sh.ngroups, kUnroll4or8(m)))), dim3(kBlock), args, 0,
                         stream) != hipSuccess)
         return launch_status("roi_mask_fwd");
     return launch_status("roi_mask_fwd");
@@ -486,7 +548,7 @@ extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, co
     a.tau = tau;
     a.inv_tau = (float)(1.0 / (double)tau);
     void* args[] = {&a};
-    if (hipLaunchKernel((const void*)fn, dim3(grid_for(sh.ngroups)), dim3(kBlock), args, 0,
+    if (hipLaunchKernel((const void*)fn, dim3(grid_for(ceil_div(sh.ngroups, kUnroll4or8(m)))), dim3(kBlock), args, 0,
                         stream) != hipSuccess)
         return launch_status("roi_mask_bwd");
     return launch_status("roi_mask_bwd");
