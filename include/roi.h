@@ -36,9 +36,11 @@
  *    hi32 step);
  *  - u = (2 (x >> 9) + 1) 2^-24, in (0, 1) (Algorithm 1: u ~ Uniform(0,1));
  *  - g = -L(-L(u)) with L the library's deterministic fp32 logarithm
- *    (Algorithm 1: g = -log(-log u)); L(x) = E ln2 + 2 atanh(s) for
- *    x = m 2^E, m in [sqrt(1/2), sqrt(2)), s = (m-1)/(m+1), evaluated by
- *    a fixed sequence of IEEE fp32 operations, so the value is reproducible;
+ *    (Algorithm 1: g = -log(-log u)): x = z 2^k with z in [0.703125, 1.40625),
+ *    a 128-cell table of (1/c, -ln(1/c)) (the two cells touching 1 hold
+ *    (1, 0)), r = fma(z, 1/c, -1), ln(1+r) by its degree-4 series, and
+ *    L = fma(k, ln2, -ln(1/c) + ln(1+r)); a fixed sequence of IEEE fp32
+ *    operations, so the value is reproducible (max error 1.45 ulp);
  *  - kappa = fl(fl(phi / lambda) + g) in fp32 (§3.2 key; §4.2.3 applies the
  *    trick to phi / lambda).
  *  Given (seed, step, elem_offset) the noise is a pure function, so the
@@ -80,7 +82,8 @@ typedef enum {
  *  tau        relaxation temperature, finite, > 0 (used only for soft_mask)
  *  lambda     sampling temperature, finite, > 0 (§4.2.3)
  *  seed, step Philox key and step counter
- *  elem_offset global index of element 0; elem_offset % 4 == 0
+ *  elem_offset global index of element 0; elem_offset % m == 0 (so groups of a
+ *             stack keep their positions in the global index space)
  *  W_masked   bf16 [rows, cols]          (written; required)
  *  soft_mask  fp32 [rows, cols] or NULL  (written when not NULL)
  *  sel_idx    uint8 [rows*cols/m, n] or NULL: the kept indices of each group in

@@ -26,6 +26,9 @@ constexpr uint32_t kWeyl1 = 0xBB67AE85u;
 struct NoiseKey {
     uint32_t k0, k1;           // lo32 / hi32 of the seed
     uint32_t step_lo, step_hi; // counter words 2 and 3
+    uint32_t block_hi;         // counter word 1: hi32 of the block index, the same for
+                               // every element of one launch (launches are split where
+                               // it changes)
 };
 
 __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2,
@@ -35,8 +38,9 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
     for (int r = 0; r < 10; ++r) {
         const uint64_t p0 = (uint64_t)kPhiloxMul0 * (uint64_t)c0;
         const uint64_t p1 = (uint64_t)kPhiloxMul1 * (uint64_t)c2;
-        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        // a ^ b ^ c in one gfx950 three-input bit operation (truth table 0x96)
+        const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c1, k0, 0x96);
+        const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c3, k1, 0x96);
         c1 = (uint32_t)p1;
         c3 = (uint32_t)p0;
         c0 = n0;
@@ -47,19 +51,22 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
     return make_uint4(c0, c1, c2, c3);
 }
 
-// The four words for global elements 4*block .. 4*block+3.
-__device__ __forceinline__ uint4 philox_block(uint64_t block, const NoiseKey& key)
+// The four words for global elements 4*block .. 4*block+3; block_lo is the
+// low 32 bits of the block index (the high 32 bits are key.block_hi).
+// Counter words 1..3 are uniform over the launch, so the first two rounds
+// run partly on the scalar unit.
+__device__ __forceinline__ uint4 philox_block(uint32_t block_lo, const NoiseKey& key)
 {
-    return philox4x32_10((uint32_t)block, (uint32_t)(block >> 32), key.step_lo, key.step_hi,
-                         key.k0, key.k1);
+    return philox4x32_10(block_lo, key.block_hi, key.step_lo, key.step_hi, key.k0, key.k1);
 }
 
 // u = (2 (x >> 9) + 1) 2^-24: odd points of the 2^-24 grid, in (0, 1).
 // Evaluated as (1 + (x >> 9) 2^-23) - (1 - 2^-24): the first term is the
-// float with mantissa x >> 9, and the difference is exact.
+// float with mantissa x >> 9 (one funnel shift of 0x7F:x by 9), and the
+// difference is exact.
 __device__ __forceinline__ float uniform_from_word(uint32_t x)
 {
-    return __uint_as_float((x >> 9) | 0x3F800000u) - 0x1.fffffep-1f;
+    return __uint_as_float(__builtin_amdgcn_alignbit(0x7Fu, x, 9)) - 0x1.fffffep-1f;
 }
 
 // Deterministic fp32 natural logarithm for finite normal x > 0, table-driven
@@ -135,7 +142,7 @@ __device__ __forceinline__ float det_log_bits(uint32_t ix, const float2* tab)
     const uint32_t t = ix - kLogZBaseBits;
     const int cell = (int)((t >> 16) & (kLogCells - 1));
     const int k = (int)t >> 23;
-    const float z = __uint_as_float(ix - (t & 0xFF800000u));
+    const float z = __uint_as_float((t & 0x007FFFFFu) + kLogZBaseBits); // = ix - (t & 0xFF800000)
     const float2 c = tab[cell];
     const float r = __builtin_fmaf(z, c.x, -1.0f);
     float p = __builtin_fmaf(r, -0.25f, kThird);
@@ -151,13 +158,13 @@ __device__ __forceinline__ float det_log(float x, const float2* tab)
     return det_log_bits(__float_as_uint(x), tab);
 }
 
-// Returns ln(-ln u) = -g for the Gumbel noise g = -log(-log u).  ln u < 0, so
-// the bits of -ln u are those of ln u with the sign bit cleared.
+// Returns ln(-ln u) = -g for the Gumbel noise g = -log(-log u).  ln u < 0 for
+// every u < 1, so the bits of -ln u are those of ln u minus the sign bit.
 __device__ __forceinline__ float neg_gumbel_from_word(uint32_t x, const float2* tab)
 {
     const float u = uniform_from_word(x);
     const float lu = det_log(u, tab);
-    return det_log_bits(__float_as_uint(lu) & 0x7FFFFFFFu, tab);
+    return det_log_bits(__float_as_uint(lu) - 0x80000000u, tab);
 }
 
 __device__ __forceinline__ float gumbel_from_word(uint32_t x, const float2* tab)

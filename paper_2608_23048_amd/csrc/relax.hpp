@@ -29,6 +29,52 @@ __device__ __forceinline__ void rank_keys(const float (&kappa)[M], int (&rank)[M
     }
 }
 
+// Hard top-n of four keys through a 64-entry table.  The six pairwise
+// comparisons c_ij = (kappa_i >= kappa_j), i < j (ties to the lower index),
+// form a 6-bit code; since >= on finite floats is transitive, the code fixes
+// every rank (rank_j = number of entries that beat j).  Entry `code` holds the
+// two bf16-pair masks that keep the entries of rank < n, and the selection
+// order packed one index per byte.
+struct Top4Entry {
+    uint32_t m01, m23, order, unused;
+};
+
+struct Top4Table {
+    Top4Entry e[64];
+};
+
+constexpr Top4Table make_top4_table(int n)
+{
+    Top4Table t{};
+    for (int code = 0; code < 64; ++code) {
+        const int c01 = code & 1, c02 = (code >> 1) & 1, c03 = (code >> 2) & 1;
+        const int c12 = (code >> 3) & 1, c13 = (code >> 4) & 1, c23 = (code >> 5) & 1;
+        const int rank[4] = {(1 - c01) + (1 - c02) + (1 - c03), c01 + (1 - c12) + (1 - c13),
+                             c02 + c12 + (1 - c23), c03 + c13 + c23};
+        uint32_t m01 = 0, m23 = 0, order = 0;
+        if (rank[0] < n) m01 |= 0x0000FFFFu;
+        if (rank[1] < n) m01 |= 0xFFFF0000u;
+        if (rank[2] < n) m23 |= 0x0000FFFFu;
+        if (rank[3] < n) m23 |= 0xFFFF0000u;
+        for (int j = 0; j < 4; ++j)
+            if (rank[j] < n) order |= (uint32_t)j << (8 * rank[j]);
+        t.e[code].m01 = m01;
+        t.e[code].m23 = m23;
+        t.e[code].order = order;
+        t.e[code].unused = 0;
+    }
+    return t;
+}
+
+template <int N>
+__device__ const Top4Table kTop4Table = make_top4_table(N);
+
+__device__ __forceinline__ uint32_t top4_code(const float (&k)[4])
+{
+    return (k[0] >= k[1] ? 1u : 0u) | (k[0] >= k[2] ? 2u : 0u) | (k[0] >= k[3] ? 4u : 0u) |
+           (k[1] >= k[2] ? 8u : 0u) | (k[1] >= k[3] ? 16u : 0u) | (k[2] >= k[3] ? 32u : 0u);
+}
+
 // One record per relaxation step, kept for the reverse sweep.
 template <int M>
 struct StepRec {

@@ -48,7 +48,7 @@ struct FwdArgs {
     float* S;
     uint8_t* idx;
     int64_t ngroups;
-    uint64_t block0; // elem_offset / 4
+    uint32_t block0; // low 32 bits of elem_offset / 4 (the high 32 are key.block_hi)
     NoiseKey key;
     float lambda;
     float inv_tau;
@@ -60,7 +60,7 @@ struct BwdArgs {
     const float* phi;
     float* dphi;
     int64_t ngroups;
-    uint64_t block0;
+    uint32_t block0;
     NoiseKey key;
     float lambda;
     float inv_lambda;
@@ -145,6 +145,22 @@ __device__ __forceinline__ void store_masked(uint16_t* p, const uint32_t (&w)[M]
     }
 }
 
+// n index bytes of a group, already packed (byte r = index of rank r).
+template <int N>
+__device__ __forceinline__ void store_order(uint8_t* p, uint32_t packed)
+{
+    if constexpr (N == 1) {
+        *p = (uint8_t)packed;
+    } else if constexpr (N == 2) {
+        *reinterpret_cast<uint16_t*>(p) = (uint16_t)packed;
+    } else if constexpr (N == 4) {
+        *reinterpret_cast<uint32_t*>(p) = packed;
+    } else {
+#pragma unroll
+        for (int r = 0; r < N; ++r) p[r] = (uint8_t)(packed >> (8 * r));
+    }
+}
+
 // Selected indices in selection order: byte r holds the index of rank r.
 template <int M, int N>
 __device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
@@ -168,7 +184,7 @@ __device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
 }
 
 template <int M, bool kLambdaOne>
-__device__ __forceinline__ void group_keys(const float (&phi)[M], uint64_t block, const NoiseKey& key,
+__device__ __forceinline__ void group_keys(const float (&phi)[M], uint32_t block, const NoiseKey& key,
                                            float lambda, const float2* tab, float (&kappa)[M])
 {
 #pragma unroll
@@ -190,7 +206,12 @@ template <int M, int N, bool kWantS, bool kWantIdx, bool kLambdaOne>
 __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
 {
     __shared__ float2 tab[kLogCells];
+    __shared__ Top4Entry top4[64];
     fill_log_table(tab);
+    if constexpr (M == 4) {
+        if (threadIdx.x >= kLogCells && threadIdx.x < kLogCells + 64)
+            top4[threadIdx.x - kLogCells] = kTop4Table<N>.e[threadIdx.x - kLogCells];
+    }
     __syncthreads();
     constexpr int U = kUnroll<M>;
     const int64_t chunk = (int64_t)kBlock * U;
@@ -211,12 +232,20 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
             const int64_t q = base + u * kBlock + threadIdx.x;
             if (q >= a.ngroups) continue;
             float kappa[M];
-            group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda,
+            group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint32_t)q * (M / 4), a.key, a.lambda,
                                       tab, kappa);
-            int rank[M];
-            rank_keys<M>(kappa, rank);
-            store_masked<M>(a.Wm + q * M, w[u], rank, N);
-            if (kWantIdx) store_idx<M, N>(a.idx + q * N, rank);
+            if constexpr (M == 4) {
+                const Top4Entry t4 = top4[top4_code(kappa)];
+                const u32x2 v = {(w[u][0] | (w[u][1] << 16)) & t4.m01,
+                                 (w[u][2] | (w[u][3] << 16)) & t4.m23};
+                stream_store(v, reinterpret_cast<u32x2*>(a.Wm + q * M));
+                if (kWantIdx) store_order<N>(a.idx + q * N, t4.order);
+            } else {
+                int rank[M];
+                rank_keys<M>(kappa, rank);
+                store_masked<M>(a.Wm + q * M, w[u], rank, N);
+                if (kWantIdx) store_idx<M, N>(a.idx + q * N, rank);
+            }
             if (kWantS) {
                 float S[M];
                 StepRec<M> unused[N]; // not written when records are not kept
@@ -258,7 +287,7 @@ __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
             const int64_t q = base + u * kBlock + threadIdx.x;
             if (q >= a.ngroups) continue;
             float kappa[M];
-            group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint64_t)q * (M / 4), a.key, a.lambda,
+            group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint32_t)q * (M / 4), a.key, a.lambda,
                                       tab, kappa);
             // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
             float sbar[M];
@@ -286,7 +315,7 @@ __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
 
 // Noise inspection: one Philox call per 4 consecutive elements.
 __global__ __launch_bounds__(kBlock) void noise_kernel(uint32_t* words, float* gum, int64_t count,
-                                                       uint64_t block0, NoiseKey key)
+                                                       uint32_t block0, NoiseKey key)
 {
     __shared__ float2 tab[kLogCells];
     fill_log_table(tab);
@@ -294,7 +323,7 @@ __global__ __launch_bounds__(kBlock) void noise_kernel(uint32_t* words, float* g
     const int64_t nblocks = (count + 3) / 4;
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     for (int64_t b = (int64_t)blockIdx.x * kBlock + threadIdx.x; b < nblocks; b += stride) {
-        const uint4 x = philox_block(block0 + (uint64_t)b, key);
+        const uint4 x = philox_block(block0 + (uint32_t)b, key);
         const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
@@ -385,9 +414,9 @@ int check_shape(int64_t rows, int64_t cols, int n, int m, float tau, float lambd
         return fail(ROI_E_INVAL, "tau must be finite and > 0");
     if (!(lambda > 0.0f) || !std::isfinite(lambda))
         return fail(ROI_E_INVAL, "lambda must be finite and > 0");
-    if (elem_offset % 4 != 0)
-        return fail(ROI_E_INVAL, "elem_offset (%llu) must be a multiple of 4",
-                    (unsigned long long)elem_offset);
+    if (elem_offset % (uint64_t)m != 0)
+        return fail(ROI_E_INVAL, "elem_offset (%llu) must be a multiple of m (%d)",
+                    (unsigned long long)elem_offset, m);
     const int64_t numel = rows * cols;
     if (elem_offset > UINT64_MAX - (uint64_t)numel)
         return fail(ROI_E_INVAL, "elem_offset + rows * cols overflows 64 bits");
@@ -396,14 +425,35 @@ int check_shape(int64_t rows, int64_t cols, int n, int m, float tau, float lambd
     return ROI_OK;
 }
 
-NoiseKey make_key(uint64_t seed, uint64_t step)
+NoiseKey make_key(uint64_t seed, uint64_t step, uint64_t block)
 {
     NoiseKey k;
     k.k0 = (uint32_t)seed;
     k.k1 = (uint32_t)(seed >> 32);
     k.step_lo = (uint32_t)step;
     k.step_hi = (uint32_t)(step >> 32);
+    k.block_hi = (uint32_t)(block >> 32);
     return k;
+}
+
+// Calls launch(first, count, elem0) for consecutive pieces of [0, items) --
+// items of `per_item` elements starting at global element elem_offset -- so
+// that within a piece every Philox block index (element / 4) has the same high
+// 32 bits.  Pieces end at multiples of 2^34 elements, which per_item divides.
+template <typename F>
+int for_each_piece(uint64_t elem_offset, int64_t items, int64_t per_item, F&& launch)
+{
+    int64_t done = 0;
+    while (done < items) {
+        const uint64_t e0 = elem_offset + (uint64_t)done * (uint64_t)per_item;
+        const uint64_t boundary = ((e0 >> 34) + 1) << 34;
+        const uint64_t fit = (boundary - e0) / (uint64_t)per_item;
+        const int64_t left = items - done;
+        const int64_t count = fit < (uint64_t)left ? (int64_t)fit : left;
+        if (int st = launch(done, count, e0)) return st;
+        done += count;
+    }
+    return ROI_OK;
 }
 
 int launch_status(const char* what)
@@ -499,22 +549,27 @@ extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows
     }
     FwdFn fn = select_fwd(m, n, soft_mask != nullptr, sel_idx != nullptr, lambda == 1.0f);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
-    FwdArgs a;
-    a.W = W;
-    a.phi = logits;
-    a.Wm = W_masked;
-    a.S = soft_mask;
-    a.idx = sel_idx;
-    a.ngroups = sh.ngroups;
-    a.block0 = elem_offset / 4;
-    a.key = make_key(seed, step);
-    a.lambda = lambda;
-    a.inv_tau = (float)(1.0 / (double)tau);
-    void* args[] = {&a};
-    if (hipLaunchKernel((const void*)fn, dim3(grid_for(ceil_div(sh.ngroups, kUnroll4or8(m)))), dim3(kBlock), args, 0,
-                        stream) != hipSuccess)
+    const NoiseKey key = make_key(seed, step, 0);
+    const float inv_tau = (float)(1.0 / (double)tau);
+    return for_each_piece(elem_offset, sh.ngroups, m, [&](int64_t g0, int64_t ng, uint64_t e0) {
+        FwdArgs a;
+        a.W = W + g0 * m;
+        a.phi = logits + g0 * m;
+        a.Wm = W_masked + g0 * m;
+        a.S = soft_mask ? soft_mask + g0 * m : nullptr;
+        a.idx = sel_idx ? sel_idx + g0 * n : nullptr;
+        a.ngroups = ng;
+        a.block0 = (uint32_t)(e0 / 4);
+        a.key = key;
+        a.key.block_hi = (uint32_t)((e0 / 4) >> 32);
+        a.lambda = lambda;
+        a.inv_tau = inv_tau;
+        void* args[] = {&a};
+        if (hipLaunchKernel((const void*)fn, dim3(grid_for(ceil_div(ng, kUnroll4or8(m)))),
+                            dim3(kBlock), args, 0, stream) != hipSuccess)
+            return launch_status("roi_mask_fwd");
         return launch_status("roi_mask_fwd");
-    return launch_status("roi_mask_fwd");
+    });
 }
 
 extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
@@ -535,23 +590,29 @@ extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, co
         return fail(ROI_E_INVAL, "grad_logits must not overlap the inputs");
     BwdFn fn = select_bwd(m, n, lambda == 1.0f);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
-    BwdArgs a;
-    a.G = grad_W_masked;
-    a.W = W;
-    a.phi = logits;
-    a.dphi = grad_logits;
-    a.ngroups = sh.ngroups;
-    a.block0 = elem_offset / 4;
-    a.key = make_key(seed, step);
-    a.lambda = lambda;
-    a.inv_lambda = (float)(1.0 / (double)lambda);
-    a.tau = tau;
-    a.inv_tau = (float)(1.0 / (double)tau);
-    void* args[] = {&a};
-    if (hipLaunchKernel((const void*)fn, dim3(grid_for(ceil_div(sh.ngroups, kUnroll4or8(m)))), dim3(kBlock), args, 0,
-                        stream) != hipSuccess)
+    const NoiseKey key = make_key(seed, step, 0);
+    const float inv_lambda = (float)(1.0 / (double)lambda);
+    const float inv_tau = (float)(1.0 / (double)tau);
+    return for_each_piece(elem_offset, sh.ngroups, m, [&](int64_t g0, int64_t ng, uint64_t e0) {
+        BwdArgs a;
+        a.G = grad_W_masked + g0 * m;
+        a.W = W + g0 * m;
+        a.phi = logits + g0 * m;
+        a.dphi = grad_logits + g0 * m;
+        a.ngroups = ng;
+        a.block0 = (uint32_t)(e0 / 4);
+        a.key = key;
+        a.key.block_hi = (uint32_t)((e0 / 4) >> 32);
+        a.lambda = lambda;
+        a.inv_lambda = inv_lambda;
+        a.tau = tau;
+        a.inv_tau = inv_tau;
+        void* args[] = {&a};
+        if (hipLaunchKernel((const void*)fn, dim3(grid_for(ceil_div(ng, kUnroll4or8(m)))),
+                            dim3(kBlock), args, 0, stream) != hipSuccess)
+            return launch_status("roi_mask_bwd");
         return launch_status("roi_mask_bwd");
-    return launch_status("roi_mask_bwd");
+    });
 }
 
 extern "C" int roi_gumbel_noise(uint64_t seed, uint64_t step, uint64_t elem_offset, int64_t count,
@@ -567,9 +628,12 @@ extern "C" int roi_gumbel_noise(uint64_t seed, uint64_t step, uint64_t elem_offs
         return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
     if (overlap(words, (size_t)count * 4, gumbel, (size_t)count * 4))
         return fail(ROI_E_INVAL, "words and gumbel must not overlap");
-    hipLaunchKernelGGL(noise_kernel, dim3(grid_for((count + 3) / 4)), dim3(kBlock), 0, stream,
-                       words, gumbel, count, elem_offset / 4, make_key(seed, step));
-    return launch_status("roi_gumbel_noise");
+    return for_each_piece(elem_offset, count, 1, [&](int64_t i0, int64_t cnt, uint64_t e0) {
+        hipLaunchKernelGGL(noise_kernel, dim3(grid_for((cnt + 3) / 4)), dim3(kBlock), 0, stream,
+                           words ? words + i0 : nullptr, gumbel ? gumbel + i0 : nullptr, cnt,
+                           (uint32_t)(e0 / 4), make_key(seed, step, e0 / 4));
+        return launch_status("roi_gumbel_noise");
+    });
 }
 
 extern "C" int roi_gumbel_from_words(const uint32_t* words, int64_t count, float* gumbel,

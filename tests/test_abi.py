@@ -77,6 +77,7 @@ def bwd(L, **kw):
     (dict(lam=0.0), roi.ROI_E_INVAL),
     (dict(lam=math.nan), roi.ROI_E_INVAL),
     (dict(off=2), roi.ROI_E_INVAL),
+    (dict(off=4, m=8, n=4), roi.ROI_E_INVAL),
     (dict(off=2**64 - 4), roi.ROI_E_INVAL),
     (dict(W=None), roi.ROI_E_INVAL),
     (dict(Wm=None), roi.ROI_E_INVAL),

@@ -48,7 +48,8 @@ def run_case(dev, rows, cols, n, m, tau, lam, seed, step, off, case_seed, w_std=
 def test_noise_words_and_gumbel_bit_exact(dev):
     import torch
     for seed, step, off, count in [(0, 0, 0, (1 << 20) + 3), (0xDEADBEEF12345678, 7, 1 << 34, 4099),
-                                   (1, 2**40 + 3, 6525288448 - 4096, 4096)]:
+                                   (1, 2**40 + 3, 6525288448 - 4096, 4096),
+                                   (3, 1, 2**34 - 40, 101)]:
         say(f"noise seed={seed} step={step} off={off} count={count}")
         words, g = roi.gumbel_noise(count, seed, step, off, device=dev)
         torch.cuda.synchronize()
@@ -89,11 +90,14 @@ SMALL = [
     (33, 64, 3, 4, 1.3, 0.6, 2, 3, 12),
     (33, 64, 4, 4, 1.0, 1.0, 2, 3, 0),
     (48, 96, 4, 8, 0.5, 1.0, 7, 4, 0),
-    (61, 88, 2, 8, 1.0, 2.0, 8, 5, 4),
-    (61, 88, 1, 8, 0.3, 1.0, 8, 5, 4),
-    (61, 88, 7, 8, 1.0, 1.0, 8, 5, 4),
+    (61, 88, 2, 8, 1.0, 2.0, 8, 5, 8),
+    (61, 88, 1, 8, 0.3, 1.0, 8, 5, 8),
+    (61, 88, 7, 8, 1.0, 1.0, 8, 5, 8),
     (61, 88, 8, 8, 0.9, 1.0, 9, 6, 0),
     (17, 8, 6, 8, 0.25, 0.5, 4, 2**33, 2**36),
+    # the Philox block index crosses a multiple of 2^32 inside the call
+    (40, 64, 2, 4, 1.0, 1.0, 6, 3, 2**34 - 4 * 256),
+    (25, 64, 4, 8, 0.5, 1.0, 6, 3, 2**35 - 8 * 100),
 ]
 
 
