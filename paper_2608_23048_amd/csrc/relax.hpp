@@ -75,12 +75,30 @@ __device__ __forceinline__ uint32_t top4_code(const float (&k)[4])
            (k[1] >= k[2] ? 8u : 0u) | (k[1] >= k[3] ? 16u : 0u) | (k[2] >= k[3] ? 32u : 0u);
 }
 
+// Sums over "all entries but j" for every j, from prefix and suffix sums
+// (no subtraction, so a dominant entry never cancels the others away).
+template <int M>
+__device__ __forceinline__ void sums_but_one(const float (&x)[M], float (&out)[M], float& total)
+{
+    float pre[M], suf[M];
+    pre[0] = x[0];
+#pragma unroll
+    for (int j = 1; j < M; ++j) pre[j] = pre[j - 1] + x[j];
+    suf[M - 1] = x[M - 1];
+#pragma unroll
+    for (int j = M - 2; j >= 0; --j) suf[j] = suf[j + 1] + x[j];
+    out[0] = suf[1];
+    out[M - 1] = pre[M - 2];
+#pragma unroll
+    for (int j = 1; j < M - 1; ++j) out[j] = pre[j - 1] + suf[j + 1];
+    total = pre[M - 1];
+}
+
 // One record per relaxation step, kept for the reverse sweep.
 template <int M>
 struct StepRec {
-    float mu[M];   // mu^(k)
-    float om_star; // 1 - mu^(k)_{i*}, evaluated as the sum of the other entries
-    int istar;     // index of the largest adjusted key at step k
+    float mu[M]; // mu^(k)
+    float om[M]; // 1 - mu^(k), evaluated as the sum of the other entries over the total
 };
 
 // Relaxation (§3.2 recursion, Algorithm 1) in fp32:
@@ -90,22 +108,15 @@ struct StepRec {
 // exp2(b - max b) and the update is b += log2(1 - mu) / tau: the same values
 // with one multiply fewer per element and step.  Subtracting the group's
 // largest key first keeps the competing entries near 0, where fp32 is
-// densest, and makes b = 0 exactly at the first argmax.
-// 1 - mu_i: for i != i* it is >= 1/2, so 1 - mu_i loses nothing; for the
-// current argmax i* it is rest / T with rest = the sum of the other
-// exponentials (no cancellation).  log(1 - mu) is floored at log(FLT_MIN).
+// densest.  1 - mu_j is evaluated as (sum of the other exponentials) / total,
+// which never cancels, and log(1 - mu) is floored at log(FLT_MIN).
 template <int M, int N, bool kWantS, bool kKeep>
 __device__ __forceinline__ void relax_forward(const float (&kappa)[M], float inv_tau,
                                               float (&S)[M], StepRec<M> (&rec)[N])
 {
     float kmax = kappa[0];
-    int istar = 0;
 #pragma unroll
-    for (int j = 1; j < M; ++j) {
-        const bool gt = kappa[j] > kmax;
-        kmax = gt ? kappa[j] : kmax;
-        istar = gt ? j : istar;
-    }
+    for (int j = 1; j < M; ++j) kmax = fmaxf(kmax, kappa[j]);
     const float c = kLog2e * inv_tau;
     float b[M];
 #pragma unroll
@@ -115,98 +126,82 @@ __device__ __forceinline__ void relax_forward(const float (&kappa)[M], float inv
     }
 #pragma unroll
     for (int k = 0; k < N; ++k) {
-        float bmax = 0.0f; // step 1: b[istar] == 0 exactly
-        if (k > 0) {
-            bmax = b[0];
-            istar = 0;
-#pragma unroll
-            for (int j = 1; j < M; ++j) {
-                const bool gt = b[j] > bmax;
-                bmax = gt ? b[j] : bmax;
-                istar = gt ? j : istar;
-            }
-        }
         float e[M];
-        float rest = 0.0f;
+        if (k == 0) { // the largest b is exactly 0
+#pragma unroll
+            for (int j = 0; j < M; ++j) e[j] = __builtin_amdgcn_exp2f(b[j]);
+        } else {
+            float bmax = b[0];
+#pragma unroll
+            for (int j = 1; j < M; ++j) bmax = fmaxf(bmax, b[j]);
+#pragma unroll
+            for (int j = 0; j < M; ++j) e[j] = __builtin_amdgcn_exp2f(b[j] - bmax);
+        }
+        float others[M], total;
+        sums_but_one<M>(e, others, total);
+        const float inv_total = __builtin_amdgcn_rcpf(total);
 #pragma unroll
         for (int j = 0; j < M; ++j) {
-            e[j] = __builtin_amdgcn_exp2f(k > 0 ? b[j] - bmax : b[j]); // e[istar] == 1 exactly
-            rest += (j == istar) ? 0.0f : e[j];
-        }
-        const float inv_total = __builtin_amdgcn_rcpf(1.0f + rest);
-        const float om_star = rest * inv_total;
-        float mu[M];
-#pragma unroll
-        for (int j = 0; j < M; ++j) {
-            mu[j] = e[j] * inv_total;
-            if (kWantS) S[j] += mu[j];
-            if (kKeep) rec[k].mu[j] = mu[j];
-        }
-        if (kKeep) {
-            rec[k].om_star = om_star;
-            rec[k].istar = istar;
-        }
-        if (k + 1 < N) {
-            const float om_star_f = fmaxf(om_star, kFltMin);
-#pragma unroll
-            for (int j = 0; j < M; ++j) {
-                const float om = (j == istar) ? om_star_f : 1.0f - mu[j];
-                b[j] = __builtin_fmaf(__builtin_amdgcn_logf(om), inv_tau, b[j]);
+            const float mu = e[j] * inv_total;
+            const float om = others[j] * inv_total;
+            if (kWantS) S[j] += mu;
+            if (kKeep) {
+                rec[k].mu[j] = mu;
+                rec[k].om[j] = om;
             }
+            if (k + 1 < N)
+                b[j] = __builtin_fmaf(__builtin_amdgcn_logf(fmaxf(om, kFltMin)), inv_tau, b[j]);
         }
     }
 }
 
 // Reverse sweep of relax_forward: given sbar = dL/dS, returns dL/dkappa.
 // Chain rule through the recursion, with a = dL/dalpha^(k+1) (0 above the
-// last step), omega = 1 - mu^(k):
-//   mubar_i = sbar_i - a_i / omega_i          (0 instead where the floor was hit)
-//   dL/dalpha^(k)_i = a_i + (mu_i / tau) (mubar_i - sum_j mu_j mubar_j).
-// For i != i* this is evaluated as written (mu_i <= 1/2, omega_i >= 1/2).  For
-// i* the product mu_i* * (...) may cancel catastrophically when mu_i* ~ 1, so
-// the identity omega_i* mubar_i* = omega_i* sbar_i* - a_i* is used:
-//   dL/dalpha^(k)_i* = a_i* (omega* + tau - 1) / tau
-//                      + (mu_i* / tau) (omega* sbar_i* - sum_{j != i*} mu_j mubar_j).
-// A floored omega* is replaced by +inf, so that a_i* / omega* = 0.
+// last step) and omega = 1 - mu^(k):
+//   mubar_j = sbar_j - a_j / omega_j            (no a_j / omega_j where the floor was hit)
+//   dL/dalpha^(k)_j = a_j + (mu_j / tau) (mubar_j - sum_l mu_l mubar_l).
+// With 1 - mu_j = omega_j and omega_j mubar_j = omega_j sbar_j - a_j this is
+//   dL/dalpha^(k)_j = a_j keep_j + (mu_j / tau) (omega_j sbar_j - sum_{l != j} mu_l mubar_l),
+//   keep_j = 1 - mu_j / tau = (omega_j + tau - 1) / tau   (1 where the floor was hit),
+// the same form for every j, with no difference of two large numbers when
+// mu_j is close to 1 (the sum over l != j is built from prefix and suffix
+// sums).
 template <int M, int N>
 __device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const float (&sbar)[M],
                                                float tau, float inv_tau, float (&abar)[M])
 {
-#pragma unroll
-    for (int j = 0; j < M; ++j) abar[j] = 0.0f;
+    const float keep0 = (tau - 1.0f) * inv_tau;
 #pragma unroll
     for (int k = N - 1; k >= 0; --k) {
         const bool has_next = (k + 1 < N);
-        const int istar = rec[k].istar;
-        const float oms = rec[k].om_star;
-        const bool floored = !(oms >= kFltMin);
         float t[M];
-        float p_all = 0.0f, p_excl = 0.0f, sbar_is = 0.0f, abar_is = 0.0f;
-        float mubar[M];
 #pragma unroll
         for (int j = 0; j < M; ++j) {
-            const bool is = (j == istar);
-            const float mu = rec[k].mu[j];
-            mubar[j] = sbar[j];
+            float mubar = sbar[j];
             if (has_next) {
-                const float om = is ? (floored ? __builtin_inff() : oms) : 1.0f - mu;
-                mubar[j] = __builtin_fmaf(-abar[j], __builtin_amdgcn_rcpf(om), sbar[j]);
+                const float om = rec[k].om[j];
+                const float r = abar[j] * __builtin_amdgcn_rcpf(om);
+                mubar = (om >= kFltMin) ? mubar - r : mubar;
             }
-            t[j] = mu * mubar[j];
-            p_all += t[j];
-            p_excl += is ? 0.0f : t[j];
-            sbar_is = is ? sbar[j] : sbar_is;
-            if (has_next) abar_is = is ? abar[j] : abar_is;
+            t[j] = rec[k].mu[j] * mubar;
         }
-        const float inner_is = __builtin_fmaf(oms, sbar_is, -p_excl);
-        float carry_is = 0.0f;
-        if (has_next) carry_is = abar_is * (floored ? 1.0f : (oms + (tau - 1.0f)) * inv_tau);
+        float q[M], unused;
+        sums_but_one<M>(t, q, unused);
 #pragma unroll
         for (int j = 0; j < M; ++j) {
-            const bool is = (j == istar);
+            const float om = rec[k].om[j];
+            const float inner = __builtin_fmaf(om, sbar[j], -q[j]);
             const float m_t = rec[k].mu[j] * inv_tau;
-            const float inner = is ? inner_is : mubar[j] - p_all;
-            const float carry = has_next ? (is ? carry_is : abar[j]) : 0.0f;
+            float carry = 0.0f;
+            if (has_next) {
+                // keep = 1 - mu/tau, from mu while mu < 1/2 and from omega above (where
+                // 1 - mu would cancel); 1 where the floor was hit
+                const float mu = rec[k].mu[j];
+                float keep = mu < 0.5f ? __builtin_fmaf(-mu, inv_tau, 1.0f)
+                                       : __builtin_fmaf(om, inv_tau, keep0);
+                keep = (om >= kFltMin) ? keep : 1.0f;
+                carry = abar[j] * keep;
+            }
             abar[j] = __builtin_fmaf(m_t, inner, carry);
         }
     }
