@@ -25,6 +25,95 @@ if ROOT not in sys.path:
 
 METRIC = "masked weights/sec (mask fwd+bwd) and achieved HBM GB/s vs peak, 7B-class 2:4"
 HBM_PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "roi_mask_qwen7b_stack_2of4_traffic.json")
+
+
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources: measured traffic is reported only for the
+    kernels it was measured on."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_23048_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".hpp", ".h")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """Per-launch HBM bytes of the dominant kernel from the committed rocprofv3
+    counter summary, or None when it is missing or the kernels changed since."""
+    import json as _json
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    rec = _json.load(open(TRAFFIC_FILE))
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec
+
+
+def copy_calibration(nbytes: int) -> int:
+    """A plain device-to-device copy of nbytes (torch's copy kernel), run under
+    rocprofv3 --pmc to learn what FETCH_SIZE / WRITE_SIZE read for known bytes."""
+    import torch
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes}), flush=True)
+    return 0
+
+
+def pmc_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes, numel, n,
+                m) -> int:
+    """Turn four rocprofv3 --pmc counter CSVs (FETCH_SIZE and WRITE_SIZE of the
+    benchmark and of the calibration copy) into the committed traffic record."""
+    import csv
+    import json as _json
+
+    def per_kernel(path, counter):
+        vals = {}
+        for r in csv.DictReader(open(path)):
+            if r.get("Counter_Name") != counter:
+                continue
+            name = r["Kernel_Name"]
+            vals.setdefault(name, []).append(float(r["Counter_Value"]))
+        return vals
+
+    def pick(vals, key):
+        hits = [v for k, v in vals.items() if key in k]
+        flat = [x for v in hits for x in v]
+        return sum(flat) / len(flat) if flat else None
+
+    cf = per_kernel(copy_fetch_csv, "FETCH_SIZE")
+    cw = per_kernel(copy_write_csv, "WRITE_SIZE")
+    copy_bytes = int(copy_bytes)
+    # the calibration copy is the HIP runtime's device-to-device copy kernel
+    copy_fetch = pick(cf, "copyBuffer")
+    copy_write = pick(cw, "copyBuffer")
+    fetch_scale = copy_bytes / (copy_fetch * 1024.0) if copy_fetch else None
+    write_scale = copy_bytes / (copy_write * 1024.0) if copy_write else None
+    f = per_kernel(fetch_csv, "FETCH_SIZE")
+    w = per_kernel(write_csv, "WRITE_SIZE")
+    bf, bb = algorithmic_bytes(n, m)
+    out = {"kernel_source_hash": kernel_source_hash(), "copy_bytes": copy_bytes,
+           "fetch_scale": fetch_scale, "write_scale": write_scale, "kernels": {}}
+    for key, alg in (("fwd_lane_kernel", bf), ("bwd_lane_kernel", bb)):
+        fk, wk = pick(f, key), pick(w, key)
+        if fk is None or wk is None:
+            continue
+        rd = fk * 1024.0 * fetch_scale
+        wr = wk * 1024.0 * write_scale
+        out["kernels"][key] = {"fetch_kib": fk, "write_kib": wk, "read_bytes": rd,
+                               "write_bytes": wr, "traffic_bytes": rd + wr,
+                               "algorithmic_bytes": alg * numel,
+                               "traffic_over_algorithmic": (rd + wr) / (alg * numel)}
+    _json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+    print(_json.dumps(out), flush=True)
+    return 0
 
 
 def algorithmic_bytes(n: int, m: int) -> tuple[float, float]:
@@ -62,7 +151,18 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="qwen2.5-7b-stack-2:4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (PMC calibration)")
+    ap.add_argument("--pmc-summary", nargs=5,
+                    metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE", "COPY_BYTES"),
+                    help="write the traffic record from rocprofv3 --pmc counter CSVs")
     args = ap.parse_args()
+    if args.copy_calibration:
+        return copy_calibration(args.copy_calibration)
+    if args.pmc_summary:
+        from paper_2608_23048_amd import workloads as wl
+        work = wl.WORKLOADS[args.workload]
+        return pmc_summary(*args.pmc_summary, work.numel, work.n, work.m)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the sampler needs no collectives, and this build "
               "runs and reports a single MI355X (pass --gpus 1).", file=sys.stderr)
@@ -124,6 +224,12 @@ def main() -> int:
     fwd_gbps = bf * numel / (fwd_avg * 1e-3) / 1e9
     bwd_gbps = bb * numel / (bwd_avg * 1e-3) / 1e9
     dominant = ("roi_mask_bwd", bwd_gbps, bb) if bwd_avg >= fwd_avg else ("roi_mask_fwd", fwd_gbps, bf)
+    traffic = None
+    rec = measured_traffic() if work.name == "qwen2.5-7b-stack-2:4" else None
+    if rec is not None:
+        key = "bwd_lane_kernel" if dominant[0] == "roi_mask_bwd" else "fwd_lane_kernel"
+        if key in rec["kernels"]:
+            traffic = rec["kernels"][key]["traffic_bytes"]
     value = numel * args.steps / elapsed
     ms_per_step = elapsed * 1e3 / args.steps
     print(f"# timed {args.steps} steps: {ms_per_step:.3f} ms/step, fwd {fwd_avg:.3f} ms "
@@ -173,7 +279,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": dominant[1] / HBM_PEAK_GBPS,
-            "traffic": None,
+            "traffic": traffic,
         },
         "cpu_baseline": cpu,
     }
