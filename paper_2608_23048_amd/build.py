@@ -19,7 +19,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libroi.so")
-SOURCES = [os.path.join(CSRC, "roi.hip")]
+SOURCES = [os.path.join(CSRC, "roi.hip"), os.path.join(CSRC, "wide.hip")]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -44,13 +44,27 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False, extra_flags: list[str] | None = None) -> str:
-    """Compile libroi.so for gfx950 (always recompiles)."""
+    """Compile libroi.so for gfx950 (always recompiles; the translation units
+    compile in parallel, then link)."""
+    import tempfile
     tmp = f"{LIB_PATH}.tmp{os.getpid()}"
-    cmd = [hipcc(), *HIPCC_FLAGS, *(extra_flags or []), f"-I{INCLUDE}", f"-I{CSRC}", *SOURCES,
-           "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+    common = [*HIPCC_FLAGS, *(extra_flags or []), f"-I{INCLUDE}", f"-I{CSRC}"]
+    with tempfile.TemporaryDirectory() as td:
+        objs, procs = [], []
+        for src in SOURCES:
+            obj = os.path.join(td, os.path.basename(src) + ".o")
+            cmd = [hipcc(), *[f for f in common if f != "-shared"], "-c", src, "-o", obj]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            procs.append((subprocess.Popen(cmd), cmd))
+            objs.append(obj)
+        for p, cmd in procs:
+            if p.wait() != 0:
+                raise subprocess.CalledProcessError(p.returncode, cmd)
+        link = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+        if verbose:
+            print(" ".join(link), flush=True)
+        subprocess.run(link, check=True)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 

@@ -126,7 +126,7 @@ constexpr LogCells make_log_cells()
     return t;
 }
 
-__device__ const LogCells kLogCellTable = make_log_cells();
+static __device__ const LogCells kLogCellTable = make_log_cells();
 
 // Copies the cells into the block's LDS copy; threads 0..127 each copy one.
 // The caller synchronises the block before the first lookup.

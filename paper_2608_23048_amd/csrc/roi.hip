@@ -18,14 +18,13 @@
 #include <string>
 #include <utility>
 
+#include "common.hpp"
 #include "noise.hpp"
 #include "relax.hpp"
 #include "roi.h"
 
 namespace roi {
 namespace {
-
-constexpr int kBlock = 256;
 
 // Groups each lane loads ahead before computing the first.
 #ifndef ROI_UNROLL_M4
@@ -34,95 +33,8 @@ constexpr int kBlock = 256;
 #ifndef ROI_UNROLL_M8
 #define ROI_UNROLL_M8 1
 #endif
-// Non-temporal hints on the HBM streams (each byte is touched once).
-#ifndef ROI_NONTEMPORAL
-#define ROI_NONTEMPORAL 1
-#endif
 template <int M>
 constexpr int kUnroll = M == 4 ? ROI_UNROLL_M4 : ROI_UNROLL_M8;
-
-struct FwdArgs {
-    const uint16_t* W;
-    const float* phi;
-    uint16_t* Wm;
-    float* S;
-    uint8_t* idx;
-    int64_t ngroups;
-    uint32_t block0; // low 32 bits of elem_offset / 4 (the high 32 are key.block_hi)
-    NoiseKey key;
-    float lambda;
-    float inv_tau;
-};
-
-struct BwdArgs {
-    const uint16_t* G;
-    const uint16_t* W;
-    const float* phi;
-    float* dphi;
-    int64_t ngroups;
-    uint32_t block0;
-    NoiseKey key;
-    float lambda;
-    float inv_lambda;
-    float tau;
-    float inv_tau;
-};
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-template <typename T>
-__device__ __forceinline__ T stream_load(const T* p)
-{
-#if ROI_NONTEMPORAL
-    return __builtin_nontemporal_load(p);
-#else
-    return *p;
-#endif
-}
-
-template <typename T>
-__device__ __forceinline__ void stream_store(const T& v, T* p)
-{
-#if ROI_NONTEMPORAL
-    __builtin_nontemporal_store(v, p);
-#else
-    *p = v;
-#endif
-}
-
-__device__ __forceinline__ float bf16_bits_to_float(uint32_t b) { return __uint_as_float(b << 16); }
-
-// Loads of one group: m fp32 logits (m/4 16-byte loads) and m bf16 values
-// (one 8-byte load for m = 4, one 16-byte load for m = 8).
-template <int M>
-__device__ __forceinline__ void load_logits(const float* p, float (&phi)[M])
-{
-    const f32x4* p4 = reinterpret_cast<const f32x4*>(p);
-#pragma unroll
-    for (int t = 0; t < M / 4; ++t) {
-        const f32x4 v = stream_load(p4 + t);
-        phi[4 * t + 0] = v.x;
-        phi[4 * t + 1] = v.y;
-        phi[4 * t + 2] = v.z;
-        phi[4 * t + 3] = v.w;
-    }
-}
-
-template <int M>
-__device__ __forceinline__ void load_bf16(const uint16_t* p, uint32_t (&w)[M])
-{
-    if constexpr (M == 4) {
-        const u32x2 v = stream_load(reinterpret_cast<const u32x2*>(p));
-        w[0] = v.x & 0xFFFFu; w[1] = v.x >> 16; w[2] = v.y & 0xFFFFu; w[3] = v.y >> 16;
-    } else {
-        static_assert(M == 8, "m");
-        const u32x4 v = stream_load(reinterpret_cast<const u32x4*>(p));
-        w[0] = v.x & 0xFFFFu; w[1] = v.x >> 16; w[2] = v.y & 0xFFFFu; w[3] = v.y >> 16;
-        w[4] = v.z & 0xFFFFu; w[5] = v.z >> 16; w[6] = v.w & 0xFFFFu; w[7] = v.w >> 16;
-    }
-}
 
 // Masked bf16 weights: the kept value, or +0.0 (bits 0x0000).
 template <int M>
@@ -389,8 +301,6 @@ int grid_for(int64_t items)
     return (int)(need < 1 ? 1 : (need < kMaxBlocks ? need : kMaxBlocks));
 }
 
-int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
-int kUnroll4or8(int m) { return m == 4 ? kUnroll<4> : kUnroll<8>; }
 
 struct Shape {
     int64_t numel = 0;
@@ -404,8 +314,8 @@ int check_shape(int64_t rows, int64_t cols, int n, int m, float tau, float lambd
                                           (long long)rows, (long long)cols);
     if (m < 1 || n < 1 || n > m)
         return fail(ROI_E_INVAL, "pattern n:m = %d:%d needs 1 <= n <= m", n, m);
-    if (m != 4 && m != 8)
-        return fail(ROI_E_UNSUPPORTED, "m = %d is not built (supported: 4, 8)", m);
+    if (m != 4 && m != 8 && m != 16 && m != 32)
+        return fail(ROI_E_UNSUPPORTED, "m = %d is not built (supported: 4, 8, 16, 32)", m);
     if (cols % m != 0) return fail(ROI_E_INVAL, "cols (%lld) must be a multiple of m (%d)",
                                    (long long)cols, m);
     if (rows > 0 && cols > ((int64_t)1 << 62) / rows)
@@ -463,9 +373,10 @@ int launch_status(const char* what)
     return ok();
 }
 
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int kUnroll4or8(int m) { return m == 4 ? kUnroll<4> : kUnroll<8>; }
+
 // ---- dispatch tables over (m, n) and the boolean variants
-using FwdFn = void (*)(FwdArgs);
-using BwdFn = void (*)(BwdArgs);
 
 template <int M, int N>
 FwdFn pick_fwd(bool want_s, bool want_idx, bool lam1)
@@ -505,14 +416,21 @@ FwdFn select_fwd(int m, int n, bool s, bool i, bool l)
 {
     if (m == 4) return fwd_for_n<4>(n, s, i, l, std::make_integer_sequence<int, 4>{});
     if (m == 8) return fwd_for_n<8>(n, s, i, l, std::make_integer_sequence<int, 8>{});
-    return nullptr;
+    return select_wide_fwd(m, n);
 }
 
 BwdFn select_bwd(int m, int n, bool l)
 {
     if (m == 4) return bwd_for_n<4>(n, l, std::make_integer_sequence<int, 4>{});
     if (m == 8) return bwd_for_n<8>(n, l, std::make_integer_sequence<int, 8>{});
-    return nullptr;
+    return select_wide_bwd(m, n);
+}
+
+// Threads per launch: one per U groups for m = 4 and 8, m / 4 per group for
+// m = 16 and 32.
+int64_t threads_for(int64_t ngroups, int m)
+{
+    return m <= 8 ? ceil_div(ngroups, kUnroll4or8(m)) : ngroups * (m / 4);
 }
 
 } // namespace
@@ -565,7 +483,7 @@ extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows
         a.lambda = lambda;
         a.inv_tau = inv_tau;
         void* args[] = {&a};
-        if (hipLaunchKernel((const void*)fn, dim3(grid_for(ceil_div(ng, kUnroll4or8(m)))),
+        if (hipLaunchKernel((const void*)fn, dim3(grid_for(threads_for(ng, m))),
                             dim3(kBlock), args, 0, stream) != hipSuccess)
             return launch_status("roi_mask_fwd");
         return launch_status("roi_mask_fwd");
@@ -608,7 +526,7 @@ extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, co
         a.tau = tau;
         a.inv_tau = inv_tau;
         void* args[] = {&a};
-        if (hipLaunchKernel((const void*)fn, dim3(grid_for(ceil_div(ng, kUnroll4or8(m)))),
+        if (hipLaunchKernel((const void*)fn, dim3(grid_for(threads_for(ng, m))),
                             dim3(kBlock), args, 0, stream) != hipSuccess)
             return launch_status("roi_mask_bwd");
         return launch_status("roi_mask_bwd");

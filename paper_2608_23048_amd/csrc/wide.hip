@@ -1,0 +1,312 @@
+// wide.hip -- gfx950 kernels for groups of m = 16 and 32 weights.
+//
+// Four consecutive elements per lane (one Philox call, one 16-byte logits load
+// and one 8-byte bf16 load per lane), a group spread over L = m / 4 adjacent
+// lanes of one wave.  Group-wide maxima and "sum over the other lanes" use
+// cross-lane butterflies: DPP quad permutations for lane distances 1..3 and
+// ds_swizzle for distance 4.  Every group is whole inside a wave and either
+// all its lanes are active or none is, so the butterflies never read a lane
+// outside the group.  Same arithmetic as the per-lane kernels for m = 4 and 8:
+// the noise of noise.hpp, ranks with ties to the lower index, and the
+// relaxation of relax.hpp in its "all entries but j" form.
+#include <hip/hip_runtime.h>
+
+#include <utility>
+
+#include "common.hpp"
+#include "noise.hpp"
+#include "relax.hpp"
+
+namespace roi {
+namespace {
+
+// Value held by lane (lane ^ D) of the same group (D < 8).
+template <int D>
+__device__ __forceinline__ float lane_xor(float v)
+{
+    static_assert(D > 0 && D < 8, "lane distance");
+    int x = __float_as_int(v);
+    if constexpr ((D & 4) != 0) x = __builtin_amdgcn_ds_swizzle(x, 0x101F); // xor 4 within 32 lanes
+    constexpr int lo = D & 3;
+    if constexpr (lo == 1) x = __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, true); // [1,0,3,2]
+    if constexpr (lo == 2) x = __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, true); // [2,3,0,1]
+    if constexpr (lo == 3) x = __builtin_amdgcn_update_dpp(0, x, 0x1B, 0xF, 0xF, true); // [3,2,1,0]
+    return __int_as_float(x);
+}
+
+template <int L>
+__device__ __forceinline__ float group_max(float v)
+{
+    v = fmaxf(v, lane_xor<1>(v));
+    if constexpr (L >= 4) v = fmaxf(v, lane_xor<2>(v));
+    if constexpr (L >= 8) v = fmaxf(v, lane_xor<4>(v));
+    return v;
+}
+
+// Sum of t over the other L - 1 lanes of the group (never includes this lane's
+// own t, so a dominant lane does not swamp the others).
+template <int L>
+__device__ __forceinline__ float sum_other_lanes(float t)
+{
+    const float o1 = lane_xor<1>(t);
+    if constexpr (L == 2) return o1;
+    const float s1 = t + o1; // pair sum
+    float other = o1 + lane_xor<2>(s1);
+    if constexpr (L == 8) {
+        const float s2 = s1 + lane_xor<2>(s1); // quad sum
+        other += lane_xor<4>(s2);
+    }
+    return other;
+}
+
+__device__ __forceinline__ float max4(const float (&x)[4])
+{
+    return fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+}
+
+// Adds, for lane distances D..L-1, how many entries of lane (lane ^ D) beat
+// each of this lane's entries (ties go to the lower index).
+template <int L, int D>
+__device__ __forceinline__ void rank_against_lane(const float (&k)[4], int part, int (&rank)[4])
+{
+    if constexpr (D < L) {
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = lane_xor<D>(k[e]);
+        const bool lower = (part ^ D) < part; // that lane's entries have lower indices
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+#pragma unroll
+            for (int f = 0; f < 4; ++f) {
+                const bool beats = lower ? (o[f] >= k[e]) : (o[f] > k[e]);
+                rank[e] += beats ? 1 : 0;
+            }
+        }
+        rank_against_lane<L, D + 1>(k, part, rank);
+    }
+}
+
+// Keys of the group beaten-by counts: rank[e] = number of entries of the group
+// that beat this lane's entry e (kappa_i > kappa_j, or equal and i < j).
+template <int L>
+__device__ __forceinline__ void wide_rank(const float (&k)[4], int part, int (&rank)[4])
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) rank[e] = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int j = i + 1; j < 4; ++j) {
+            const bool i_wins = k[i] >= k[j];
+            rank[j] += i_wins ? 1 : 0;
+            rank[i] += i_wins ? 0 : 1;
+        }
+    }
+    rank_against_lane<L, 1>(k, part, rank);
+}
+
+// Relaxation over the group (§3.2 recursion, Algorithm 1), four entries per
+// lane; see relax_forward in relax.hpp for the arithmetic.
+template <int L, int N, bool kKeep>
+__device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], float inv_tau,
+                                                   bool want_s, float (&S)[4],
+                                                   StepRec<4> (&rec)[N])
+{
+    const float kmax = group_max<L>(max4(kappa));
+    const float c = kLog2e * inv_tau;
+    float b[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        b[e] = (kappa[e] - kmax) * c;
+        S[e] = 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        float ex[4];
+        const float bmax = k == 0 ? 0.0f : group_max<L>(max4(b));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ex[e] = __builtin_amdgcn_exp2f(b[e] - bmax);
+        float others[4], t;
+        sums_but_one<4>(ex, others, t);
+        const float ext = sum_other_lanes<L>(t);
+        const float inv_total = __builtin_amdgcn_rcpf(t + ext);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float mu = ex[e] * inv_total;
+            const float om = (others[e] + ext) * inv_total;
+            if (want_s) S[e] += mu;
+            if (kKeep) {
+                rec[k].mu[e] = mu;
+                rec[k].om[e] = om;
+            }
+            if (k + 1 < N)
+                b[e] = __builtin_fmaf(__builtin_amdgcn_logf(fmaxf(om, kFltMin)), inv_tau, b[e]);
+        }
+    }
+}
+
+// Reverse sweep over the group; see relax_backward in relax.hpp.
+template <int L, int N>
+__device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
+                                                    const float (&sbar)[4], float tau,
+                                                    float inv_tau, float (&abar)[4])
+{
+    const float keep0 = (tau - 1.0f) * inv_tau;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) abar[e] = 0.0f;
+#pragma unroll
+    for (int k = N - 1; k >= 0; --k) {
+        const bool has_next = (k + 1 < N);
+        float t[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float mubar = sbar[e];
+            if (has_next) {
+                const float om = rec[k].om[e];
+                const float r = abar[e] * __builtin_amdgcn_rcpf(om);
+                mubar = (om >= kFltMin) ? mubar - r : mubar;
+            }
+            t[e] = rec[k].mu[e] * mubar;
+        }
+        float q[4], tl;
+        sums_but_one<4>(t, q, tl);
+        const float ext = sum_other_lanes<L>(tl);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float om = rec[k].om[e];
+            const float mu = rec[k].mu[e];
+            const float inner = __builtin_fmaf(om, sbar[e], -(q[e] + ext));
+            float carry = 0.0f;
+            if (has_next) {
+                float keep = mu < 0.5f ? __builtin_fmaf(-mu, inv_tau, 1.0f)
+                                       : __builtin_fmaf(om, inv_tau, keep0);
+                keep = (om >= kFltMin) ? keep : 1.0f;
+                carry = abar[e] * keep;
+            }
+            abar[e] = __builtin_fmaf(mu * inv_tau, inner, carry);
+        }
+    }
+}
+
+__device__ __forceinline__ void wide_keys(const float (&phi)[4], uint32_t block, const NoiseKey& key,
+                                          float lambda, const float2* tab, float (&kappa)[4])
+{
+    const uint4 x = philox_block(block, key);
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+    const bool lam_one = lambda == 1.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float ng = neg_gumbel_from_word(w[e], tab);
+        const float phi_bar = lam_one ? phi[e] : phi[e] / lambda;
+        kappa[e] = phi_bar - ng;
+    }
+}
+
+template <int M, int N>
+__global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdArgs a)
+{
+    constexpr int L = M / 4;
+    __shared__ float2 tab[kLogCells];
+    fill_log_table(tab);
+    __syncthreads();
+    const int64_t nslots = a.ngroups * L;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t slot = (int64_t)blockIdx.x * kBlock + threadIdx.x; slot < nslots; slot += stride) {
+        const int part = (int)(slot % L);
+        const int64_t group = slot / L;
+        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(a.phi + slot * 4));
+        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(a.W + slot * 4));
+        const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
+        float kappa[4];
+        wide_keys(phi, a.block0 + (uint32_t)slot, a.key, a.lambda, tab, kappa);
+        int rank[4];
+        wide_rank<L>(kappa, part, rank);
+        const uint32_t m01 = (rank[0] < N ? 0x0000FFFFu : 0u) | (rank[1] < N ? 0xFFFF0000u : 0u);
+        const uint32_t m23 = (rank[2] < N ? 0x0000FFFFu : 0u) | (rank[3] < N ? 0xFFFF0000u : 0u);
+        const u32x2 out = {wv.x & m01, wv.y & m23};
+        stream_store(out, reinterpret_cast<u32x2*>(a.Wm + slot * 4));
+        if (a.idx) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (rank[e] < N) a.idx[group * N + rank[e]] = (uint8_t)(part * 4 + e);
+        }
+        if (a.S) {
+            float S[4];
+            StepRec<4> unused[N]; // not written when records are not kept
+            wide_relax_forward<L, N, false>(kappa, a.inv_tau, true, S, unused);
+            const f32x4 sv = {S[0], S[1], S[2], S[3]};
+            stream_store(sv, reinterpret_cast<f32x4*>(a.S + slot * 4));
+        }
+    }
+}
+
+template <int M, int N>
+__global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdArgs a)
+{
+    constexpr int L = M / 4;
+    __shared__ float2 tab[kLogCells];
+    fill_log_table(tab);
+    __syncthreads();
+    const int64_t nslots = a.ngroups * L;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t slot = (int64_t)blockIdx.x * kBlock + threadIdx.x; slot < nslots; slot += stride) {
+        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(a.phi + slot * 4));
+        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(a.W + slot * 4));
+        const u32x2 gv = stream_load(reinterpret_cast<const u32x2*>(a.G + slot * 4));
+        const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
+        float kappa[4];
+        wide_keys(phi, a.block0 + (uint32_t)slot, a.key, a.lambda, tab, kappa);
+        // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32.
+        const float sbar[4] = {
+            bf16_bits_to_float(gv.x & 0xFFFFu) * bf16_bits_to_float(wv.x & 0xFFFFu),
+            bf16_bits_to_float(gv.x >> 16) * bf16_bits_to_float(wv.x >> 16),
+            bf16_bits_to_float(gv.y & 0xFFFFu) * bf16_bits_to_float(wv.y & 0xFFFFu),
+            bf16_bits_to_float(gv.y >> 16) * bf16_bits_to_float(wv.y >> 16)};
+        StepRec<4> rec[N];
+        float S_unused[4];
+        wide_relax_forward<L, N, true>(kappa, a.inv_tau, false, S_unused, rec);
+        float abar[4];
+        wide_relax_backward<L, N>(rec, sbar, a.tau, a.inv_tau, abar);
+        const bool lam_one = a.lambda == 1.0f;
+        f32x4 dv;
+        dv.x = lam_one ? abar[0] : abar[0] * a.inv_lambda;
+        dv.y = lam_one ? abar[1] : abar[1] * a.inv_lambda;
+        dv.z = lam_one ? abar[2] : abar[2] * a.inv_lambda;
+        dv.w = lam_one ? abar[3] : abar[3] * a.inv_lambda;
+        stream_store(dv, reinterpret_cast<f32x4*>(a.dphi + slot * 4));
+    }
+}
+
+template <int M, int... Ns>
+FwdFn wide_fwd_for_n(int n, std::integer_sequence<int, Ns...>)
+{
+    FwdFn f = nullptr;
+    ((n == Ns + 1 ? (f = fwd_wide_kernel<M, Ns + 1>, 0) : 0), ...);
+    return f;
+}
+
+template <int M, int... Ns>
+BwdFn wide_bwd_for_n(int n, std::integer_sequence<int, Ns...>)
+{
+    BwdFn f = nullptr;
+    ((n == Ns + 1 ? (f = bwd_wide_kernel<M, Ns + 1>, 0) : 0), ...);
+    return f;
+}
+
+} // namespace
+
+FwdFn select_wide_fwd(int m, int n)
+{
+    if (m == 16) return wide_fwd_for_n<16>(n, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_fwd_for_n<32>(n, std::make_integer_sequence<int, 32>{});
+    return nullptr;
+}
+
+BwdFn select_wide_bwd(int m, int n)
+{
+    if (m == 16) return wide_bwd_for_n<16>(n, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_bwd_for_n<32>(n, std::make_integer_sequence<int, 32>{});
+    return nullptr;
+}
+
+} // namespace roi

@@ -66,7 +66,8 @@ def bwd(L, **kw):
     (dict(n=0), roi.ROI_E_INVAL),
     (dict(n=5), roi.ROI_E_INVAL),
     (dict(m=3, n=1, cols=9), roi.ROI_E_UNSUPPORTED),
-    (dict(m=16, n=8, cols=16), roi.ROI_E_UNSUPPORTED),
+    (dict(m=12, n=6, cols=12), roi.ROI_E_UNSUPPORTED),
+    (dict(m=64, n=32, cols=64), roi.ROI_E_UNSUPPORTED),
     (dict(cols=6), roi.ROI_E_INVAL),
     (dict(rows=-1), roi.ROI_E_INVAL),
     (dict(rows=1 << 40, cols=1 << 40), roi.ROI_E_INVAL),
@@ -94,7 +95,8 @@ def test_fwd_rejects_before_launch(L, kw, status):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(n=0), roi.ROI_E_INVAL),
-    (dict(m=32, n=16, cols=32), roi.ROI_E_UNSUPPORTED),
+    (dict(m=64, n=16, cols=64), roi.ROI_E_UNSUPPORTED),
+    (dict(m=16, n=8, cols=24), roi.ROI_E_INVAL),
     (dict(cols=10), roi.ROI_E_INVAL),
     (dict(tau=0.0), roi.ROI_E_INVAL),
     (dict(lam=-2.0), roi.ROI_E_INVAL),

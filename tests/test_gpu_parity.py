@@ -106,6 +106,16 @@ SMALL = [
     # the Philox block index crosses a multiple of 2^32 inside the call
     (40, 64, 2, 4, 1.0, 1.0, 6, 3, 2**34 - 4 * 256),
     (25, 64, 4, 8, 0.5, 1.0, 6, 3, 2**35 - 8 * 100),
+    # m = 16 and 32: groups spread over 4 and 8 lanes
+    (37, 48, 8, 16, 1.0, 1.0, 2, 0, 0),
+    (21, 80, 1, 16, 0.5, 1.0, 3, 7, 32),
+    (21, 80, 15, 16, 0.7, 1.0, 3, 7, 16),
+    (9, 64, 16, 16, 1.0, 1.0, 3, 1, 0),
+    (33, 96, 16, 32, 1.0, 1.0, 4, 2, 0),
+    (13, 64, 5, 32, 0.3, 0.8, 5, 3, 64),
+    (13, 64, 31, 32, 1.0, 1.0, 5, 3, 32),
+    (7, 32, 32, 32, 0.9, 1.0, 6, 4, 0),
+    (20, 64, 8, 16, 0.5, 1.0, 7, 8, 2**34 - 16 * 40),
 ]
 
 
@@ -136,7 +146,7 @@ def test_ties_go_to_lowest_index(dev):
     """Logits equal to minus the noise make every key exactly +0.0: all keys
     tie and the kept entries are the lowest indices, in index order."""
     import torch
-    for n, m in ((2, 4), (3, 8), (1, 4), (5, 8)):
+    for n, m in ((2, 4), (3, 8), (1, 4), (5, 8), (8, 16), (3, 16), (16, 32), (7, 32)):
         say(f"ties {n}:{m}")
         rows, cols, seed, step = 16, 64, 21, 4
         _, g = roi.gumbel_noise(rows * cols, seed, step, 0, device=dev, want_words=False)
@@ -162,7 +172,7 @@ def test_split_calls_equal_one_slab_call(dev):
     """Per-tensor calls with cumulative elem_offset give exactly the outputs of
     one call over the back-to-back slab."""
     import torch
-    shapes = [(128, 96), (32, 96), (32, 96), (128, 96), (200, 96), (96, 200)]
+    shapes = [(128, 96), (32, 96), (32, 96), (128, 96), (200, 96), (96, 224)]
     offs = np.cumsum([0] + [r * c for r, c in shapes])
     total = int(offs[-1])
     gen = torch.Generator(device="cpu")
@@ -170,7 +180,7 @@ def test_split_calls_equal_one_slab_call(dev):
     W = (torch.randn(total, generator=gen) * 0.02).to(torch.bfloat16).to(dev)
     L = torch.randn(total, generator=gen).to(dev)
     G = (torch.randn(total, generator=gen) * 1e-3).to(torch.bfloat16).to(dev)
-    for n, m in ((2, 4), (4, 8)):
+    for n, m in ((2, 4), (4, 8), (8, 16), (16, 32)):
         say(f"split vs slab {n}:{m}")
         Wm, S, idx = roi.mask_fwd(W, L, n, m, 0.5, 1.0, 9, 2, 0, want_soft=True)
         d = roi.mask_bwd(G, W, L, n, m, 0.5, 1.0, 9, 2, 0)
@@ -190,7 +200,7 @@ def test_split_calls_equal_one_slab_call(dev):
 def test_every_output_written_and_deterministic(dev):
     import torch
     W, L, G = wl.small_case(333, 64, 1, device=dev)
-    for n, m in ((2, 4), (3, 8)):
+    for n, m in ((2, 4), (3, 8), (8, 16), (16, 32)):
         say(f"sentinel/determinism {n}:{m}")
         outs = []
         for _ in range(2):
@@ -298,3 +308,9 @@ def test_full_qwen7b_layer_4of8(dev):
 def test_full_qwen7b_stack_2of4(dev, step):
     tau = roi.anneal(1.0, 0.1, step, 9)
     full_workload_check(dev, "qwen2.5-7b-stack-2:4", 2, 4, tau, step, 30000)
+
+
+@pytest.mark.parametrize("name,n,m", [("qwen2.5-1.5b-stack-8:16", 8, 16),
+                                      ("qwen2.5-1.5b-stack-16:32", 16, 32)])
+def test_full_qwen15b_stack_wide(dev, name, n, m):
+    full_workload_check(dev, name, n, m, 1.0, 0, 20000)
