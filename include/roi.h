@@ -27,7 +27,7 @@
  *    launched; nothing is written then.  No exceptions cross the ABI.
  *  - Return value: ROI_OK or a negative roi_status; roi_last_error() gives a
  *    thread-local human-readable detail of the last failure.
- *  - Supported patterns: m in {4, 8} with 1 <= n <= m.
+ *  - Supported patterns: m in {4, 8, 16, 32} with 1 <= n <= m.
  *
  * Noise (the same definition the forward and the backward use):
  *  - global element index e = elem_offset + (flat index of the element);
@@ -60,7 +60,7 @@ extern "C" {
 typedef enum {
     ROI_OK = 0,
     ROI_E_INVAL = -1,       /* invalid argument (sizes, pattern, temperatures, pointers) */
-    ROI_E_UNSUPPORTED = -2, /* valid for the method but not built: m outside {4, 8} */
+    ROI_E_UNSUPPORTED = -2, /* valid for the method but not built: m outside {4, 8, 16, 32} */
     ROI_E_HIP = -3          /* the HIP runtime reported an error at launch */
 } roi_status;
 
@@ -78,7 +78,7 @@ typedef enum {
  *  W          bf16 [rows, cols]          frozen weights (read)
  *  logits     fp32 [rows, cols]          phi (read)
  *  rows, cols sizes, rows >= 0, cols >= 0, cols % m == 0, rows * cols < 2^62
- *  n, m       keep n of every m; m in {4, 8}, 1 <= n <= m
+ *  n, m       keep n of every m; m in {4, 8, 16, 32}, 1 <= n <= m
  *  tau        relaxation temperature, finite, > 0 (used only for soft_mask)
  *  lambda     sampling temperature, finite, > 0 (§4.2.3)
  *  seed, step Philox key and step counter
@@ -93,6 +93,21 @@ int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows, int64_t c
                  int m, float tau, float lambda, uint64_t seed, uint64_t step,
                  uint64_t elem_offset, uint16_t* W_masked, float* soft_mask, uint8_t* sel_idx,
                  hipStream_t stream);
+
+/*
+ * roi_mask_fwd_soft -- the pure soft forward (the paper's default setting:
+ * "w/o STE" in the appendix comparison with the straight-through variant;
+ * §4.2.2 relaxation used directly in the forward pass).  Same arguments and
+ * noise as roi_mask_fwd; the output is
+ *   W_soft = bf16_rne(W (.) S), S = sum_{k=1..n} mu^(k) (fp32, §3.2 recursion),
+ * and soft_mask / sel_idx, when not NULL, receive S and the hard top-n indices
+ * of the same keys.  The backward is roi_mask_bwd (the relaxation is the
+ * differentiated path in both settings).
+ */
+int roi_mask_fwd_soft(const uint16_t* W, const float* logits, int64_t rows, int64_t cols, int n,
+                      int m, float tau, float lambda, uint64_t seed, uint64_t step,
+                      uint64_t elem_offset, uint16_t* W_soft, float* soft_mask, uint8_t* sel_idx,
+                      hipStream_t stream);
 
 /*
  * roi_mask_bwd -- dL/dlogits from dL/dW_masked.

@@ -18,7 +18,7 @@ ROI_E_INVAL = -1
 ROI_E_UNSUPPORTED = -2
 ROI_E_HIP = -3
 
-SUPPORTED_M = (4, 8)
+SUPPORTED_M = (4, 8, 16, 32)
 
 
 class RoiError(RuntimeError):
@@ -46,6 +46,8 @@ def lib() -> ctypes.CDLL:
         L.roi_mask_fwd.argtypes = [_vp, _vp, _i64, _i64, _int, _int, _f32, _f32, _u64, _u64, _u64,
                                    _vp, _vp, _vp, _vp]
         L.roi_mask_fwd.restype = _int
+        L.roi_mask_fwd_soft.argtypes = L.roi_mask_fwd.argtypes
+        L.roi_mask_fwd_soft.restype = _int
         L.roi_mask_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _int, _int, _f32, _f32, _u64, _u64,
                                    _u64, _vp, _vp]
         L.roi_mask_bwd.restype = _int
@@ -103,11 +105,13 @@ def _check_tensor(t, dtype, name, like=None):
 # --------------------------------------------------------------------------- tensor API
 def mask_fwd(W, logits, n: int, m: int, tau: float = 1.0, lam: float = 1.0, seed: int = 0,
              step: int = 0, elem_offset: int = 0, want_soft: bool = False, want_idx: bool = True,
-             out: dict | None = None):
+             out: dict | None = None, soft_forward: bool = False):
     """Forward sample.  W: bf16 [rows, cols] (or 1-D), logits: fp32 same shape.
 
     Returns (W_masked bf16, soft_mask fp32 or None, sel_idx uint8 [groups, n] or
     None).  ``out`` may hold preallocated "W_masked", "soft_mask", "sel_idx".
+    soft_forward=False: straight-through forward, W_masked = W (.) hard mask;
+    soft_forward=True: pure soft forward, W_masked = bf16(W (.) S).
     """
     import torch
     _check_tensor(W, torch.bfloat16, "W")
@@ -123,8 +127,9 @@ def mask_fwd(W, logits, n: int, m: int, tau: float = 1.0, lam: float = 1.0, seed
     idx = out.get("sel_idx") if want_idx else None
     if want_idx and idx is None:
         idx = torch.empty((W.numel() // m if m > 0 else 0, n), dtype=torch.uint8, device=W.device)
-    st = lib().roi_mask_fwd(_ptr(W), _ptr(logits), rows, cols, n, m, tau, lam, seed, step,
-                            elem_offset, _ptr(Wm), _ptr(S), _ptr(idx), _stream(W))
+    fn = lib().roi_mask_fwd_soft if soft_forward else lib().roi_mask_fwd
+    st = fn(_ptr(W), _ptr(logits), rows, cols, n, m, tau, lam, seed, step, elem_offset, _ptr(Wm),
+            _ptr(S), _ptr(idx), _stream(W))
     _raise_on(st)
     return Wm, S, idx
 

@@ -27,6 +27,7 @@ struct FwdArgs {
     NoiseKey key;
     float lambda;
     float inv_tau;
+    int soft; // 1: W_masked = W (.) S (pure soft forward), 0: W (.) hard mask
 };
 
 struct BwdArgs {
@@ -68,6 +69,13 @@ __device__ __forceinline__ void stream_store(const T& v, T* p)
 }
 
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t b) { return __uint_as_float(b << 16); }
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t float_to_bf16_rne(float f)
+{
+    const uint32_t b = __float_as_uint(f);
+    return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
 
 // Loads of one group: m fp32 logits (m/4 16-byte loads) and m bf16 values
 // (one 8-byte load for m = 4, one 16-byte load for m = 8).

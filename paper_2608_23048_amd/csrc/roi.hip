@@ -36,6 +36,21 @@ namespace {
 template <int M>
 constexpr int kUnroll = M == 4 ? ROI_UNROLL_M4 : ROI_UNROLL_M8;
 
+// m bf16 values (16-bit patterns in the low half of each word), stored packed.
+template <int M>
+__device__ __forceinline__ void store_pairs(uint16_t* p, const uint32_t (&h)[M])
+{
+    if constexpr (M == 4) {
+        const u32x2 v = {h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+        stream_store(v, reinterpret_cast<u32x2*>(p));
+    } else {
+        static_assert(M == 8, "m");
+        const u32x4 v = {h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                         h[6] | (h[7] << 16)};
+        stream_store(v, reinterpret_cast<u32x4*>(p));
+    }
+}
+
 // Masked bf16 weights: the kept value, or +0.0 (bits 0x0000).
 template <int M>
 __device__ __forceinline__ void store_masked(uint16_t* p, const uint32_t (&w)[M], const int (&rank)[M],
@@ -114,7 +129,7 @@ __device__ __forceinline__ void group_keys(const float (&phi)[M], uint32_t block
 // and store instruction of a wave is one contiguous span, and all of a lane's
 // loads are issued before its first group is computed (more bytes in flight
 // per wave for the HBM stream).
-template <int M, int N, bool kWantS, bool kWantIdx, bool kLambdaOne>
+template <int M, int N, bool kRelax, bool kWantIdx, bool kLambdaOne>
 __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
 {
     __shared__ float2 tab[kLogCells];
@@ -146,27 +161,39 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
             float kappa[M];
             group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint32_t)q * (M / 4), a.key, a.lambda,
                                       tab, kappa);
+            const bool soft = kRelax && a.soft;
             if constexpr (M == 4) {
                 const Top4Entry t4 = top4[top4_code(kappa)];
-                const u32x2 v = {(w[u][0] | (w[u][1] << 16)) & t4.m01,
-                                 (w[u][2] | (w[u][3] << 16)) & t4.m23};
-                stream_store(v, reinterpret_cast<u32x2*>(a.Wm + q * M));
+                if (!soft) {
+                    const u32x2 v = {(w[u][0] | (w[u][1] << 16)) & t4.m01,
+                                     (w[u][2] | (w[u][3] << 16)) & t4.m23};
+                    stream_store(v, reinterpret_cast<u32x2*>(a.Wm + q * M));
+                }
                 if (kWantIdx) store_order<N>(a.idx + q * N, t4.order);
             } else {
                 int rank[M];
                 rank_keys<M>(kappa, rank);
-                store_masked<M>(a.Wm + q * M, w[u], rank, N);
+                if (!soft) store_masked<M>(a.Wm + q * M, w[u], rank, N);
                 if (kWantIdx) store_idx<M, N>(a.idx + q * N, rank);
             }
-            if (kWantS) {
+            if (kRelax) {
                 float S[M];
                 StepRec<M> unused[N]; // not written when records are not kept
                 relax_forward<M, N, true, false>(kappa, a.inv_tau, S, unused);
-                f32x4* s4 = reinterpret_cast<f32x4*>(a.S + q * M);
+                if (a.S) {
+                    f32x4* s4 = reinterpret_cast<f32x4*>(a.S + q * M);
 #pragma unroll
-                for (int t = 0; t < M / 4; ++t) {
-                    const f32x4 v = {S[4 * t], S[4 * t + 1], S[4 * t + 2], S[4 * t + 3]};
-                    stream_store(v, s4 + t);
+                    for (int t = 0; t < M / 4; ++t) {
+                        const f32x4 v = {S[4 * t], S[4 * t + 1], S[4 * t + 2], S[4 * t + 3]};
+                        stream_store(v, s4 + t);
+                    }
+                }
+                if (soft) { // pure soft forward: W (.) S, rounded to bf16
+                    uint32_t ws[M];
+#pragma unroll
+                    for (int j = 0; j < M; ++j)
+                        ws[j] = float_to_bf16_rne(bf16_bits_to_float(w[u][j]) * S[j]);
+                    store_pairs<M>(a.Wm + q * M, ws);
                 }
             }
         }
@@ -438,10 +465,12 @@ int64_t threads_for(int64_t ngroups, int m)
 
 using namespace roi;
 
-extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows, int64_t cols,
-                            int n, int m, float tau, float lambda, uint64_t seed, uint64_t step,
-                            uint64_t elem_offset, uint16_t* W_masked, float* soft_mask,
-                            uint8_t* sel_idx, hipStream_t stream)
+namespace roi {
+namespace {
+int mask_fwd_impl(const char* what, bool soft, const uint16_t* W, const float* logits,
+                  int64_t rows, int64_t cols, int n, int m, float tau, float lambda, uint64_t seed,
+                  uint64_t step, uint64_t elem_offset, uint16_t* W_masked, float* soft_mask,
+                  uint8_t* sel_idx, hipStream_t stream)
 {
     Shape sh;
     if (int st = check_shape(rows, cols, n, m, tau, lambda, elem_offset, &sh)) return st;
@@ -465,7 +494,7 @@ extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows
             if (overlap(outs[i], out_n[i], outs[j], out_n[j]))
                 return fail(ROI_E_INVAL, "outputs must not overlap each other");
     }
-    FwdFn fn = select_fwd(m, n, soft_mask != nullptr, sel_idx != nullptr, lambda == 1.0f);
+    FwdFn fn = select_fwd(m, n, soft || soft_mask != nullptr, sel_idx != nullptr, lambda == 1.0f);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     const NoiseKey key = make_key(seed, step, 0);
     const float inv_tau = (float)(1.0 / (double)tau);
@@ -482,12 +511,34 @@ extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows
         a.key.block_hi = (uint32_t)((e0 / 4) >> 32);
         a.lambda = lambda;
         a.inv_tau = inv_tau;
+        a.soft = soft ? 1 : 0;
         void* args[] = {&a};
         if (hipLaunchKernel((const void*)fn, dim3(grid_for(threads_for(ng, m))),
                             dim3(kBlock), args, 0, stream) != hipSuccess)
-            return launch_status("roi_mask_fwd");
-        return launch_status("roi_mask_fwd");
+            return launch_status(what);
+        return launch_status(what);
     });
+}
+} // namespace
+} // namespace roi
+
+extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows, int64_t cols,
+                            int n, int m, float tau, float lambda, uint64_t seed, uint64_t step,
+                            uint64_t elem_offset, uint16_t* W_masked, float* soft_mask,
+                            uint8_t* sel_idx, hipStream_t stream)
+{
+    return mask_fwd_impl("roi_mask_fwd", false, W, logits, rows, cols, n, m, tau, lambda, seed,
+                         step, elem_offset, W_masked, soft_mask, sel_idx, stream);
+}
+
+extern "C" int roi_mask_fwd_soft(const uint16_t* W, const float* logits, int64_t rows,
+                                 int64_t cols, int n, int m, float tau, float lambda,
+                                 uint64_t seed, uint64_t step, uint64_t elem_offset,
+                                 uint16_t* W_soft, float* soft_mask, uint8_t* sel_idx,
+                                 hipStream_t stream)
+{
+    return mask_fwd_impl("roi_mask_fwd_soft", true, W, logits, rows, cols, n, m, tau, lambda,
+                         seed, step, elem_offset, W_soft, soft_mask, sel_idx, stream);
 }
 
 extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,

@@ -221,21 +221,33 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdArgs a)
         wide_keys(phi, a.block0 + (uint32_t)slot, a.key, a.lambda, tab, kappa);
         int rank[4];
         wide_rank<L>(kappa, part, rank);
-        const uint32_t m01 = (rank[0] < N ? 0x0000FFFFu : 0u) | (rank[1] < N ? 0xFFFF0000u : 0u);
-        const uint32_t m23 = (rank[2] < N ? 0x0000FFFFu : 0u) | (rank[3] < N ? 0xFFFF0000u : 0u);
-        const u32x2 out = {wv.x & m01, wv.y & m23};
-        stream_store(out, reinterpret_cast<u32x2*>(a.Wm + slot * 4));
+        if (!a.soft) {
+            const uint32_t m01 = (rank[0] < N ? 0x0000FFFFu : 0u) | (rank[1] < N ? 0xFFFF0000u : 0u);
+            const uint32_t m23 = (rank[2] < N ? 0x0000FFFFu : 0u) | (rank[3] < N ? 0xFFFF0000u : 0u);
+            const u32x2 out = {wv.x & m01, wv.y & m23};
+            stream_store(out, reinterpret_cast<u32x2*>(a.Wm + slot * 4));
+        }
         if (a.idx) {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
                 if (rank[e] < N) a.idx[group * N + rank[e]] = (uint8_t)(part * 4 + e);
         }
-        if (a.S) {
+        if (a.S || a.soft) {
             float S[4];
             StepRec<4> unused[N]; // not written when records are not kept
             wide_relax_forward<L, N, false>(kappa, a.inv_tau, true, S, unused);
-            const f32x4 sv = {S[0], S[1], S[2], S[3]};
-            stream_store(sv, reinterpret_cast<f32x4*>(a.S + slot * 4));
+            if (a.S) {
+                const f32x4 sv = {S[0], S[1], S[2], S[3]};
+                stream_store(sv, reinterpret_cast<f32x4*>(a.S + slot * 4));
+            }
+            if (a.soft) { // pure soft forward: W (.) S, rounded to bf16
+                const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
+                const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
+                const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
+                const uint32_t h3 = float_to_bf16_rne(bf16_bits_to_float(wv.y >> 16) * S[3]);
+                const u32x2 out = {h0 | (h1 << 16), h2 | (h3 << 16)};
+                stream_store(out, reinterpret_cast<u32x2*>(a.Wm + slot * 4));
+            }
         }
     }
 }

@@ -30,7 +30,8 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert {"roi_mask_fwd", "roi_mask_bwd", "roi_gumbel_noise", "roi_gumbel_from_words",
+    assert {"roi_mask_fwd", "roi_mask_fwd_soft", "roi_mask_bwd", "roi_gumbel_noise",
+            "roi_gumbel_from_words",
             "roi_anneal", "roi_status_string", "roi_last_error", "roi_abi_version"} <= set(names)
     for name in names:
         assert hasattr(L, name), name
@@ -91,6 +92,12 @@ def bwd(L, **kw):
 def test_fwd_rejects_before_launch(L, kw, status):
     assert fwd(L, **kw) == status
     assert L.roi_last_error()
+    a = dict(W=FAKE, logits=FAKE + (1 << 30), rows=4, cols=8, n=2, m=4, tau=1.0, lam=1.0, seed=0,
+             step=0, off=0, Wm=FAKE + (2 << 30), S=None, idx=None)
+    a.update(kw)
+    assert L.roi_mask_fwd_soft(a["W"], a["logits"], a["rows"], a["cols"], a["n"], a["m"],
+                               a["tau"], a["lam"], a["seed"], a["step"], a["off"], a["Wm"],
+                               a["S"], a["idx"], None) == status
 
 
 @pytest.mark.parametrize("kw,status", [

@@ -314,3 +314,35 @@ def test_full_qwen7b_stack_2of4(dev, step):
                                       ("qwen2.5-1.5b-stack-16:32", 16, 32)])
 def test_full_qwen15b_stack_wide(dev, name, n, m):
     full_workload_check(dev, name, n, m, 1.0, 0, 20000)
+
+
+# --------------------------------------------------------------------------- pure soft forward
+SOFT = [(37, 36, 2, 4, 1.0, 1.0, 3, 1, 0), (64, 96, 2, 4, 0.1, 1.0, 5, 9, 8),
+        (33, 64, 3, 4, 1.3, 0.6, 2, 3, 12), (61, 88, 4, 8, 0.5, 1.0, 8, 5, 8),
+        (37, 48, 8, 16, 1.0, 1.0, 2, 0, 0), (33, 96, 16, 32, 1.0, 1.0, 4, 2, 0),
+        (13, 64, 5, 32, 0.3, 0.8, 5, 3, 64)]
+
+
+@pytest.mark.parametrize("case", SOFT, ids=lambda c: "x".join(map(str, c[:4])))
+def test_soft_forward(dev, case):
+    """Pure soft forward (the paper's default, without the straight-through
+    estimator): W_soft = bf16(W (.) S).  Against W (.) S from the oracle's fp64
+    S: within one bf16 rounding step plus the float tolerance; S and the
+    indices as in the straight-through forward."""
+    import torch
+    rows, cols, n, m, tau, lam, seed, step, off = case
+    say(f"soft forward rows={rows} cols={cols} {n}:{m} tau={tau} lam={lam}")
+    W, L, _ = wl.small_case(rows, cols, rows * 7 + cols, device=dev, w_std=1.0)
+    Ws, S, idx = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True,
+                              soft_forward=True)
+    Wh, S2, idx2 = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2) and torch.equal(S.view(torch.int32), S2.view(torch.int32))
+    tau32, lam32 = float(np.float32(tau)), float(np.float32(lam))
+    _, S_o, idx_o = oracle.mask_fwd(bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
+    assert np.array_equal(idx.cpu().numpy(), idx_o)
+    ref = (bf16_bits(W).astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1) \
+        * S_o
+    got = (bf16_bits(Ws).astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1)
+    ulp = np.where(ref != 0, 2.0 ** (np.floor(np.log2(np.abs(ref) + 1e-300)) - 7), 0.0)
+    assert_close(got, ref, "W (.) S", floor=ulp)
