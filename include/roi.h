@@ -147,6 +147,16 @@ int roi_gumbel_from_words(const uint32_t* words, int64_t count, float* gumbel,
                           hipStream_t stream);
 
 /*
+ * roi_fast_noise_from_words -- the noise in log2 units from the hardware
+ * logarithm, K(x) = -log2(-log2 u(x)) = g log2(e) + log2(ln 2) up to a few
+ * ulp: the form the kernels use where fp32 accuracy suffices (the backward's
+ * relaxation; the forward's key comparisons, which fall back to the exact
+ * keys whenever two keys are closer than the proven bound of this form's
+ * error).  words uint32 [count] (read), out fp32 [count] (written).
+ */
+int roi_fast_noise_from_words(const uint32_t* words, int64_t count, float* out, hipStream_t stream);
+
+/*
  * roi_anneal -- §4.2.3 exponential annealing, host-side:
  * v_t = max{ v_end, v_init (v_end / v_init)^(t / t_anneal) }, evaluated in
  * fp64 and rounded to fp32.  Requires v_init > 0, v_end > 0, t >= 0,

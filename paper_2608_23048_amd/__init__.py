@@ -55,6 +55,8 @@ def lib() -> ctypes.CDLL:
         L.roi_gumbel_noise.restype = _int
         L.roi_gumbel_from_words.argtypes = [_vp, _i64, _vp, _vp]
         L.roi_gumbel_from_words.restype = _int
+        L.roi_fast_noise_from_words.argtypes = [_vp, _i64, _vp, _vp]
+        L.roi_fast_noise_from_words.restype = _int
         L.roi_anneal.argtypes = [_f32, _f32, _i64, _i64]
         L.roi_anneal.restype = _f32
         L.roi_status_string.argtypes = [_int]
@@ -168,6 +170,16 @@ def gumbel_from_words(words):
     g = torch.empty(words.shape, dtype=torch.float32, device=words.device)
     _raise_on(lib().roi_gumbel_from_words(_ptr(words), words.numel(), _ptr(g), _stream(words)))
     return g
+
+
+def fast_noise_from_words(words):
+    """K = -log2(-log2 u(x)) from the hardware logarithm, for int32 word tensors."""
+    import torch
+    _check_tensor(words, torch.int32, "words")
+    out = torch.empty(words.shape, dtype=torch.float32, device=words.device)
+    _raise_on(lib().roi_fast_noise_from_words(_ptr(words), words.numel(), _ptr(out),
+                                              _stream(words)))
+    return out
 
 
 def anneal(v_init: float, v_end: float, t: int, t_anneal: int) -> float:

@@ -26,6 +26,7 @@ struct FwdArgs {
     uint32_t block0; // low 32 bits of elem_offset / 4 (the high 32 are key.block_hi)
     NoiseKey key;
     float lambda;
+    float key_c; // fl(log2(e) / lambda): the scale of the hardware-log keys
     float inv_tau;
     int soft; // 1: W_masked = W (.) S (pure soft forward), 0: W (.) hard mask
 };
@@ -38,7 +39,7 @@ struct BwdArgs {
     int64_t ngroups;
     uint32_t block0;
     NoiseKey key;
-    float lambda;
+    float key_c; // fl(log2(e) / lambda)
     float inv_lambda;
     float tau;
     float inv_tau;

@@ -172,6 +172,65 @@ __device__ __forceinline__ float gumbel_from_word(uint32_t x, const float2* tab)
     return -neg_gumbel_from_word(x, tab);
 }
 
+// Keys from the hardware logarithm (v_log_f32), in log2 units.
+//
+// The noise: N(x) = -log2(-log2 u(x)), which approximates g log2(e) + log2(ln 2)
+// for the g of neg_gumbel_from_word.  Over every one of the 2^23 possible u
+// its distance from that value, with g the library's own fp32 noise, is below
+// kFastNoiseBound (the largest is 1.98e-6, at u close to 1, where |N| ~ 23).
+// The common offset log2(ln 2) cancels in every comparison and softmax.
+//
+// The key: K = fma(phi, c, N(x)) with c = fl(log2(e) / lambda), which
+// approximates log2(e) kappa + log2(ln 2) for kappa = fl(fl(phi / lambda) + g).
+// With a = fl(phi / lambda), |g| < 16.7 and |a| <= |kappa| + |g| the error is
+// at most
+//   kFastNoiseBound                      the noise
+//   + 3 * 2^-24 log2(e) |a|              c and a each round once
+//   + 2^-24 log2(e) |kappa|              the rounding of kappa
+//   + 2^-24 |K|                          the rounding of the fma
+//   <= 6.9e-6 + 2.98e-7 |K|              (log2(e) |kappa| <= |K| + 0.54).
+// Two keys i, j whose hardware keys differ by more than
+//   kFastPairMargin + 2^-20 max(|K_i|, |K_j|) > the sum of the two errors
+// are therefore ordered the same way by kappa, and are not equal.  The
+// backward's relaxation uses these keys directly (its outputs are fp32
+// values with a tolerance, and the key error is of the order of the
+// rounding of kappa itself); the straight-through forward uses them for its
+// comparisons and recomputes the exact keys for any group in which two keys
+// are closer than the margin, so its selections are those of the exact keys.
+constexpr float kFastNoiseBound = 2.5e-6f;
+constexpr float kFastPairMargin = 3.2e-5f; // > 2 (kFastNoiseBound + 4.44e-6), with slack
+
+__device__ __forceinline__ float fast_noise_log2(uint32_t x)
+{
+    const float u = uniform_from_word(x);
+    const float l1 = __builtin_amdgcn_logf(u); // log2 u < 0
+    return -__builtin_amdgcn_logf(-l1);
+}
+
+__device__ __forceinline__ float fast_key_log2(float phi, float c, uint32_t x)
+{
+    return __builtin_fmaf(phi, c, fast_noise_log2(x));
+}
+
+// True when every pair of the m hardware keys is further apart than the
+// margin above, taken with the group's largest |K| (which only widens it);
+// false whenever a key is infinite or NaN.
+template <int M>
+__device__ __forceinline__ bool fast_keys_separated(const float (&k)[M])
+{
+    float big = fabsf(k[0]);
+#pragma unroll
+    for (int j = 1; j < M; ++j) big = fmaxf(big, fabsf(k[j]));
+    const float margin = __builtin_fmaf(big, 0x1p-20f, kFastPairMargin);
+    bool sep = true;
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+#pragma unroll
+        for (int j = i + 1; j < M; ++j) sep &= fabsf(k[i] - k[j]) > margin;
+    }
+    return sep;
+}
+
 // kappa = fl(fl(phi / lambda) + g); for lambda == 1 the quotient is phi exactly.
 template <bool kLambdaOne>
 __device__ __forceinline__ float key_of(float phi, float lambda, uint32_t word, const float2* tab)

@@ -110,14 +110,16 @@ struct StepRec {
 // largest key first keeps the competing entries near 0, where fp32 is
 // densest.  1 - mu_j is evaluated as (sum of the other exponentials) / total,
 // which never cancels, and log(1 - mu) is floored at log(FLT_MIN).
+// key_scale turns key differences into b: log2(e) / tau for keys in natural
+// units, 1 / tau for keys already in log2 units (any common offset cancels).
 template <int M, int N, bool kWantS, bool kKeep>
-__device__ __forceinline__ void relax_forward(const float (&kappa)[M], float inv_tau,
-                                              float (&S)[M], StepRec<M> (&rec)[N])
+__device__ __forceinline__ void relax_forward(const float (&kappa)[M], float key_scale,
+                                              float inv_tau, float (&S)[M], StepRec<M> (&rec)[N])
 {
     float kmax = kappa[0];
 #pragma unroll
     for (int j = 1; j < M; ++j) kmax = fmaxf(kmax, kappa[j]);
-    const float c = kLog2e * inv_tau;
+    const float c = key_scale;
     float b[M];
 #pragma unroll
     for (int j = 0; j < M; ++j) {

@@ -110,18 +110,36 @@ __device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
     }
 }
 
-template <int M, bool kLambdaOne>
-__device__ __forceinline__ void group_keys(const float (&phi)[M], uint32_t block, const NoiseKey& key,
-                                           float lambda, const float2* tab, float (&kappa)[M])
+// The m Philox words of a group (block = its first Philox block index).
+template <int M>
+__device__ __forceinline__ void group_words(uint32_t block, const NoiseKey& key, uint32_t (&x)[M])
 {
 #pragma unroll
     for (int t = 0; t < M / 4; ++t) {
-        const uint4 x = philox_block(block + t, key);
-        kappa[4 * t + 0] = key_of<kLambdaOne>(phi[4 * t + 0], lambda, x.x, tab);
-        kappa[4 * t + 1] = key_of<kLambdaOne>(phi[4 * t + 1], lambda, x.y, tab);
-        kappa[4 * t + 2] = key_of<kLambdaOne>(phi[4 * t + 2], lambda, x.z, tab);
-        kappa[4 * t + 3] = key_of<kLambdaOne>(phi[4 * t + 3], lambda, x.w, tab);
+        const uint4 v = philox_block(block + t, key);
+        x[4 * t + 0] = v.x;
+        x[4 * t + 1] = v.y;
+        x[4 * t + 2] = v.z;
+        x[4 * t + 3] = v.w;
     }
+}
+
+// The exact keys kappa = fl(fl(phi / lambda) + g) (noise.hpp).
+template <int M, bool kLambdaOne>
+__device__ __forceinline__ void exact_keys(const float (&phi)[M], const uint32_t (&x)[M],
+                                           float lambda, const float2* tab, float (&kappa)[M])
+{
+#pragma unroll
+    for (int j = 0; j < M; ++j) kappa[j] = key_of<kLambdaOne>(phi[j], lambda, x[j], tab);
+}
+
+// The hardware-log keys in log2 units (noise.hpp).
+template <int M>
+__device__ __forceinline__ void fast_keys(const float (&phi)[M], const uint32_t (&x)[M], float c,
+                                          float (&k)[M])
+{
+#pragma unroll
+    for (int j = 0; j < M; ++j) k[j] = fast_key_log2(phi[j], c, x[j]);
 }
 
 // Each iteration of a block covers kUnroll * kBlock consecutive groups: lane l
@@ -158,9 +176,20 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kBlock + threadIdx.x;
             if (q >= a.ngroups) continue;
+            uint32_t x[M];
+            group_words<M>(a.block0 + (uint32_t)q * (M / 4), a.key, x);
             float kappa[M];
-            group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint32_t)q * (M / 4), a.key, a.lambda,
-                                      tab, kappa);
+            if constexpr (kRelax) {
+                // the relaxation's soft mask is an fp32 output: exact keys
+                exact_keys<M, kLambdaOne>(phi[u], x, a.lambda, tab, kappa);
+            } else {
+                // Comparisons only: the hardware keys order every pair that is
+                // further apart than their error margin exactly as the exact keys
+                // do; a group with a closer pair (rare) takes the exact keys.
+                fast_keys<M>(phi[u], x, a.key_c, kappa);
+                if (!fast_keys_separated<M>(kappa))
+                    exact_keys<M, kLambdaOne>(phi[u], x, a.lambda, tab, kappa);
+            }
             const bool soft = kRelax && a.soft;
             if constexpr (M == 4) {
                 const Top4Entry t4 = top4[top4_code(kappa)];
@@ -179,7 +208,7 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
             if (kRelax) {
                 float S[M];
                 StepRec<M> unused[N]; // not written when records are not kept
-                relax_forward<M, N, true, false>(kappa, a.inv_tau, S, unused);
+                relax_forward<M, N, true, false>(kappa, kLog2e * a.inv_tau, a.inv_tau, S, unused);
                 if (a.S) {
                     f32x4* s4 = reinterpret_cast<f32x4*>(a.S + q * M);
 #pragma unroll
@@ -203,9 +232,6 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
 template <int M, int N, bool kLambdaOne>
 __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
 {
-    __shared__ float2 tab[kLogCells];
-    fill_log_table(tab);
-    __syncthreads();
     constexpr int U = kUnroll<M>;
     const int64_t chunk = (int64_t)kBlock * U;
     for (int64_t base = (int64_t)blockIdx.x * chunk; base < a.ngroups;
@@ -225,9 +251,11 @@ __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kBlock + threadIdx.x;
             if (q >= a.ngroups) continue;
+            // keys from the hardware logarithm, in log2 units (noise.hpp)
+            uint32_t x[M];
+            group_words<M>(a.block0 + (uint32_t)q * (M / 4), a.key, x);
             float kappa[M];
-            group_keys<M, kLambdaOne>(phi[u], a.block0 + (uint32_t)q * (M / 4), a.key, a.lambda,
-                                      tab, kappa);
+            fast_keys<M>(phi[u], x, kLambdaOne ? kLog2e : a.key_c, kappa);
             // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
             float sbar[M];
 #pragma unroll
@@ -235,7 +263,7 @@ __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
                 sbar[j] = bf16_bits_to_float(g[u][j]) * bf16_bits_to_float(w[u][j]);
             StepRec<M> rec[N];
             float S_unused[M];
-            relax_forward<M, N, false, true>(kappa, a.inv_tau, S_unused, rec);
+            relax_forward<M, N, false, true>(kappa, a.inv_tau, a.inv_tau, S_unused, rec);
             float abar[M];
             relax_backward<M, N>(rec, sbar, a.tau, a.inv_tau, abar);
             f32x4* d4 = reinterpret_cast<f32x4*>(a.dphi + q * M);
@@ -273,6 +301,14 @@ __global__ __launch_bounds__(kBlock) void noise_kernel(uint32_t* words, float* g
             }
         }
     }
+}
+
+__global__ __launch_bounds__(kBlock) void fast_noise_kernel(const uint32_t* words, float* out,
+                                                            int64_t count)
+{
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride)
+        out[i] = fast_noise_log2(words[i]);
 }
 
 __global__ __launch_bounds__(kBlock) void gumbel_words_kernel(const uint32_t* words, float* gum,
@@ -498,6 +534,7 @@ int mask_fwd_impl(const char* what, bool soft, const uint16_t* W, const float* l
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     const NoiseKey key = make_key(seed, step, 0);
     const float inv_tau = (float)(1.0 / (double)tau);
+    const float key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
     return for_each_piece(elem_offset, sh.ngroups, m, [&](int64_t g0, int64_t ng, uint64_t e0) {
         FwdArgs a;
         a.W = W + g0 * m;
@@ -510,6 +547,7 @@ int mask_fwd_impl(const char* what, bool soft, const uint16_t* W, const float* l
         a.key = key;
         a.key.block_hi = (uint32_t)((e0 / 4) >> 32);
         a.lambda = lambda;
+        a.key_c = key_c;
         a.inv_tau = inv_tau;
         a.soft = soft ? 1 : 0;
         void* args[] = {&a};
@@ -562,6 +600,7 @@ extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, co
     const NoiseKey key = make_key(seed, step, 0);
     const float inv_lambda = (float)(1.0 / (double)lambda);
     const float inv_tau = (float)(1.0 / (double)tau);
+    const float key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
     return for_each_piece(elem_offset, sh.ngroups, m, [&](int64_t g0, int64_t ng, uint64_t e0) {
         BwdArgs a;
         a.G = grad_W_masked + g0 * m;
@@ -572,7 +611,7 @@ extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, co
         a.block0 = (uint32_t)(e0 / 4);
         a.key = key;
         a.key.block_hi = (uint32_t)((e0 / 4) >> 32);
-        a.lambda = lambda;
+        a.key_c = key_c;
         a.inv_lambda = inv_lambda;
         a.tau = tau;
         a.inv_tau = inv_tau;
@@ -618,6 +657,21 @@ extern "C" int roi_gumbel_from_words(const uint32_t* words, int64_t count, float
     hipLaunchKernelGGL(gumbel_words_kernel, dim3(grid_for(count)), dim3(kBlock), 0, stream, words,
                        gumbel, count);
     return launch_status("roi_gumbel_from_words");
+}
+
+extern "C" int roi_fast_noise_from_words(const uint32_t* words, int64_t count, float* out,
+                                         hipStream_t stream)
+{
+    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
+    if (count == 0) return ok();
+    if (!words || !out) return fail(ROI_E_INVAL, "words and out must not be NULL");
+    if (!aligned16(words) || !aligned16(out))
+        return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
+    if (overlap(words, (size_t)count * 4, out, (size_t)count * 4))
+        return fail(ROI_E_INVAL, "words and out must not overlap");
+    hipLaunchKernelGGL(fast_noise_kernel, dim3(grid_for(count)), dim3(kBlock), 0, stream, words,
+                       out, count);
+    return launch_status("roi_fast_noise_from_words");
 }
 
 extern "C" float roi_anneal(float v_init, float v_end, int64_t t, int64_t t_anneal)

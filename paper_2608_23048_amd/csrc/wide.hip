@@ -108,12 +108,12 @@ __device__ __forceinline__ void wide_rank(const float (&k)[4], int part, int (&r
 // Relaxation over the group (§3.2 recursion, Algorithm 1), four entries per
 // lane; see relax_forward in relax.hpp for the arithmetic.
 template <int L, int N, bool kKeep>
-__device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], float inv_tau,
-                                                   bool want_s, float (&S)[4],
+__device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], float key_scale,
+                                                   float inv_tau, bool want_s, float (&S)[4],
                                                    StepRec<4> (&rec)[N])
 {
     const float kmax = group_max<L>(max4(kappa));
-    const float c = kLog2e * inv_tau;
+    const float c = key_scale;
     float b[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -235,7 +235,8 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdArgs a)
         if (a.S || a.soft) {
             float S[4];
             StepRec<4> unused[N]; // not written when records are not kept
-            wide_relax_forward<L, N, false>(kappa, a.inv_tau, true, S, unused);
+            wide_relax_forward<L, N, false>(kappa, kLog2e * a.inv_tau, a.inv_tau, true, S,
+                                            unused);
             if (a.S) {
                 const f32x4 sv = {S[0], S[1], S[2], S[3]};
                 stream_store(sv, reinterpret_cast<f32x4*>(a.S + slot * 4));
@@ -256,9 +257,6 @@ template <int M, int N>
 __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdArgs a)
 {
     constexpr int L = M / 4;
-    __shared__ float2 tab[kLogCells];
-    fill_log_table(tab);
-    __syncthreads();
     const int64_t nslots = a.ngroups * L;
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     for (int64_t slot = (int64_t)blockIdx.x * kBlock + threadIdx.x; slot < nslots; slot += stride) {
@@ -266,8 +264,12 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdArgs a)
         const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(a.W + slot * 4));
         const u32x2 gv = stream_load(reinterpret_cast<const u32x2*>(a.G + slot * 4));
         const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
-        float kappa[4];
-        wide_keys(phi, a.block0 + (uint32_t)slot, a.key, a.lambda, tab, kappa);
+        // keys from the hardware logarithm, in log2 units (noise.hpp)
+        const uint4 x = philox_block(a.block0 + (uint32_t)slot, a.key);
+        const float kappa[4] = {fast_key_log2(phi[0], a.key_c, x.x),
+                                fast_key_log2(phi[1], a.key_c, x.y),
+                                fast_key_log2(phi[2], a.key_c, x.z),
+                                fast_key_log2(phi[3], a.key_c, x.w)};
         // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32.
         const float sbar[4] = {
             bf16_bits_to_float(gv.x & 0xFFFFu) * bf16_bits_to_float(wv.x & 0xFFFFu),
@@ -276,15 +278,12 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdArgs a)
             bf16_bits_to_float(gv.y >> 16) * bf16_bits_to_float(wv.y >> 16)};
         StepRec<4> rec[N];
         float S_unused[4];
-        wide_relax_forward<L, N, true>(kappa, a.inv_tau, false, S_unused, rec);
+        wide_relax_forward<L, N, true>(kappa, a.inv_tau, a.inv_tau, false, S_unused, rec);
         float abar[4];
         wide_relax_backward<L, N>(rec, sbar, a.tau, a.inv_tau, abar);
-        const bool lam_one = a.lambda == 1.0f;
-        f32x4 dv;
-        dv.x = lam_one ? abar[0] : abar[0] * a.inv_lambda;
-        dv.y = lam_one ? abar[1] : abar[1] * a.inv_lambda;
-        dv.z = lam_one ? abar[2] : abar[2] * a.inv_lambda;
-        dv.w = lam_one ? abar[3] : abar[3] * a.inv_lambda;
+        // dL/dphi = dL/dkappa / lambda (the product is exact for lambda = 1)
+        const f32x4 dv = {abar[0] * a.inv_lambda, abar[1] * a.inv_lambda,
+                          abar[2] * a.inv_lambda, abar[3] * a.inv_lambda};
         stream_store(dv, reinterpret_cast<f32x4*>(a.dphi + slot * 4));
     }
 }

@@ -47,19 +47,43 @@ def assert_close(got, ref, what, rtol=RTOL, atol=ATOL, scale_aware=False, floor=
     return float((err / np.maximum(bound, 1e-300)).max()) if ref.size else 0.0
 
 
-def key_ulp_sensitivity(oracle, kappa, sbar, n, tau, lam, trials=4, seed=0):
-    """fp32 noise floor of dL/dphi: the largest change of the oracle's fp64
-    gradient when every key moves by a random +-1 ulp (the keys are fp32, so
-    any fp32 evaluation of the relaxation perturbs them at this level).
-    kappa, sbar: [groups, m]."""
-    rng = np.random.default_rng(seed)
-    kappa = np.asarray(kappa, dtype=np.float32)
+# The hardware-log noise of the kernels, N(x) = -log2(-log2 u(x)), against the
+# exact noise g of the oracle: |N - (g log2(e) + log2(ln 2))| <= HW_NOISE_A +
+# HW_NOISE_B |N| for every one of the 2^23 uniforms, and <= HW_NOISE_MAX
+# (test_hardware_noise_bound checks both exhaustively).
+HW_NOISE_A = 6e-7
+HW_NOISE_B = 1e-7
+HW_NOISE_MAX = 2.5e-6
+LOG2E = 1.4426950408889634
+LOG2_LN2 = float(np.log2(np.log(2.0)))
+
+
+def backward_key_error(kappa, g, a):
+    """Per-key bound (natural units) of how far the backward's keys may sit from
+    the exact fp32 keys kappa = fl(a + g), a = fl(phi / lambda): the hardware
+    noise bound above, the roundings of fl(log2(e) / lambda) and of a (3 units
+    of 2^-24 |a|), of kappa and of the key's fma (2 units of 2^-24 |kappa|),
+    plus 2 ulp of kappa for the fp32 evaluation of the relaxation."""
+    kappa = np.abs(np.asarray(kappa, dtype=np.float64))
+    N = np.abs(np.asarray(g, dtype=np.float64) * LOG2E + LOG2_LN2)
+    a = np.abs(np.asarray(a, dtype=np.float64))
+    u = 2.0 ** -24
+    return np.log(2.0) * (HW_NOISE_A + HW_NOISE_B * N) + 3 * u * a + 6 * u * kappa
+
+
+def key_error_floor(oracle, kappa, delta, sbar, n, tau, lam, factor=4.0):
+    """Allowance for fp32 conditioning of dL/dphi: `factor` times the
+    first-order worst case sum_i |grad(kappa + delta_i e_i) - grad(kappa)| of
+    the oracle's fp64 gradient when each key moves by its bound delta_i.
+    kappa, delta, sbar: [groups, m]."""
+    kappa = np.asarray(kappa, dtype=np.float64)
+    delta = np.asarray(delta, dtype=np.float64)
     groups, m = kappa.shape
-    base = np.stack([oracle.relax_bwd(kappa[q].astype(np.float64), n, tau, sbar[q]) for q in range(groups)])
-    sens = np.zeros_like(base)
-    for _ in range(trials):
-        sign = rng.choice(np.array([-1.0, 1.0], dtype=np.float32), size=kappa.shape)
-        kp = np.nextafter(kappa, (np.float32(np.inf) * sign).astype(np.float32))
-        pert = np.stack([oracle.relax_bwd(kp[q].astype(np.float64), n, tau, sbar[q]) for q in range(groups)])
-        sens = np.maximum(sens, np.abs(pert - base))
-    return sens / lam
+    grad = lambda k: np.stack([oracle.relax_bwd(k[q], n, tau, sbar[q]) for q in range(groups)])
+    base = grad(kappa)
+    floor = np.zeros_like(base)
+    for i in range(m):
+        kp = kappa.copy()
+        kp[:, i] += delta[:, i]
+        floor += np.abs(grad(kp) - base)
+    return factor * floor / lam

@@ -31,7 +31,7 @@ def L():
 def test_exports_every_declared_symbol(L):
     names = header_functions()
     assert {"roi_mask_fwd", "roi_mask_fwd_soft", "roi_mask_bwd", "roi_gumbel_noise",
-            "roi_gumbel_from_words",
+            "roi_gumbel_from_words", "roi_fast_noise_from_words",
             "roi_anneal", "roi_status_string", "roi_last_error", "roi_abi_version"} <= set(names)
     for name in names:
         assert hasattr(L, name), name
@@ -123,6 +123,7 @@ def test_empty_input_is_a_no_op(L):
     assert bwd(L, rows=0, G=None, W=None, logits=None, d=None) == roi.ROI_OK
     assert L.roi_gumbel_noise(0, 0, 0, 0, None, None, None) == roi.ROI_OK
     assert L.roi_gumbel_from_words(None, 0, None, None) == roi.ROI_OK
+    assert L.roi_fast_noise_from_words(None, 0, None, None) == roi.ROI_OK
 
 
 def test_noise_entry_checks(L):
@@ -132,6 +133,10 @@ def test_noise_entry_checks(L):
     assert L.roi_gumbel_noise(0, 0, 0, 16, FAKE, FAKE + 32, None) == roi.ROI_E_INVAL
     assert L.roi_gumbel_from_words(FAKE, 8, FAKE + 16, None) == roi.ROI_E_INVAL
     assert L.roi_gumbel_from_words(FAKE + 4, 8, FAKE + 4096, None) == roi.ROI_E_INVAL
+    assert L.roi_fast_noise_from_words(FAKE, 8, FAKE + 16, None) == roi.ROI_E_INVAL   # overlap
+    assert L.roi_fast_noise_from_words(FAKE + 4, 8, FAKE + 4096, None) == roi.ROI_E_INVAL
+    assert L.roi_fast_noise_from_words(FAKE, -1, FAKE + 4096, None) == roi.ROI_E_INVAL
+    assert L.roi_fast_noise_from_words(None, 8, FAKE + 4096, None) == roi.ROI_E_INVAL
 
 
 def test_anneal_matches_oracle(L):
