@@ -26,15 +26,31 @@
 namespace roi {
 namespace {
 
-// Groups each lane loads ahead before computing the first.
-#ifndef ROI_UNROLL_M4
-#define ROI_UNROLL_M4 2
+// Groups each lane loads ahead before computing the first, per kernel and m,
+// and the block size of the per-lane kernels (measured on the 7B-class 2:4
+// stack; one group per lane is the fastest HBM stream for the backward's
+// three inputs).
+#ifndef ROI_UNROLL_FWD_M4
+#define ROI_UNROLL_FWD_M4 2
 #endif
-#ifndef ROI_UNROLL_M8
-#define ROI_UNROLL_M8 1
+#ifndef ROI_UNROLL_FWD_M8
+#define ROI_UNROLL_FWD_M8 1
+#endif
+#ifndef ROI_UNROLL_BWD_M4
+#define ROI_UNROLL_BWD_M4 1
+#endif
+#ifndef ROI_UNROLL_BWD_M8
+#define ROI_UNROLL_BWD_M8 1
+#endif
+#ifndef ROI_LANE_BLOCK
+#define ROI_LANE_BLOCK 256
 #endif
 template <int M>
-constexpr int kUnroll = M == 4 ? ROI_UNROLL_M4 : ROI_UNROLL_M8;
+constexpr int kUnrollFwd = M == 4 ? ROI_UNROLL_FWD_M4 : ROI_UNROLL_FWD_M8;
+template <int M>
+constexpr int kUnrollBwd = M == 4 ? ROI_UNROLL_BWD_M4 : ROI_UNROLL_BWD_M8;
+constexpr int kLaneBlock = ROI_LANE_BLOCK;
+static_assert(kLaneBlock >= kLogCells + 64 && kLaneBlock % 64 == 0, "lane block size");
 
 // m bf16 values (16-bit patterns in the low half of each word), stored packed.
 template <int M>
@@ -77,11 +93,11 @@ template <int N>
 __device__ __forceinline__ void store_order(uint8_t* p, uint32_t packed)
 {
     if constexpr (N == 1) {
-        *p = (uint8_t)packed;
+        stream_store((uint8_t)packed, p);
     } else if constexpr (N == 2) {
-        *reinterpret_cast<uint16_t*>(p) = (uint16_t)packed;
+        stream_store((uint16_t)packed, reinterpret_cast<uint16_t*>(p));
     } else if constexpr (N == 4) {
-        *reinterpret_cast<uint32_t*>(p) = packed;
+        stream_store(packed, reinterpret_cast<uint32_t*>(p));
     } else {
 #pragma unroll
         for (int r = 0; r < N; ++r) p[r] = (uint8_t)(packed >> (8 * r));
@@ -97,13 +113,13 @@ __device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
     for (int j = 0; j < M; ++j)
         packed |= (rank[j] < N) ? ((uint64_t)j << (8 * rank[j])) : 0ull;
     if constexpr (N == 1) {
-        *p = (uint8_t)packed;
+        stream_store((uint8_t)packed, p);
     } else if constexpr (N == 2) {
-        *reinterpret_cast<uint16_t*>(p) = (uint16_t)packed;
+        stream_store((uint16_t)packed, reinterpret_cast<uint16_t*>(p));
     } else if constexpr (N == 4) {
-        *reinterpret_cast<uint32_t*>(p) = (uint32_t)packed;
+        stream_store((uint32_t)packed, reinterpret_cast<uint32_t*>(p));
     } else if constexpr (N == 8) {
-        *reinterpret_cast<uint64_t*>(p) = packed;
+        stream_store(packed, reinterpret_cast<uint64_t*>(p));
     } else {
 #pragma unroll
         for (int r = 0; r < N; ++r) p[r] = (uint8_t)(packed >> (8 * r));
@@ -148,7 +164,7 @@ __device__ __forceinline__ void fast_keys(const float (&phi)[M], const uint32_t 
 // loads are issued before its first group is computed (more bytes in flight
 // per wave for the HBM stream).
 template <int M, int N, bool kRelax, bool kWantIdx, bool kLambdaOne>
-__global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
+__global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdArgs a)
 {
     __shared__ float2 tab[kLogCells];
     __shared__ Top4Entry top4[64];
@@ -158,15 +174,15 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
             top4[threadIdx.x - kLogCells] = kTop4Table<N>.e[threadIdx.x - kLogCells];
     }
     __syncthreads();
-    constexpr int U = kUnroll<M>;
-    const int64_t chunk = (int64_t)kBlock * U;
+    constexpr int U = kUnrollFwd<M>;
+    const int64_t chunk = (int64_t)kLaneBlock * U;
     for (int64_t base = (int64_t)blockIdx.x * chunk; base < a.ngroups;
          base += (int64_t)gridDim.x * chunk) {
         float phi[U][M];
         uint32_t w[U][M];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t q = base + u * kBlock + threadIdx.x;
+            const int64_t q = base + u * kLaneBlock + threadIdx.x;
             if (q < a.ngroups) {
                 load_logits<M>(a.phi + q * M, phi[u]);
                 load_bf16<M>(a.W + q * M, w[u]);
@@ -174,7 +190,7 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t q = base + u * kBlock + threadIdx.x;
+            const int64_t q = base + u * kLaneBlock + threadIdx.x;
             if (q >= a.ngroups) continue;
             uint32_t x[M];
             group_words<M>(a.block0 + (uint32_t)q * (M / 4), a.key, x);
@@ -230,17 +246,17 @@ __global__ __launch_bounds__(kBlock) void fwd_lane_kernel(FwdArgs a)
 }
 
 template <int M, int N, bool kLambdaOne>
-__global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
+__global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdArgs a)
 {
-    constexpr int U = kUnroll<M>;
-    const int64_t chunk = (int64_t)kBlock * U;
+    constexpr int U = kUnrollBwd<M>;
+    const int64_t chunk = (int64_t)kLaneBlock * U;
     for (int64_t base = (int64_t)blockIdx.x * chunk; base < a.ngroups;
          base += (int64_t)gridDim.x * chunk) {
         float phi[U][M];
         uint32_t w[U][M], g[U][M];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t q = base + u * kBlock + threadIdx.x;
+            const int64_t q = base + u * kLaneBlock + threadIdx.x;
             if (q < a.ngroups) {
                 load_logits<M>(a.phi + q * M, phi[u]);
                 load_bf16<M>(a.W + q * M, w[u]);
@@ -249,7 +265,7 @@ __global__ __launch_bounds__(kBlock) void bwd_lane_kernel(BwdArgs a)
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t q = base + u * kBlock + threadIdx.x;
+            const int64_t q = base + u * kLaneBlock + threadIdx.x;
             if (q >= a.ngroups) continue;
             // keys from the hardware logarithm, in log2 units (noise.hpp)
             uint32_t x[M];
@@ -352,16 +368,17 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb)
     return a0 < b0 + nb && b0 < a0 + na;
 }
 
-// Grid for `items` work items of one thread each.  One block per kBlock items
+// Grid for `items` work items of one thread each: one block per `block` items
 // (a one-shot grid dispatched in address order keeps the set of DRAM pages in
 // use compact; measured on MI355X, a plain copy streams at ~6.3 TB/s this way
-// against ~5 TB/s with a fixed grid looping with a large stride).  Kernels
-// keep a stride loop only for grids beyond kMaxBlocks.
-constexpr int64_t kMaxBlocks = (int64_t)1 << 22;
-int grid_for(int64_t items)
+// against ~5 TB/s with a fixed grid looping with a large stride).  A dispatch
+// holds its total work-item count in 32 bits, so grids stop below 2^32
+// threads; kernels keep a stride loop for the items beyond.
+int grid_for(int64_t items, int block = kBlock)
 {
-    const int64_t need = (items + kBlock - 1) / kBlock;
-    return (int)(need < 1 ? 1 : (need < kMaxBlocks ? need : kMaxBlocks));
+    const int64_t max_blocks = (int64_t)(0xFFFFFFFFu / (uint32_t)block);
+    const int64_t need = (items + block - 1) / block;
+    return (int)(need < 1 ? 1 : (need < max_blocks ? need : max_blocks));
 }
 
 
@@ -437,7 +454,6 @@ int launch_status(const char* what)
 }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
-int kUnroll4or8(int m) { return m == 4 ? kUnroll<4> : kUnroll<8>; }
 
 // ---- dispatch tables over (m, n) and the boolean variants
 
@@ -489,11 +505,18 @@ BwdFn select_bwd(int m, int n, bool l)
     return select_wide_bwd(m, n);
 }
 
-// Threads per launch: one per U groups for m = 4 and 8, m / 4 per group for
-// m = 16 and 32.
-int64_t threads_for(int64_t ngroups, int m)
+// Launch shape: one thread per U groups (and kLaneBlock threads per block)
+// for m = 4 and 8, m / 4 threads per group (kBlock per block) for m = 16, 32.
+struct LaunchShape {
+    int grid, block;
+};
+
+LaunchShape launch_shape(int64_t ngroups, int m, bool fwd)
 {
-    return m <= 8 ? ceil_div(ngroups, kUnroll4or8(m)) : ngroups * (m / 4);
+    if (m > 8) return {grid_for(ngroups * (m / 4)), kBlock};
+    const int u = fwd ? (m == 4 ? kUnrollFwd<4> : kUnrollFwd<8>)
+                      : (m == 4 ? kUnrollBwd<4> : kUnrollBwd<8>);
+    return {grid_for(ceil_div(ngroups, u), kLaneBlock), kLaneBlock};
 }
 
 } // namespace
@@ -551,8 +574,9 @@ int mask_fwd_impl(const char* what, bool soft, const uint16_t* W, const float* l
         a.inv_tau = inv_tau;
         a.soft = soft ? 1 : 0;
         void* args[] = {&a};
-        if (hipLaunchKernel((const void*)fn, dim3(grid_for(threads_for(ng, m))),
-                            dim3(kBlock), args, 0, stream) != hipSuccess)
+        const LaunchShape ls = launch_shape(ng, m, true);
+        if (hipLaunchKernel((const void*)fn, dim3(ls.grid), dim3(ls.block), args, 0, stream) !=
+            hipSuccess)
             return launch_status(what);
         return launch_status(what);
     });
@@ -616,8 +640,9 @@ extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, co
         a.tau = tau;
         a.inv_tau = inv_tau;
         void* args[] = {&a};
-        if (hipLaunchKernel((const void*)fn, dim3(grid_for(threads_for(ng, m))),
-                            dim3(kBlock), args, 0, stream) != hipSuccess)
+        const LaunchShape ls = launch_shape(ng, m, false);
+        if (hipLaunchKernel((const void*)fn, dim3(ls.grid), dim3(ls.block), args, 0, stream) !=
+            hipSuccess)
             return launch_status("roi_mask_bwd");
         return launch_status("roi_mask_bwd");
     });
