@@ -236,6 +236,50 @@ def main() -> int:
           f"({fwd_gbps:.0f} GB/s), bwd {bwd_avg:.3f} ms ({bwd_gbps:.0f} GB/s)", file=sys.stderr,
           flush=True)
 
+    # The same step through the grouped entry points, one descriptor per tensor
+    # (the layout of a model whose linear layers are separate tensors): a
+    # secondary figure, timed after the headline steps.
+    views = []
+    for t in work.tensors:
+        sl = slice(t.offset, t.offset + t.numel)
+        views.append((W[sl].view(t.rows, t.cols), L[sl].view(t.rows, t.cols),
+                      G[sl].view(t.rows, t.cols), Wm[sl].view(t.rows, t.cols),
+                      idx[t.offset // m:(t.offset + t.numel) // m],
+                      dphi[sl].view(t.rows, t.cols)))
+    fwd_in = [(v[0], v[1]) for v in views]
+    fwd_out = [(v[3], None, v[4]) for v in views]
+    bwd_in = [(v[2], v[0], v[1]) for v in views]
+    bwd_out = [v[5] for v in views]
+    offs = [t.offset for t in work.tensors]
+
+    def grouped_step(t: int, ev=None):
+        tau = tau_at(t)
+        if ev is not None:
+            ev[0].record()
+        roi.mask_fwd_grouped(fwd_in, n, m, tau, 1.0, 0, t, offsets=offs, outs=fwd_out)
+        if ev is not None:
+            ev[1].record()
+        roi.mask_bwd_grouped(bwd_in, n, m, tau, 1.0, 0, t, offsets=offs, outs=bwd_out)
+        if ev is not None:
+            ev[2].record()
+
+    grouped_step(1000)
+    gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    g0 = time.perf_counter()
+    for t in range(args.steps):
+        grouped_step(t, gev[t])
+    torch.cuda.synchronize()
+    g_elapsed = time.perf_counter() - g0
+    g_fwd = sum(e[0].elapsed_time(e[1]) for e in gev) / len(gev)
+    g_bwd = sum(e[1].elapsed_time(e[2]) for e in gev) / len(gev)
+    per_launch = 16  # pieces per grid (common.hpp kMaxPieces)
+    grouped = {"ms_per_step": g_elapsed * 1e3 / args.steps, "fwd_ms": g_fwd, "bwd_ms": g_bwd,
+               "descriptors": len(work.tensors),
+               "launches_per_step": 2 * -(-len(work.tensors) // per_launch)}
+    print(f"# grouped calls over {len(work.tensors)} tensors: {grouped['ms_per_step']:.3f} "
+          f"ms/step, fwd {g_fwd:.3f} ms, bwd {g_bwd:.3f} ms", file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
@@ -282,6 +326,7 @@ def main() -> int:
             "traffic": traffic,
         },
         "cpu_baseline": cpu,
+        "grouped_calls": grouped,
     }
     print(json.dumps(out), flush=True)
     return 0

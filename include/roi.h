@@ -129,6 +129,49 @@ int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* 
                  uint64_t step, uint64_t elem_offset, float* grad_logits, hipStream_t stream);
 
 /*
+ * Grouped calls: one call over many separately allocated tensors (e.g. every
+ * linear layer of a model), with the shared pattern, temperatures, seed and
+ * step.  Tensor i is processed exactly as the single-tensor call with its own
+ * pointers, rows, cols and elem_offset would process it (same outputs, bit
+ * for bit); the library launches the work of up to 16 tensor pieces per grid
+ * instead of one grid per tensor.  The descriptor array is host memory, read
+ * during the call only; the pointers in it follow the conventions above.
+ * Tensors with rows * cols == 0 are skipped (their pointers may be NULL).
+ * soft_mask and sel_idx must each be non-NULL for every nonempty tensor or
+ * for none.  No output may overlap any input or output of any tensor (inputs
+ * may overlap each other).  Any argument error returns before anything is
+ * launched; roi_last_error() names the offending tensor.
+ */
+typedef struct {
+    const uint16_t* W;     /* bf16 [rows, cols] (read) */
+    const float* logits;   /* fp32 [rows, cols] (read) */
+    uint16_t* W_masked;    /* bf16 [rows, cols] (written) */
+    float* soft_mask;      /* fp32 [rows, cols] or NULL */
+    uint8_t* sel_idx;      /* uint8 [rows*cols/m, n] or NULL */
+    int64_t rows, cols;
+    uint64_t elem_offset;  /* global index of element 0, % m == 0 */
+} roi_fwd_tensor;
+
+typedef struct {
+    const uint16_t* grad_W_masked; /* bf16 [rows, cols] (read) */
+    const uint16_t* W;             /* bf16 [rows, cols] (read) */
+    const float* logits;           /* fp32 [rows, cols] (read) */
+    float* grad_logits;            /* fp32 [rows, cols] (overwritten) */
+    int64_t rows, cols;
+    uint64_t elem_offset;
+} roi_bwd_tensor;
+
+/* roi_mask_fwd over `count` tensors (count >= 0). */
+int roi_mask_fwd_grouped(const roi_fwd_tensor* tensors, int count, int n, int m, float tau,
+                         float lambda, uint64_t seed, uint64_t step, hipStream_t stream);
+/* roi_mask_fwd_soft over `count` tensors (W_masked receives W_soft). */
+int roi_mask_fwd_soft_grouped(const roi_fwd_tensor* tensors, int count, int n, int m, float tau,
+                              float lambda, uint64_t seed, uint64_t step, hipStream_t stream);
+/* roi_mask_bwd over `count` tensors. */
+int roi_mask_bwd_grouped(const roi_bwd_tensor* tensors, int count, int n, int m, float tau,
+                         float lambda, uint64_t seed, uint64_t step, hipStream_t stream);
+
+/*
  * roi_gumbel_noise -- the noise of `count` consecutive elements starting at
  * global index elem_offset (elem_offset % 4 == 0): the raw Philox words
  * and/or g = -L(-L(u)) (Algorithm 1).  Either output may be NULL, not both.

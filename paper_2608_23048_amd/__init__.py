@@ -29,6 +29,22 @@ class RoiError(RuntimeError):
 
 _lib = None
 
+
+class FwdTensor(ctypes.Structure):
+    """roi_fwd_tensor (include/roi.h)."""
+    _fields_ = [("W", ctypes.c_void_p), ("logits", ctypes.c_void_p),
+                ("W_masked", ctypes.c_void_p), ("soft_mask", ctypes.c_void_p),
+                ("sel_idx", ctypes.c_void_p), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("elem_offset", ctypes.c_uint64)]
+
+
+class BwdTensor(ctypes.Structure):
+    """roi_bwd_tensor (include/roi.h)."""
+    _fields_ = [("grad_W_masked", ctypes.c_void_p), ("W", ctypes.c_void_p),
+                ("logits", ctypes.c_void_p), ("grad_logits", ctypes.c_void_p),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("elem_offset", ctypes.c_uint64)]
+
 _vp = ctypes.c_void_p
 _i64 = ctypes.c_int64
 _u64 = ctypes.c_uint64
@@ -51,6 +67,10 @@ def lib() -> ctypes.CDLL:
         L.roi_mask_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _int, _int, _f32, _f32, _u64, _u64,
                                    _u64, _vp, _vp]
         L.roi_mask_bwd.restype = _int
+        grouped = [_vp, _int, _int, _int, _f32, _f32, _u64, _u64, _vp]
+        for name in ("roi_mask_fwd_grouped", "roi_mask_fwd_soft_grouped", "roi_mask_bwd_grouped"):
+            getattr(L, name).argtypes = grouped
+            getattr(L, name).restype = _int
         L.roi_gumbel_noise.argtypes = [_u64, _u64, _u64, _i64, _vp, _vp, _vp]
         L.roi_gumbel_noise.restype = _int
         L.roi_gumbel_from_words.argtypes = [_vp, _i64, _vp, _vp]
@@ -149,6 +169,74 @@ def mask_bwd(grad_W_masked, W, logits, n: int, m: int, tau: float = 1.0, lam: fl
                             seed, step, elem_offset, _ptr(d), _stream(W))
     _raise_on(st)
     return d
+
+
+def _offsets(sizes, offsets):
+    if offsets is not None:
+        if len(offsets) != len(sizes):
+            raise ValueError("one elem_offset per tensor")
+        return [int(o) for o in offsets]
+    out, acc = [], 0
+    for k in sizes:
+        out.append(acc)
+        acc += k
+    return out
+
+
+def mask_fwd_grouped(tensors, n: int, m: int, tau: float = 1.0, lam: float = 1.0, seed: int = 0,
+                     step: int = 0, offsets=None, want_soft: bool = False, want_idx: bool = True,
+                     soft_forward: bool = False, outs=None):
+    """mask_fwd over a list of (W, logits) pairs in one call.  The element
+    offsets default to the running sum of the sizes (a stack in list order).
+    Returns a list of (W_masked, soft_mask or None, sel_idx or None); `outs`
+    may hold such a list, preallocated."""
+    import torch
+    given, outs, descs = outs, [], []
+    offs = _offsets([W.numel() for W, _ in tensors], offsets)
+    for i, ((W, logits), off) in enumerate(zip(tensors, offs)):
+        _check_tensor(W, torch.bfloat16, "W")
+        _check_tensor(logits, torch.float32, "logits", like=W)
+        rows, cols = _shape2d(W)
+        if given is not None:
+            Wm, S, idx = given[i]
+            S = S if want_soft else None
+            idx = idx if want_idx else None
+        else:
+            Wm = torch.empty_like(W)
+            S = torch.empty_like(logits) if want_soft else None
+            idx = (torch.empty((W.numel() // m if m > 0 else 0, n), dtype=torch.uint8,
+                               device=W.device) if want_idx else None)
+        outs.append((Wm, S, idx))
+        descs.append(FwdTensor(_ptr(W), _ptr(logits), _ptr(Wm), _ptr(S), _ptr(idx), rows, cols,
+                               off))
+    arr = (FwdTensor * max(1, len(descs)))(*descs)
+    fn = lib().roi_mask_fwd_soft_grouped if soft_forward else lib().roi_mask_fwd_grouped
+    stream = _stream(tensors[0][0]) if tensors else 0
+    _raise_on(fn(ctypes.addressof(arr), len(descs), n, m, tau, lam, seed, step, stream))
+    return outs
+
+
+def mask_bwd_grouped(tensors, n: int, m: int, tau: float = 1.0, lam: float = 1.0, seed: int = 0,
+                     step: int = 0, offsets=None, outs=None):
+    """mask_bwd over a list of (grad_W_masked, W, logits) triples in one call;
+    returns the list of grad_logits (`outs`: preallocated, optional)."""
+    import torch
+    given, outs, descs = outs, [], []
+    offs = _offsets([W.numel() for _, W, _ in tensors], offsets)
+    for i, ((G, W, logits), off) in enumerate(zip(tensors, offs)):
+        _check_tensor(G, torch.bfloat16, "grad_W_masked")
+        _check_tensor(W, torch.bfloat16, "W", like=G)
+        _check_tensor(logits, torch.float32, "logits", like=G)
+        rows, cols = _shape2d(W)
+        d = given[i] if given is not None else torch.empty_like(logits)
+        _check_tensor(d, torch.float32, "grad_logits", like=logits)
+        outs.append(d)
+        descs.append(BwdTensor(_ptr(G), _ptr(W), _ptr(logits), _ptr(d), rows, cols, off))
+    arr = (BwdTensor * max(1, len(descs)))(*descs)
+    stream = _stream(tensors[0][1]) if tensors else 0
+    _raise_on(lib().roi_mask_bwd_grouped(ctypes.addressof(arr), len(descs), n, m, tau, lam, seed,
+                                         step, stream))
+    return outs
 
 
 def gumbel_noise(count: int, seed: int = 0, step: int = 0, elem_offset: int = 0, device="cuda",

@@ -16,34 +16,64 @@ constexpr int kBlock = 256;
 #define ROI_NONTEMPORAL 1
 #endif
 
-struct FwdArgs {
+// A launch processes a batch of up to kMaxPieces pieces: consecutive groups of
+// one tensor whose Philox block indices share their high 32 bits.  Piece i
+// owns the launch's blocks [first_block, first_block + nblocks); its blocks
+// stride over the piece when it has more groups than blocks cover.
+constexpr int kMaxPieces = 16;
+
+struct FwdPiece {
     const uint16_t* W;
     const float* phi;
     uint16_t* Wm;
     float* S;
     uint8_t* idx;
     int64_t ngroups;
-    uint32_t block0; // low 32 bits of elem_offset / 4 (the high 32 are key.block_hi)
-    NoiseKey key;
+    uint32_t block0;   // low 32 bits of the Philox block index (element / 4) of group 0
+    uint32_t block_hi; // its high 32 bits, the same for every group of the piece
+    uint32_t first_block, nblocks;
+};
+
+struct FwdBatch {
+    FwdPiece p[kMaxPieces];
+    int count;
+    NoiseKey key_base; // key_base.block_hi is replaced by the piece's
     float lambda;
     float key_c; // fl(log2(e) / lambda): the scale of the hardware-log keys
     float inv_tau;
     int soft; // 1: W_masked = W (.) S (pure soft forward), 0: W (.) hard mask
 };
 
-struct BwdArgs {
+struct BwdPiece {
     const uint16_t* G;
     const uint16_t* W;
     const float* phi;
     float* dphi;
     int64_t ngroups;
-    uint32_t block0;
-    NoiseKey key;
+    uint32_t block0, block_hi;
+    uint32_t first_block, nblocks;
+};
+
+struct BwdBatch {
+    BwdPiece p[kMaxPieces];
+    int count;
+    NoiseKey key_base; // key_base.block_hi is replaced by the piece's
     float key_c; // fl(log2(e) / lambda)
     float inv_lambda;
     float tau;
     float inv_tau;
 };
+
+// The piece that owns this block (the table is in the kernel arguments; the
+// scan is uniform over the block).
+template <typename Batch>
+__device__ __forceinline__ int find_piece(const Batch& a)
+{
+    const uint32_t b = blockIdx.x;
+    int i = 0;
+    while (i + 1 < a.count && b >= a.p[i + 1].first_block) ++i;
+    return i;
+}
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -108,8 +138,8 @@ __device__ __forceinline__ void load_bf16(const uint16_t* p, uint32_t (&w)[M])
     }
 }
 
-using FwdFn = void (*)(FwdArgs);
-using BwdFn = void (*)(BwdArgs);
+using FwdFn = void (*)(FwdBatch);
+using BwdFn = void (*)(BwdBatch);
 
 // Kernels for m = 16 and 32 (wide.hip): four consecutive elements per lane,
 // a group spread over m / 4 adjacent lanes.

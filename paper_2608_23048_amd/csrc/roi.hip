@@ -16,7 +16,9 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <algorithm>
 #include <utility>
+#include <vector>
 
 #include "common.hpp"
 #include "noise.hpp"
@@ -158,13 +160,13 @@ __device__ __forceinline__ void fast_keys(const float (&phi)[M], const uint32_t 
     for (int j = 0; j < M; ++j) k[j] = fast_key_log2(phi[j], c, x[j]);
 }
 
-// Each iteration of a block covers kUnroll * kBlock consecutive groups: lane l
-// of the block takes groups base + u * kBlock + l, u < kUnroll, so every load
-// and store instruction of a wave is one contiguous span, and all of a lane's
-// loads are issued before its first group is computed (more bytes in flight
-// per wave for the HBM stream).
+// A block works on one piece of the batch (common.hpp).  Each iteration of a
+// block covers U * kLaneBlock consecutive groups of the piece: lane l takes
+// groups base + u * kLaneBlock + l, u < U, so every load and store instruction
+// of a wave is one contiguous span, and all of a lane's loads are issued
+// before its first group is computed (more bytes in flight per wave).
 template <int M, int N, bool kRelax, bool kWantIdx, bool kLambdaOne>
-__global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdArgs a)
+__global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
 {
     __shared__ float2 tab[kLogCells];
     __shared__ Top4Entry top4[64];
@@ -174,26 +176,30 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdArgs a)
             top4[threadIdx.x - kLogCells] = kTop4Table<N>.e[threadIdx.x - kLogCells];
     }
     __syncthreads();
+    const FwdPiece& pc = a.p[find_piece(a)];
+    NoiseKey key = a.key_base;
+    key.block_hi = pc.block_hi;
+    const int64_t ng = pc.ngroups;
     constexpr int U = kUnrollFwd<M>;
     const int64_t chunk = (int64_t)kLaneBlock * U;
-    for (int64_t base = (int64_t)blockIdx.x * chunk; base < a.ngroups;
-         base += (int64_t)gridDim.x * chunk) {
+    for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * chunk; base < ng;
+         base += (int64_t)pc.nblocks * chunk) {
         float phi[U][M];
         uint32_t w[U][M];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q < a.ngroups) {
-                load_logits<M>(a.phi + q * M, phi[u]);
-                load_bf16<M>(a.W + q * M, w[u]);
+            if (q < ng) {
+                load_logits<M>(pc.phi + q * M, phi[u]);
+                load_bf16<M>(pc.W + q * M, w[u]);
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q >= a.ngroups) continue;
+            if (q >= ng) continue;
             uint32_t x[M];
-            group_words<M>(a.block0 + (uint32_t)q * (M / 4), a.key, x);
+            group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
             float kappa[M];
             if constexpr (kRelax) {
                 // the relaxation's soft mask is an fp32 output: exact keys
@@ -212,21 +218,21 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdArgs a)
                 if (!soft) {
                     const u32x2 v = {(w[u][0] | (w[u][1] << 16)) & t4.m01,
                                      (w[u][2] | (w[u][3] << 16)) & t4.m23};
-                    stream_store(v, reinterpret_cast<u32x2*>(a.Wm + q * M));
+                    stream_store(v, reinterpret_cast<u32x2*>(pc.Wm + q * M));
                 }
-                if (kWantIdx) store_order<N>(a.idx + q * N, t4.order);
+                if (kWantIdx) store_order<N>(pc.idx + q * N, t4.order);
             } else {
                 int rank[M];
                 rank_keys<M>(kappa, rank);
-                if (!soft) store_masked<M>(a.Wm + q * M, w[u], rank, N);
-                if (kWantIdx) store_idx<M, N>(a.idx + q * N, rank);
+                if (!soft) store_masked<M>(pc.Wm + q * M, w[u], rank, N);
+                if (kWantIdx) store_idx<M, N>(pc.idx + q * N, rank);
             }
             if (kRelax) {
                 float S[M];
                 StepRec<M> unused[N]; // not written when records are not kept
                 relax_forward<M, N, true, false>(kappa, kLog2e * a.inv_tau, a.inv_tau, S, unused);
-                if (a.S) {
-                    f32x4* s4 = reinterpret_cast<f32x4*>(a.S + q * M);
+                if (pc.S) {
+                    f32x4* s4 = reinterpret_cast<f32x4*>(pc.S + q * M);
 #pragma unroll
                     for (int t = 0; t < M / 4; ++t) {
                         const f32x4 v = {S[4 * t], S[4 * t + 1], S[4 * t + 2], S[4 * t + 3]};
@@ -238,7 +244,7 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdArgs a)
 #pragma unroll
                     for (int j = 0; j < M; ++j)
                         ws[j] = float_to_bf16_rne(bf16_bits_to_float(w[u][j]) * S[j]);
-                    store_pairs<M>(a.Wm + q * M, ws);
+                    store_pairs<M>(pc.Wm + q * M, ws);
                 }
             }
         }
@@ -246,30 +252,34 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdArgs a)
 }
 
 template <int M, int N, bool kLambdaOne>
-__global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdArgs a)
+__global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
 {
+    const BwdPiece& pc = a.p[find_piece(a)];
+    NoiseKey key = a.key_base;
+    key.block_hi = pc.block_hi;
+    const int64_t ng = pc.ngroups;
     constexpr int U = kUnrollBwd<M>;
     const int64_t chunk = (int64_t)kLaneBlock * U;
-    for (int64_t base = (int64_t)blockIdx.x * chunk; base < a.ngroups;
-         base += (int64_t)gridDim.x * chunk) {
+    for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * chunk; base < ng;
+         base += (int64_t)pc.nblocks * chunk) {
         float phi[U][M];
         uint32_t w[U][M], g[U][M];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q < a.ngroups) {
-                load_logits<M>(a.phi + q * M, phi[u]);
-                load_bf16<M>(a.W + q * M, w[u]);
-                load_bf16<M>(a.G + q * M, g[u]);
+            if (q < ng) {
+                load_logits<M>(pc.phi + q * M, phi[u]);
+                load_bf16<M>(pc.W + q * M, w[u]);
+                load_bf16<M>(pc.G + q * M, g[u]);
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q >= a.ngroups) continue;
+            if (q >= ng) continue;
             // keys from the hardware logarithm, in log2 units (noise.hpp)
             uint32_t x[M];
-            group_words<M>(a.block0 + (uint32_t)q * (M / 4), a.key, x);
+            group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
             float kappa[M];
             fast_keys<M>(phi[u], x, kLambdaOne ? kLog2e : a.key_c, kappa);
             // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
@@ -282,7 +292,7 @@ __global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdArgs a)
             relax_forward<M, N, false, true>(kappa, a.inv_tau, a.inv_tau, S_unused, rec);
             float abar[M];
             relax_backward<M, N>(rec, sbar, a.tau, a.inv_tau, abar);
-            f32x4* d4 = reinterpret_cast<f32x4*>(a.dphi + q * M);
+            f32x4* d4 = reinterpret_cast<f32x4*>(pc.dphi + q * M);
 #pragma unroll
             for (int t = 0; t < M / 4; ++t) {
                 f32x4 v;
@@ -505,20 +515,6 @@ BwdFn select_bwd(int m, int n, bool l)
     return select_wide_bwd(m, n);
 }
 
-// Launch shape: one thread per U groups (and kLaneBlock threads per block)
-// for m = 4 and 8, m / 4 threads per group (kBlock per block) for m = 16, 32.
-struct LaunchShape {
-    int grid, block;
-};
-
-LaunchShape launch_shape(int64_t ngroups, int m, bool fwd)
-{
-    if (m > 8) return {grid_for(ngroups * (m / 4)), kBlock};
-    const int u = fwd ? (m == 4 ? kUnrollFwd<4> : kUnrollFwd<8>)
-                      : (m == 4 ? kUnrollBwd<4> : kUnrollBwd<8>);
-    return {grid_for(ceil_div(ngroups, u), kLaneBlock), kLaneBlock};
-}
-
 } // namespace
 } // namespace roi
 
@@ -526,60 +522,228 @@ using namespace roi;
 
 namespace roi {
 namespace {
-int mask_fwd_impl(const char* what, bool soft, const uint16_t* W, const float* logits,
-                  int64_t rows, int64_t cols, int n, int m, float tau, float lambda, uint64_t seed,
-                  uint64_t step, uint64_t elem_offset, uint16_t* W_masked, float* soft_mask,
-                  uint8_t* sel_idx, hipStream_t stream)
+
+// One checked address range of a call: [p, p + n), an input or an output.
+struct Range {
+    uintptr_t p;
+    size_t n;
+    bool out;
+};
+
+// Outputs may overlap nothing; inputs may overlap each other.  Sorted by
+// start, a range overlaps an earlier one exactly when it starts before the
+// largest end seen so far (of any range, for an output; of the outputs, for
+// an input).
+int check_overlaps(std::vector<Range>& r)
 {
-    Shape sh;
-    if (int st = check_shape(rows, cols, n, m, tau, lambda, elem_offset, &sh)) return st;
-    if (sh.numel == 0) return ok();
-    if (!W || !logits || !W_masked)
-        return fail(ROI_E_INVAL, "W, logits and W_masked must not be NULL");
-    if (!aligned16(W) || !aligned16(logits) || !aligned16(W_masked) ||
-        (soft_mask && !aligned16(soft_mask)) || (sel_idx && !aligned16(sel_idx)))
-        return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
-    const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
-    const size_t nbi = (size_t)sh.ngroups * (size_t)n;
-    const void* ins[2] = {W, logits};
-    const size_t in_n[2] = {nb2, nb4};
-    void* outs[3] = {W_masked, soft_mask, sel_idx};
-    const size_t out_n[3] = {nb2, nb4, nbi};
-    for (int i = 0; i < 3; ++i) {
-        for (int j = 0; j < 2; ++j)
-            if (overlap(outs[i], out_n[i], ins[j], in_n[j]))
-                return fail(ROI_E_INVAL, "outputs must not overlap inputs");
-        for (int j = i + 1; j < 3; ++j)
-            if (overlap(outs[i], out_n[i], outs[j], out_n[j]))
-                return fail(ROI_E_INVAL, "outputs must not overlap each other");
+    std::sort(r.begin(), r.end(), [](const Range& a, const Range& b) { return a.p < b.p; });
+    uintptr_t end_any = 0, end_out = 0;
+    for (const Range& x : r) {
+        if (x.out ? x.p < end_any : x.p < end_out)
+            return fail(ROI_E_INVAL, "an output overlaps another input or output");
+        end_any = std::max(end_any, x.p + x.n);
+        if (x.out) end_out = std::max(end_out, x.p + x.n);
     }
-    FwdFn fn = select_fwd(m, n, soft || soft_mask != nullptr, sel_idx != nullptr, lambda == 1.0f);
-    if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
-    const NoiseKey key = make_key(seed, step, 0);
-    const float inv_tau = (float)(1.0 / (double)tau);
-    const float key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
-    return for_each_piece(elem_offset, sh.ngroups, m, [&](int64_t g0, int64_t ng, uint64_t e0) {
-        FwdArgs a;
-        a.W = W + g0 * m;
-        a.phi = logits + g0 * m;
-        a.Wm = W_masked + g0 * m;
-        a.S = soft_mask ? soft_mask + g0 * m : nullptr;
-        a.idx = sel_idx ? sel_idx + g0 * n : nullptr;
-        a.ngroups = ng;
-        a.block0 = (uint32_t)(e0 / 4);
-        a.key = key;
-        a.key.block_hi = (uint32_t)((e0 / 4) >> 32);
-        a.lambda = lambda;
-        a.key_c = key_c;
-        a.inv_tau = inv_tau;
-        a.soft = soft ? 1 : 0;
-        void* args[] = {&a};
-        const LaunchShape ls = launch_shape(ng, m, true);
-        if (hipLaunchKernel((const void*)fn, dim3(ls.grid), dim3(ls.block), args, 0, stream) !=
-            hipSuccess)
-            return launch_status(what);
+    return ROI_OK;
+}
+
+void add_range(std::vector<Range>& r, const void* p, size_t n, bool out)
+{
+    if (p && n) r.push_back({(uintptr_t)p, n, out});
+}
+
+// Blocks one piece of `ngroups` groups needs in a launch.
+int64_t blocks_for(int64_t ngroups, int m, bool fwd)
+{
+    if (m > 8) return ceil_div(ngroups * (m / 4), kBlock);
+    const int u = fwd ? (m == 4 ? kUnrollFwd<4> : kUnrollFwd<8>)
+                      : (m == 4 ? kUnrollBwd<4> : kUnrollBwd<8>);
+    return ceil_div(ngroups, (int64_t)u * kLaneBlock);
+}
+
+// Collects pieces into batches of up to kMaxPieces and launches each batch as
+// one grid (kept below 2^32 threads; a piece that alone needs more blocks
+// gets the largest grid and its blocks stride over it).
+template <typename Batch, typename Piece, typename Fn>
+struct Launcher {
+    Batch batch;
+    Fn fn;
+    int block;
+    int m;
+    bool fwd;
+    hipStream_t stream;
+    const char* what;
+    int64_t blocks = 0;
+
+    int64_t max_blocks() const { return (int64_t)(0xFFFFFFFFu / (uint32_t)block); }
+
+    int flush()
+    {
+        if (batch.count == 0) return ROI_OK;
+        void* args[] = {&batch};
+        const hipError_t e = hipLaunchKernel((const void*)fn, dim3((unsigned)blocks),
+                                             dim3(block), args, 0, stream);
+        batch.count = 0;
+        blocks = 0;
+        if (e != hipSuccess) return launch_status(what);
         return launch_status(what);
-    });
+    }
+
+    int add(Piece pc)
+    {
+        const int64_t nb = std::min(blocks_for(pc.ngroups, m, fwd), max_blocks());
+        if (batch.count == kMaxPieces || blocks + nb > max_blocks())
+            if (int st = flush()) return st;
+        pc.first_block = (uint32_t)blocks;
+        pc.nblocks = (uint32_t)nb;
+        batch.p[batch.count++] = pc;
+        blocks += nb;
+        return ROI_OK;
+    }
+};
+
+int check_common(int n, int m, float tau, float lambda)
+{
+    if (m < 1 || n < 1 || n > m)
+        return fail(ROI_E_INVAL, "pattern n:m = %d:%d needs 1 <= n <= m", n, m);
+    if (m != 4 && m != 8 && m != 16 && m != 32)
+        return fail(ROI_E_UNSUPPORTED, "m = %d is not built (supported: 4, 8, 16, 32)", m);
+    if (!(tau > 0.0f) || !std::isfinite(tau))
+        return fail(ROI_E_INVAL, "tau must be finite and > 0");
+    if (!(lambda > 0.0f) || !std::isfinite(lambda))
+        return fail(ROI_E_INVAL, "lambda must be finite and > 0");
+    return ROI_OK;
+}
+
+int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count, int n, int m,
+                 float tau, float lambda, uint64_t seed, uint64_t step, hipStream_t stream)
+{
+    if (int st = check_common(n, m, tau, lambda)) return st;
+    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
+    if (count > 0 && !t) return fail(ROI_E_INVAL, "tensors must not be NULL");
+    std::vector<Range> ranges;
+    int with_s = -1, with_idx = -1; // -1: no nonempty tensor seen yet
+    for (int i = 0; i < count; ++i) {
+        Shape sh;
+        if (int st = check_shape(t[i].rows, t[i].cols, n, m, tau, lambda, t[i].elem_offset, &sh))
+            return count > 1 ? fail(st, "tensor %d: %s", i, g_last_error.c_str()) : st;
+        if (sh.numel == 0) continue;
+        if (!t[i].W || !t[i].logits || !t[i].W_masked)
+            return fail(ROI_E_INVAL, "tensor %d: W, logits and W_masked must not be NULL", i);
+        if (!aligned16(t[i].W) || !aligned16(t[i].logits) || !aligned16(t[i].W_masked) ||
+            (t[i].soft_mask && !aligned16(t[i].soft_mask)) ||
+            (t[i].sel_idx && !aligned16(t[i].sel_idx)))
+            return fail(ROI_E_INVAL, "tensor %d: device pointers must be 16-byte aligned", i);
+        const int s_i = t[i].soft_mask != nullptr, x_i = t[i].sel_idx != nullptr;
+        if ((with_s >= 0 && s_i != with_s) || (with_idx >= 0 && x_i != with_idx))
+            return fail(ROI_E_INVAL,
+                        "soft_mask and sel_idx must each be given for every tensor or for none");
+        with_s = s_i;
+        with_idx = x_i;
+        const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
+        add_range(ranges, t[i].W, nb2, false);
+        add_range(ranges, t[i].logits, nb4, false);
+        add_range(ranges, t[i].W_masked, nb2, true);
+        add_range(ranges, t[i].soft_mask, nb4, true);
+        add_range(ranges, t[i].sel_idx, (size_t)sh.ngroups * (size_t)n, true);
+    }
+    if (with_s < 0) return ok(); // nothing to do
+    if (int st = check_overlaps(ranges)) return st;
+    FwdFn fn = select_fwd(m, n, soft || with_s == 1, with_idx == 1, lambda == 1.0f);
+    if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
+    Launcher<FwdBatch, FwdPiece, FwdFn> L{};
+    L.fn = fn;
+    L.block = m > 8 ? kBlock : kLaneBlock;
+    L.m = m;
+    L.fwd = true;
+    L.stream = stream;
+    L.what = what;
+    L.batch.key_base = make_key(seed, step, 0);
+    L.batch.lambda = lambda;
+    L.batch.key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
+    L.batch.inv_tau = (float)(1.0 / (double)tau);
+    L.batch.soft = soft ? 1 : 0;
+    for (int i = 0; i < count; ++i) {
+        const int64_t ngroups = t[i].rows * t[i].cols / m;
+        if (ngroups == 0) continue;
+        const int st = for_each_piece(t[i].elem_offset, ngroups, m,
+                                      [&](int64_t g0, int64_t ng, uint64_t e0) {
+            FwdPiece pc{};
+            pc.W = t[i].W + g0 * m;
+            pc.phi = t[i].logits + g0 * m;
+            pc.Wm = t[i].W_masked + g0 * m;
+            pc.S = t[i].soft_mask ? t[i].soft_mask + g0 * m : nullptr;
+            pc.idx = t[i].sel_idx ? t[i].sel_idx + g0 * n : nullptr;
+            pc.ngroups = ng;
+            pc.block0 = (uint32_t)(e0 / 4);
+            pc.block_hi = (uint32_t)((e0 / 4) >> 32);
+            return L.add(pc);
+        });
+        if (st) return st;
+    }
+    return L.flush();
+}
+
+int mask_bwd_run(const roi_bwd_tensor* t, int count, int n, int m, float tau, float lambda,
+                 uint64_t seed, uint64_t step, hipStream_t stream)
+{
+    if (int st = check_common(n, m, tau, lambda)) return st;
+    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
+    if (count > 0 && !t) return fail(ROI_E_INVAL, "tensors must not be NULL");
+    std::vector<Range> ranges;
+    bool any = false;
+    for (int i = 0; i < count; ++i) {
+        Shape sh;
+        if (int st = check_shape(t[i].rows, t[i].cols, n, m, tau, lambda, t[i].elem_offset, &sh))
+            return count > 1 ? fail(st, "tensor %d: %s", i, g_last_error.c_str()) : st;
+        if (sh.numel == 0) continue;
+        if (!t[i].grad_W_masked || !t[i].W || !t[i].logits || !t[i].grad_logits)
+            return fail(ROI_E_INVAL,
+                        "tensor %d: grad_W_masked, W, logits and grad_logits must not be NULL", i);
+        if (!aligned16(t[i].grad_W_masked) || !aligned16(t[i].W) || !aligned16(t[i].logits) ||
+            !aligned16(t[i].grad_logits))
+            return fail(ROI_E_INVAL, "tensor %d: device pointers must be 16-byte aligned", i);
+        const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
+        add_range(ranges, t[i].grad_W_masked, nb2, false);
+        add_range(ranges, t[i].W, nb2, false);
+        add_range(ranges, t[i].logits, nb4, false);
+        add_range(ranges, t[i].grad_logits, nb4, true);
+        any = true;
+    }
+    if (!any) return ok();
+    if (int st = check_overlaps(ranges)) return st;
+    BwdFn fn = select_bwd(m, n, lambda == 1.0f);
+    if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
+    Launcher<BwdBatch, BwdPiece, BwdFn> L{};
+    L.fn = fn;
+    L.block = m > 8 ? kBlock : kLaneBlock;
+    L.m = m;
+    L.fwd = false;
+    L.stream = stream;
+    L.what = "roi_mask_bwd";
+    L.batch.key_base = make_key(seed, step, 0);
+    L.batch.key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
+    L.batch.inv_lambda = (float)(1.0 / (double)lambda);
+    L.batch.tau = tau;
+    L.batch.inv_tau = (float)(1.0 / (double)tau);
+    for (int i = 0; i < count; ++i) {
+        const int64_t ngroups = t[i].rows * t[i].cols / m;
+        if (ngroups == 0) continue;
+        const int st = for_each_piece(t[i].elem_offset, ngroups, m,
+                                      [&](int64_t g0, int64_t ng, uint64_t e0) {
+            BwdPiece pc{};
+            pc.G = t[i].grad_W_masked + g0 * m;
+            pc.W = t[i].W + g0 * m;
+            pc.phi = t[i].logits + g0 * m;
+            pc.dphi = t[i].grad_logits + g0 * m;
+            pc.ngroups = ng;
+            pc.block0 = (uint32_t)(e0 / 4);
+            pc.block_hi = (uint32_t)((e0 / 4) >> 32);
+            return L.add(pc);
+        });
+        if (st) return st;
+    }
+    return L.flush();
 }
 } // namespace
 } // namespace roi
@@ -589,8 +753,8 @@ extern "C" int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows
                             uint64_t elem_offset, uint16_t* W_masked, float* soft_mask,
                             uint8_t* sel_idx, hipStream_t stream)
 {
-    return mask_fwd_impl("roi_mask_fwd", false, W, logits, rows, cols, n, m, tau, lambda, seed,
-                         step, elem_offset, W_masked, soft_mask, sel_idx, stream);
+    const roi_fwd_tensor t = {W, logits, W_masked, soft_mask, sel_idx, rows, cols, elem_offset};
+    return mask_fwd_run("roi_mask_fwd", false, &t, 1, n, m, tau, lambda, seed, step, stream);
 }
 
 extern "C" int roi_mask_fwd_soft(const uint16_t* W, const float* logits, int64_t rows,
@@ -599,8 +763,24 @@ extern "C" int roi_mask_fwd_soft(const uint16_t* W, const float* logits, int64_t
                                  uint16_t* W_soft, float* soft_mask, uint8_t* sel_idx,
                                  hipStream_t stream)
 {
-    return mask_fwd_impl("roi_mask_fwd_soft", true, W, logits, rows, cols, n, m, tau, lambda,
-                         seed, step, elem_offset, W_soft, soft_mask, sel_idx, stream);
+    const roi_fwd_tensor t = {W, logits, W_soft, soft_mask, sel_idx, rows, cols, elem_offset};
+    return mask_fwd_run("roi_mask_fwd_soft", true, &t, 1, n, m, tau, lambda, seed, step, stream);
+}
+
+extern "C" int roi_mask_fwd_grouped(const roi_fwd_tensor* tensors, int count, int n, int m,
+                                    float tau, float lambda, uint64_t seed, uint64_t step,
+                                    hipStream_t stream)
+{
+    return mask_fwd_run("roi_mask_fwd_grouped", false, tensors, count, n, m, tau, lambda, seed,
+                        step, stream);
+}
+
+extern "C" int roi_mask_fwd_soft_grouped(const roi_fwd_tensor* tensors, int count, int n, int m,
+                                         float tau, float lambda, uint64_t seed, uint64_t step,
+                                         hipStream_t stream)
+{
+    return mask_fwd_run("roi_mask_fwd_soft_grouped", true, tensors, count, n, m, tau, lambda,
+                        seed, step, stream);
 }
 
 extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
@@ -608,44 +788,15 @@ extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, co
                             uint64_t seed, uint64_t step, uint64_t elem_offset, float* grad_logits,
                             hipStream_t stream)
 {
-    Shape sh;
-    if (int st = check_shape(rows, cols, n, m, tau, lambda, elem_offset, &sh)) return st;
-    if (sh.numel == 0) return ok();
-    if (!grad_W_masked || !W || !logits || !grad_logits)
-        return fail(ROI_E_INVAL, "grad_W_masked, W, logits and grad_logits must not be NULL");
-    if (!aligned16(grad_W_masked) || !aligned16(W) || !aligned16(logits) || !aligned16(grad_logits))
-        return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
-    const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
-    if (overlap(grad_logits, nb4, grad_W_masked, nb2) || overlap(grad_logits, nb4, W, nb2) ||
-        overlap(grad_logits, nb4, logits, nb4))
-        return fail(ROI_E_INVAL, "grad_logits must not overlap the inputs");
-    BwdFn fn = select_bwd(m, n, lambda == 1.0f);
-    if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
-    const NoiseKey key = make_key(seed, step, 0);
-    const float inv_lambda = (float)(1.0 / (double)lambda);
-    const float inv_tau = (float)(1.0 / (double)tau);
-    const float key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
-    return for_each_piece(elem_offset, sh.ngroups, m, [&](int64_t g0, int64_t ng, uint64_t e0) {
-        BwdArgs a;
-        a.G = grad_W_masked + g0 * m;
-        a.W = W + g0 * m;
-        a.phi = logits + g0 * m;
-        a.dphi = grad_logits + g0 * m;
-        a.ngroups = ng;
-        a.block0 = (uint32_t)(e0 / 4);
-        a.key = key;
-        a.key.block_hi = (uint32_t)((e0 / 4) >> 32);
-        a.key_c = key_c;
-        a.inv_lambda = inv_lambda;
-        a.tau = tau;
-        a.inv_tau = inv_tau;
-        void* args[] = {&a};
-        const LaunchShape ls = launch_shape(ng, m, false);
-        if (hipLaunchKernel((const void*)fn, dim3(ls.grid), dim3(ls.block), args, 0, stream) !=
-            hipSuccess)
-            return launch_status("roi_mask_bwd");
-        return launch_status("roi_mask_bwd");
-    });
+    const roi_bwd_tensor t = {grad_W_masked, W, logits, grad_logits, rows, cols, elem_offset};
+    return mask_bwd_run(&t, 1, n, m, tau, lambda, seed, step, stream);
+}
+
+extern "C" int roi_mask_bwd_grouped(const roi_bwd_tensor* tensors, int count, int n, int m,
+                                    float tau, float lambda, uint64_t seed, uint64_t step,
+                                    hipStream_t stream)
+{
+    return mask_bwd_run(tensors, count, n, m, tau, lambda, seed, step, stream);
 }
 
 extern "C" int roi_gumbel_noise(uint64_t seed, uint64_t step, uint64_t elem_offset, int64_t count,

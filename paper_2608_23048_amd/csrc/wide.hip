@@ -203,43 +203,47 @@ __device__ __forceinline__ void wide_keys(const float (&phi)[4], uint32_t block,
 }
 
 template <int M, int N>
-__global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdArgs a)
+__global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
 {
     constexpr int L = M / 4;
     __shared__ float2 tab[kLogCells];
     fill_log_table(tab);
     __syncthreads();
-    const int64_t nslots = a.ngroups * L;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t slot = (int64_t)blockIdx.x * kBlock + threadIdx.x; slot < nslots; slot += stride) {
+    const FwdPiece& pc = a.p[find_piece(a)];
+    NoiseKey key = a.key_base;
+    key.block_hi = pc.block_hi;
+    const int64_t nslots = pc.ngroups * L;
+    const int64_t stride = (int64_t)pc.nblocks * kBlock;
+    for (int64_t slot = (int64_t)(blockIdx.x - pc.first_block) * kBlock + threadIdx.x;
+         slot < nslots; slot += stride) {
         const int part = (int)(slot % L);
         const int64_t group = slot / L;
-        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(a.phi + slot * 4));
-        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(a.W + slot * 4));
+        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
+        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
         const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
         float kappa[4];
-        wide_keys(phi, a.block0 + (uint32_t)slot, a.key, a.lambda, tab, kappa);
+        wide_keys(phi, pc.block0 + (uint32_t)slot, key, a.lambda, tab, kappa);
         int rank[4];
         wide_rank<L>(kappa, part, rank);
         if (!a.soft) {
             const uint32_t m01 = (rank[0] < N ? 0x0000FFFFu : 0u) | (rank[1] < N ? 0xFFFF0000u : 0u);
             const uint32_t m23 = (rank[2] < N ? 0x0000FFFFu : 0u) | (rank[3] < N ? 0xFFFF0000u : 0u);
             const u32x2 out = {wv.x & m01, wv.y & m23};
-            stream_store(out, reinterpret_cast<u32x2*>(a.Wm + slot * 4));
+            stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
         }
-        if (a.idx) {
+        if (pc.idx) {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                if (rank[e] < N) a.idx[group * N + rank[e]] = (uint8_t)(part * 4 + e);
+                if (rank[e] < N) pc.idx[group * N + rank[e]] = (uint8_t)(part * 4 + e);
         }
-        if (a.S || a.soft) {
+        if (pc.S || a.soft) {
             float S[4];
             StepRec<4> unused[N]; // not written when records are not kept
             wide_relax_forward<L, N, false>(kappa, kLog2e * a.inv_tau, a.inv_tau, true, S,
                                             unused);
-            if (a.S) {
+            if (pc.S) {
                 const f32x4 sv = {S[0], S[1], S[2], S[3]};
-                stream_store(sv, reinterpret_cast<f32x4*>(a.S + slot * 4));
+                stream_store(sv, reinterpret_cast<f32x4*>(pc.S + slot * 4));
             }
             if (a.soft) { // pure soft forward: W (.) S, rounded to bf16
                 const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
@@ -247,25 +251,29 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdArgs a)
                 const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
                 const uint32_t h3 = float_to_bf16_rne(bf16_bits_to_float(wv.y >> 16) * S[3]);
                 const u32x2 out = {h0 | (h1 << 16), h2 | (h3 << 16)};
-                stream_store(out, reinterpret_cast<u32x2*>(a.Wm + slot * 4));
+                stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
             }
         }
     }
 }
 
 template <int M, int N>
-__global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdArgs a)
+__global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
 {
     constexpr int L = M / 4;
-    const int64_t nslots = a.ngroups * L;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t slot = (int64_t)blockIdx.x * kBlock + threadIdx.x; slot < nslots; slot += stride) {
-        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(a.phi + slot * 4));
-        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(a.W + slot * 4));
-        const u32x2 gv = stream_load(reinterpret_cast<const u32x2*>(a.G + slot * 4));
+    const BwdPiece& pc = a.p[find_piece(a)];
+    NoiseKey key = a.key_base;
+    key.block_hi = pc.block_hi;
+    const int64_t nslots = pc.ngroups * L;
+    const int64_t stride = (int64_t)pc.nblocks * kBlock;
+    for (int64_t slot = (int64_t)(blockIdx.x - pc.first_block) * kBlock + threadIdx.x;
+         slot < nslots; slot += stride) {
+        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
+        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
+        const u32x2 gv = stream_load(reinterpret_cast<const u32x2*>(pc.G + slot * 4));
         const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
         // keys from the hardware logarithm, in log2 units (noise.hpp)
-        const uint4 x = philox_block(a.block0 + (uint32_t)slot, a.key);
+        const uint4 x = philox_block(pc.block0 + (uint32_t)slot, key);
         const float kappa[4] = {fast_key_log2(phi[0], a.key_c, x.x),
                                 fast_key_log2(phi[1], a.key_c, x.y),
                                 fast_key_log2(phi[2], a.key_c, x.z),
@@ -284,7 +292,7 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdArgs a)
         // dL/dphi = dL/dkappa / lambda (the product is exact for lambda = 1)
         const f32x4 dv = {abar[0] * a.inv_lambda, abar[1] * a.inv_lambda,
                           abar[2] * a.inv_lambda, abar[3] * a.inv_lambda};
-        stream_store(dv, reinterpret_cast<f32x4*>(a.dphi + slot * 4));
+        stream_store(dv, reinterpret_cast<f32x4*>(pc.dphi + slot * 4));
     }
 }
 

@@ -32,6 +32,7 @@ def test_exports_every_declared_symbol(L):
     names = header_functions()
     assert {"roi_mask_fwd", "roi_mask_fwd_soft", "roi_mask_bwd", "roi_gumbel_noise",
             "roi_gumbel_from_words", "roi_fast_noise_from_words",
+            "roi_mask_fwd_grouped", "roi_mask_fwd_soft_grouped", "roi_mask_bwd_grouped",
             "roi_anneal", "roi_status_string", "roi_last_error", "roi_abi_version"} <= set(names)
     for name in names:
         assert hasattr(L, name), name
@@ -114,6 +115,79 @@ def test_fwd_rejects_before_launch(L, kw, status):
 ])
 def test_bwd_rejects_before_launch(L, kw, status):
     assert bwd(L, **kw) == status
+
+
+GB = 1 << 30
+
+
+def fwd_desc(i, **kw):
+    """Fake descriptor i (disjoint 1 GiB slots per tensor); never launched."""
+    base = FAKE + i * 8 * GB
+    a = dict(W=base, logits=base + GB, W_masked=base + 2 * GB, soft_mask=None, sel_idx=None,
+             rows=4, cols=8, elem_offset=i * 32)
+    a.update(kw)
+    return roi.FwdTensor(a["W"], a["logits"], a["W_masked"], a["soft_mask"], a["sel_idx"],
+                         a["rows"], a["cols"], a["elem_offset"])
+
+
+def bwd_desc(i, **kw):
+    base = FAKE + i * 8 * GB
+    a = dict(G=base, W=base + GB, logits=base + 2 * GB, d=base + 3 * GB, rows=4, cols=8,
+             elem_offset=i * 32)
+    a.update(kw)
+    return roi.BwdTensor(a["G"], a["W"], a["logits"], a["d"], a["rows"], a["cols"],
+                         a["elem_offset"])
+
+
+def grouped(L, fn, descs, n=2, m=4, tau=1.0, lam=1.0):
+    T = type(descs[0]) if descs else roi.FwdTensor
+    arr = (T * max(1, len(descs)))(*descs)
+    return getattr(L, fn)(ctypes.addressof(arr), len(descs), n, m, tau, lam, 0, 0, None)
+
+
+@pytest.mark.parametrize("fn", ["roi_mask_fwd_grouped", "roi_mask_fwd_soft_grouped"])
+def test_fwd_grouped_rejects_before_launch(L, fn):
+    ok = [fwd_desc(0), fwd_desc(1)]
+    cases = [
+        ([ok[0], fwd_desc(1, cols=6)], roi.ROI_E_INVAL, "tensor 1"),
+        ([ok[0], fwd_desc(1, elem_offset=34)], roi.ROI_E_INVAL, "tensor 1"),
+        ([ok[0], fwd_desc(1, W=None)], roi.ROI_E_INVAL, "tensor 1"),
+        ([fwd_desc(0, logits=FAKE + GB + 4), ok[1]], roi.ROI_E_INVAL, "tensor 0"),
+        ([fwd_desc(0, sel_idx=FAKE + 3 * GB), ok[1]], roi.ROI_E_INVAL, "every tensor"),
+        ([ok[0], fwd_desc(1, soft_mask=FAKE + 8 * GB + 3 * GB)], roi.ROI_E_INVAL, "every tensor"),
+        ([ok[0], fwd_desc(1, W_masked=FAKE + GB + 64)], roi.ROI_E_INVAL, "overlap"),  # into logits 0
+        ([ok[0], fwd_desc(1, W_masked=FAKE + 2 * GB)], roi.ROI_E_INVAL, "overlap"),  # same output
+    ]
+    for descs, status, msg in cases:
+        assert grouped(L, fn, descs) == status
+        assert msg in L.roi_last_error().decode()
+    assert grouped(L, fn, ok, m=12, n=6) == roi.ROI_E_UNSUPPORTED
+    assert grouped(L, fn, ok, tau=0.0) == roi.ROI_E_INVAL
+    assert L.roi_mask_fwd_grouped(None, 2, 2, 4, 1.0, 1.0, 0, 0, None) == roi.ROI_E_INVAL
+    assert L.roi_mask_fwd_grouped(None, -1, 2, 4, 1.0, 1.0, 0, 0, None) == roi.ROI_E_INVAL
+    # nothing to do: no tensors, or only empty ones (their pointers are never read)
+    assert L.roi_mask_fwd_grouped(None, 0, 2, 4, 1.0, 1.0, 0, 0, None) == roi.ROI_OK
+    empty = [fwd_desc(0, rows=0, W=None, logits=None, W_masked=None), fwd_desc(1, cols=0)]
+    assert grouped(L, fn, empty) == roi.ROI_OK
+
+
+def test_bwd_grouped_rejects_before_launch(L):
+    ok = [bwd_desc(0), bwd_desc(1)]
+    cases = [
+        ([ok[0], bwd_desc(1, cols=10)], roi.ROI_E_INVAL, "tensor 1"),
+        ([ok[0], bwd_desc(1, d=None)], roi.ROI_E_INVAL, "tensor 1"),
+        ([bwd_desc(0, G=FAKE + 2), ok[1]], roi.ROI_E_INVAL, "tensor 0"),
+        ([ok[0], bwd_desc(1, d=FAKE + 2 * GB)], roi.ROI_E_INVAL, "overlap"),  # logits of tensor 0
+        ([bwd_desc(0, W=FAKE + 8 * GB + GB), ok[1]], roi.ROI_E_INVAL, None),  # shared input: fine,
+    ]
+    for descs, status, msg in cases[:-1]:
+        assert grouped(L, "roi_mask_bwd_grouped", descs) == status
+        assert msg in L.roi_last_error().decode()
+    # inputs may be shared between tensors; the call still fails here, on the
+    # unsupported pattern, before anything is launched
+    assert grouped(L, "roi_mask_bwd_grouped", cases[-1][0], m=64, n=2) == roi.ROI_E_UNSUPPORTED
+    assert L.roi_mask_bwd_grouped(None, 0, 2, 4, 1.0, 1.0, 0, 0, None) == roi.ROI_OK
+    assert L.roi_mask_bwd_grouped(None, 3, 2, 4, 1.0, 1.0, 0, 0, None) == roi.ROI_E_INVAL
 
 
 def test_empty_input_is_a_no_op(L):

@@ -279,6 +279,79 @@ def test_split_calls_equal_one_slab_call(dev):
             assert torch.equal(d_t.reshape(-1).view(torch.int32), d[sl].view(torch.int32))
 
 
+def grouped_inputs(dev, m, count=20, seed=5):
+    """`count` separately allocated tensors of mixed shapes (cols % 32 == 0),
+    one of them empty, with stack offsets except one piece placed just below
+    a multiple of 2^34 elements, so that its noise crosses the boundary."""
+    import torch
+    rng = np.random.default_rng(seed)
+    shapes = [(int(rng.integers(1, 90)), 32 * int(rng.integers(1, 9))) for _ in range(count)]
+    shapes[3] = (0, 64)
+    if count > 7:
+        shapes[7] = (40, 96)
+    gen = torch.Generator(device="cpu").manual_seed(seed)
+    tensors, offsets, off = [], [], 0
+    for i, (r, c) in enumerate(shapes):
+        W = (torch.randn(r, c, generator=gen) * 0.02).to(torch.bfloat16).to(dev)
+        L = torch.randn(r, c, generator=gen).to(dev)
+        G = (torch.randn(r, c, generator=gen) * 1e-3).to(torch.bfloat16).to(dev)
+        tensors.append((W, L, G))
+        if i == 7:
+            off = (1 << 34) - 32 * ((r * c // 2) // 32)
+        offsets.append(off)
+        off += r * c
+    return tensors, offsets
+
+
+@pytest.mark.parametrize("n,m", [(2, 4), (4, 8), (8, 16), (16, 32)])
+def test_grouped_equals_single_calls(dev, n, m):
+    """The grouped calls over separately allocated tensors give, bit for bit,
+    the outputs of one single-tensor call per tensor (forward with and
+    without S and indices, soft forward, backward)."""
+    import torch
+    say(f"grouped vs single {n}:{m}")
+    tensors, offs = grouped_inputs(dev, m)
+    args = (n, m, 0.7, 1.0, 13, 4)
+    for soft, want_soft, want_idx in ((False, False, True), (False, True, True),
+                                      (False, False, False), (True, True, True)):
+        outs = roi.mask_fwd_grouped([(W, L) for W, L, _ in tensors], *args, offsets=offs,
+                                    want_soft=want_soft, want_idx=want_idx, soft_forward=soft)
+        for (W, L, _), off, (Wm, S, idx) in zip(tensors, offs, outs):
+            Wm1, S1, idx1 = roi.mask_fwd(W, L, *args, elem_offset=off, want_soft=want_soft,
+                                         want_idx=want_idx, soft_forward=soft)
+            torch.cuda.synchronize()
+            assert torch.equal(Wm.view(torch.int16), Wm1.view(torch.int16))
+            if want_soft:
+                assert torch.equal(S.view(torch.int32), S1.view(torch.int32))
+            if want_idx:
+                assert torch.equal(idx, idx1)
+    ds = roi.mask_bwd_grouped([(G, W, L) for W, L, G in tensors], *args, offsets=offs)
+    for (W, L, G), off, d in zip(tensors, offs, ds):
+        d1 = roi.mask_bwd(G, W, L, *args, elem_offset=off)
+        torch.cuda.synchronize()
+        assert torch.equal(d.view(torch.int32), d1.view(torch.int32))
+
+
+def test_grouped_against_oracle(dev):
+    """A grouped call over separate tensors against the oracle, tensor by tensor."""
+    import torch
+    say("grouped vs oracle 2:4")
+    tensors, offs = grouped_inputs(dev, 4, count=6, seed=9)
+    n, m, tau, lam, seed, step = 2, 4, 0.5, 1.0, 3, 2
+    outs = roi.mask_fwd_grouped([(W, L) for W, L, _ in tensors], n, m, tau, lam, seed, step,
+                                offsets=offs, want_soft=True)
+    ds = roi.mask_bwd_grouped([(G, W, L) for W, L, G in tensors], n, m, tau, lam, seed, step,
+                              offsets=offs)
+    torch.cuda.synchronize()
+    for (W, L, G), off, (Wm, S, idx), d in zip(tensors, offs, outs, ds):
+        Wm_o, S_o, idx_o = oracle.mask_fwd(bf16_bits(W), f32(L), n, m, tau, lam, seed, step, off)
+        d_o = oracle.mask_bwd(bf16_bits(G), bf16_bits(W), f32(L), n, m, tau, lam, seed, step, off)
+        assert np.array_equal(idx.cpu().numpy(), idx_o)
+        assert np.array_equal(bf16_bits(Wm).reshape(-1), Wm_o)
+        assert_close(f32(S), S_o, "soft mask (grouped)")
+        assert_close(f32(d), d_o, "grad_logits (grouped)")
+
+
 def test_every_output_written_and_deterministic(dev):
     import torch
     W, L, G = wl.small_case(333, 64, 1, device=dev)
