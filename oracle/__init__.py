@@ -94,6 +94,9 @@ def lib():
         L.roi_oracle_bwd_groups.restype = _int
         L.oracle_anneal.argtypes = [_f64, _f64, _f64, _f64]
         L.oracle_anneal.restype = _f64
+        L.oracle_adamw.argtypes = [_f64p, _i64, _f64, _f64, _f64, _f64, _f64, _i64, _f32p, _f32p,
+                                   _f32p, _f64p, _f64p, _f64p]
+        L.oracle_adamw.restype = _int
         _lib = L
     return _lib
 
@@ -188,6 +191,23 @@ def relax_bwd(kappa, n: int, tau: float, sbar) -> np.ndarray:
 
 def anneal(v_init: float, v_end: float, t: float, t_anneal: float) -> float:
     return float(lib().oracle_anneal(v_init, v_end, t, t_anneal))
+
+
+def adamw(grad, phi, m, v, lr: float, beta1: float, beta2: float, eps: float,
+          weight_decay: float, t: int):
+    """One AdamW step (fp64) from the fp64 gradient and the fp32 logits and
+    moments; returns (phi, m, v) in fp64."""
+    g = np.ascontiguousarray(grad, dtype=np.float64).reshape(-1)
+    p = np.ascontiguousarray(phi, dtype=np.float32).reshape(-1)
+    mm = np.ascontiguousarray(m, dtype=np.float32).reshape(-1)
+    vv = np.ascontiguousarray(v, dtype=np.float32).reshape(-1)
+    assert g.size == p.size == mm.size == vv.size
+    po, mo, vo = (np.empty(g.size, dtype=np.float64) for _ in range(3))
+    _check(lib().oracle_adamw(_ptr(g, ctypes.c_double), g.size, lr, beta1, beta2, eps,
+                              weight_decay, t, _ptr(p, ctypes.c_float), _ptr(mm, ctypes.c_float),
+                              _ptr(vv, ctypes.c_float), _ptr(po, ctypes.c_double),
+                              _ptr(mo, ctypes.c_double), _ptr(vo, ctypes.c_double)), "adamw")
+    return po, mo, vo
 
 
 # --------------------------------------------------------------------------- whole arrays

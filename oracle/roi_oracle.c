@@ -498,3 +498,37 @@ double oracle_anneal(double v_init, double v_end, double t, double t_anneal)
     double v = v_init * pow(v_end / v_init, t / t_anneal);
     return v > v_end ? v : v_end;
 }
+
+/* ------------------------------------------------------------------------- *
+ * 8. AdamW on the logits (appendix hyperparameters: the logits are trained
+ *    with AdamW, beta1 = 0.9, beta2 = 0.95, weight decay 0.05 and a decaying
+ *    learning rate; the weights stay frozen).  AdamW is decoupled weight
+ *    decay (Loshchilov & Hutter, ICLR 2019) followed by Adam's bias-corrected
+ *    moment step (Kingma & Ba, ICLR 2015), at optimizer step t >= 1:
+ *        phi <- phi (1 - lr wd)
+ *        m   <- beta1 m + (1 - beta1) g
+ *        v   <- beta2 v + (1 - beta2) g^2
+ *        phi <- phi - lr (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ *    in fp64 from the fp32 state and the fp64 gradient.
+ * ------------------------------------------------------------------------- */
+int oracle_adamw(const double* grad, int64_t numel, double lr, double beta1, double beta2,
+                 double eps, double weight_decay, int64_t t, const float* phi, const float* m,
+                 const float* v, double* phi_out, double* m_out, double* v_out)
+{
+    if (numel < 0 || t < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) ||
+        !(eps > 0.0) || !(lr >= 0.0) || !(weight_decay >= 0.0))
+        return -1;
+    const double bc1 = 1.0 - pow(beta1, (double)t);
+    const double bc2 = 1.0 - pow(beta2, (double)t);
+    for (int64_t i = 0; i < numel; ++i) {
+        const double g = grad[i];
+        double p = (double)phi[i] * (1.0 - lr * weight_decay);
+        const double mm = beta1 * (double)m[i] + (1.0 - beta1) * g;
+        const double vv = beta2 * (double)v[i] + (1.0 - beta2) * g * g;
+        p -= lr * (mm / bc1) / (sqrt(vv / bc2) + eps);
+        phi_out[i] = p;
+        m_out[i] = mm;
+        v_out[i] = vv;
+    }
+    return 0;
+}

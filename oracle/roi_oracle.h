@@ -56,6 +56,11 @@ int roi_oracle_bwd_groups(const uint16_t* grad_W_masked, const uint16_t* W, cons
 /* Exponential annealing of a temperature. */
 double oracle_anneal(double v_init, double v_end, double t, double t_anneal);
 
+/* AdamW step on numel logits from an fp64 gradient (fp64 outputs). */
+int oracle_adamw(const double* grad, int64_t numel, double lr, double beta1, double beta2,
+                 double eps, double weight_decay, int64_t t, const float* phi, const float* m,
+                 const float* v, double* phi_out, double* m_out, double* v_out);
+
 #ifdef __cplusplus
 }
 #endif

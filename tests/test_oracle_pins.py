@@ -562,3 +562,57 @@ def test_anneal_schedule_paper_hyperparameters():
     # 10-step schedule from 1.0 to 0.1 reaching 0.1 at the last step
     taus = [oracle.anneal(1.0, 0.1, t, 9) for t in range(10)]
     assert taus[0] == 1.0 and math.isclose(taus[9], 0.1, rel_tol=1e-12)
+
+
+# --------------------------------------------------------------------------- AdamW on the logits
+def _torch_adamw_step(phi, m, v, g, lr, b1, b2, eps, wd, t):
+    """One step of PyTorch's AdamW (fp64, CPU) from an explicit state."""
+    import torch
+    p = torch.tensor(np.asarray(phi, np.float64), requires_grad=True)
+    opt = torch.optim.AdamW([p], lr=lr, betas=(b1, b2), eps=eps, weight_decay=wd, foreach=False)
+    opt.state[p] = {"step": torch.tensor(float(t - 1), dtype=torch.float64),
+                    "exp_avg": torch.tensor(np.asarray(m, np.float64)),
+                    "exp_avg_sq": torch.tensor(np.asarray(v, np.float64))}
+    p.grad = torch.tensor(np.asarray(g, np.float64))
+    opt.step()
+    st = opt.state[p]
+    return p.detach().numpy(), st["exp_avg"].numpy(), st["exp_avg_sq"].numpy()
+
+
+@pytest.mark.parametrize("t,lr", [(1, 1e-3), (2, 1e-3), (7, 5e-4), (100, 2e-4), (1500, 1e-4)])
+def test_adamw_matches_torch(t, lr):
+    """The oracle's AdamW step against PyTorch's AdamW implementation (fp64) on
+    random states, with the appendix's betas and weight decay."""
+    rng = np.random.default_rng(t)
+    n = 4096
+    phi = rng.normal(0, 1, n).astype(np.float32)
+    m = (rng.normal(0, 1e-4, n)).astype(np.float32)
+    v = (rng.random(n) * 1e-8).astype(np.float32)
+    g = rng.normal(0, 1e-4, n)
+    got = oracle.adamw(g, phi, m, v, lr, 0.9, 0.95, 1e-8, 0.05, t)
+    ref = _torch_adamw_step(phi, m, v, g, lr, 0.9, 0.95, 1e-8, 0.05, t)
+    for a, b in zip(got, ref):
+        np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-18)
+
+
+def test_adamw_closed_forms():
+    """From a zero state at t = 1 the step is phi (1 - lr wd) - lr g / (|g| + eps);
+    a zero gradient with zero moments only decays; lr = 0 changes nothing."""
+    rng = np.random.default_rng(11)
+    phi = rng.normal(0, 1, 1000).astype(np.float32)
+    g = rng.normal(0, 1e-3, 1000)
+    z = np.zeros(1000, np.float32)
+    lr, wd, eps = 1e-3, 0.05, 1e-8
+    p, m, v = oracle.adamw(g, phi, z, z, lr, 0.9, 0.95, eps, wd, 1)
+    phi64 = phi.astype(np.float64)
+    np.testing.assert_allclose(p, phi64 * (1 - lr * wd) - lr * g / (np.abs(g) + eps), rtol=1e-14)
+    np.testing.assert_allclose(m, 0.1 * g, rtol=1e-14)
+    np.testing.assert_allclose(v, 0.05 * g * g, rtol=1e-14)
+    p, _, _ = oracle.adamw(np.zeros(1000), phi, z, z, lr, 0.9, 0.95, eps, wd, 5)
+    np.testing.assert_allclose(p, phi64 * (1 - lr * wd), rtol=1e-15)
+    m0 = rng.normal(0, 1, 1000).astype(np.float32)
+    v0 = rng.random(1000).astype(np.float32)
+    p, m, v = oracle.adamw(g, phi, m0, v0, 0.0, 0.9, 0.95, eps, wd, 3)
+    np.testing.assert_array_equal(p, phi.astype(np.float64))
+    with pytest.raises(ValueError):
+        oracle.adamw(g, phi, z, z, lr, 0.9, 0.95, eps, wd, 0)
