@@ -144,6 +144,124 @@ def cpu_baseline(W, L, G, work, n, m, tau):
             "sample": f"layer 0 {names} ({end} weights), one mask fwd+bwd, {dt:.1f} s on 1 thread"}
 
 
+def run_adamw(args) -> int:
+    """--mode adamw: the training step with the optimizer, as the appendix
+    trains the logits: forward (masked weights + indices) and the backward with
+    one AdamW step fused in (beta 0.9 / 0.95, weight decay 0.05, the learning
+    rate annealed 1e-3 -> 1e-4 like the temperatures).  For comparison, the
+    same step unfused: roi_mask_bwd, then PyTorch's fused AdamW kernel over the
+    per-tensor views of the logits."""
+    import torch
+
+    import paper_2608_23048_amd as roi
+    from paper_2608_23048_amd import workloads as wl
+
+    roi.lib()
+    work = wl.WORKLOADS[args.workload]
+    n, m = work.n, work.m
+    dev = torch.device("cuda:0")
+    numel = work.numel
+    print(f"# adamw mode, workload {work.name}: {numel} weights, {n}:{m}", file=sys.stderr,
+          flush=True)
+    W, L, G = wl.fill_slab(work, dev, step=0)
+    Wm = torch.empty_like(W)
+    idx = torch.empty((numel // m, n), dtype=torch.uint8, device=dev)
+    mom = torch.zeros_like(L)
+    sec = torch.zeros_like(L)
+    sched = work.tau_schedule or (work.tau, work.tau, 1)
+    T = sched[2]
+
+    def tau_at(t):
+        return roi.anneal(sched[0], sched[1], t, T)
+
+    def lr_at(t):
+        return roi.anneal(1e-3, 1e-4, t, T)
+
+    def fused_step(t, ev=None):
+        tau = tau_at(t)
+        if ev is not None:
+            ev[0].record()
+        roi.mask_fwd(W, L, n, m, tau, 1.0, 0, t, 0, out={"W_masked": Wm, "sel_idx": idx})
+        if ev is not None:
+            ev[1].record()
+        roi.mask_bwd_adamw(G, W, L, mom, sec, n, m, tau, 1.0, 0, t, 0,
+                           opt=roi.adamw_params(lr_at(t), t=t + 1))
+        if ev is not None:
+            ev[2].record()
+
+    def timed(fn, steps):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for t in range(steps):
+            fn(t, evs[t])
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        f = sum(e[0].elapsed_time(e[1]) for e in evs) / steps
+        b = sum(e[1].elapsed_time(e[2]) for e in evs) / steps
+        return el, f, b
+
+    for i in range(args.warmup):
+        fused_step(i)
+    el, f_ms, b_ms = timed(fused_step, args.steps)
+    bf, _ = algorithmic_bytes(n, m)
+    bb = 2 + 2 + 4 + 4 + 4 + 4 + 4 + 4  # G, W, logits, m, v read; logits, m, v written
+    b_gbps = bb * numel / (b_ms * 1e-3) / 1e9
+    print(f"# fused: {el * 1e3 / args.steps:.3f} ms/step, fwd {f_ms:.3f} ms, bwd+AdamW "
+          f"{b_ms:.3f} ms ({b_gbps:.0f} GB/s)", file=sys.stderr, flush=True)
+
+    # unfused: roi_mask_bwd, then PyTorch's fused AdamW over the per-tensor views
+    dphi = torch.empty_like(L)
+    views = lambda x: [x[t.offset:t.offset + t.numel].view(t.rows, t.cols) for t in work.tensors]
+    Lv, Dv, Mv, Sv = views(L), views(dphi), views(mom), views(sec)
+
+    # PyTorch's fused AdamW reads the (already incremented) step count per tensor
+    step_tensors = [[torch.full((), float(t + 1), device=dev) for _ in Lv]
+                    for t in range(max(args.steps, 1))]
+
+    def unfused_step(t, ev=None):
+        tau = tau_at(t)
+        if ev is not None:
+            ev[0].record()
+        roi.mask_fwd(W, L, n, m, tau, 1.0, 0, t, 0, out={"W_masked": Wm, "sel_idx": idx})
+        if ev is not None:
+            ev[1].record()
+        roi.mask_bwd(G, W, L, n, m, tau, 1.0, 0, t, 0, out=dphi)
+        torch._fused_adamw_(Lv, Dv, Mv, Sv, [], step_tensors[t], lr=lr_at(t), beta1=0.9,
+                            beta2=0.95,
+                            weight_decay=0.05, eps=1e-8, amsgrad=False, maximize=False)
+        if ev is not None:
+            ev[2].record()
+
+    unfused_step(0)
+    uel, uf_ms, ub_ms = timed(unfused_step, args.steps)
+    print(f"# unfused: {uel * 1e3 / args.steps:.3f} ms/step, fwd {uf_ms:.3f} ms, bwd + torch "
+          f"AdamW {ub_ms:.3f} ms", file=sys.stderr, flush=True)
+    value = numel * args.steps / el
+    out = {
+        "metric": "masked weights/sec (mask fwd + bwd with fused AdamW on the logits), "
+                  "7B-class 2:4",
+        "value": value, "unit": "masked weights/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": el * 1e3 / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (as the default mode); AdamW moments start at zero",
+        "config": {"workload": work.name, "masked_weights": numel, "pattern": f"{n}:{m}",
+                   "optimizer": "AdamW beta=(0.9, 0.95) wd=0.05 eps=1e-8, "
+                                "lr 1e-3->1e-4 exponential", "launches_per_step": 2},
+        "kernels": {"roi_mask_fwd": {"avg_ms": f_ms, "algorithmic_bytes_per_weight": bf},
+                    "roi_mask_bwd_adamw": {"avg_ms": b_ms, "algorithmic_bytes_per_weight": bb,
+                                           "GBps": b_gbps}},
+        "roofline": {"kernel": "roi_mask_bwd_adamw", "bound": "hbm", "achieved": b_gbps,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": b_gbps / HBM_PEAK_GBPS,
+                     "traffic": None},
+        "unfused": {"ms_per_step": uel * 1e3 / args.steps, "fwd_ms": uf_ms,
+                    "bwd_plus_torch_fused_adamw_ms": ub_ms,
+                    "algorithmic_bytes_per_weight": 12 + 28},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,6 +269,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="qwen2.5-7b-stack-2:4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", choices=("st", "adamw"), default="st",
+                    help="st: forward + backward (the headline); adamw: forward + backward "
+                         "with the AdamW step on the logits fused in")
     ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
                     help="only run a plain device copy of BYTES (PMC calibration)")
     ap.add_argument("--pmc-summary", nargs=5,
@@ -167,6 +288,9 @@ def main() -> int:
         print("bench.py measures one GPU only: the sampler needs no collectives, and this build "
               "runs and reports a single MI355X (pass --gpus 1).", file=sys.stderr)
         return 2
+
+    if args.mode == "adamw":
+        return run_adamw(args)
 
     import torch
 

@@ -172,6 +172,59 @@ int roi_mask_bwd_grouped(const roi_bwd_tensor* tensors, int count, int n, int m,
                          float lambda, uint64_t seed, uint64_t step, hipStream_t stream);
 
 /*
+ * roi_mask_bwd_adamw -- roi_mask_bwd with one AdamW step on the logits fused
+ * in (appendix: the logits are trained with AdamW, beta1 = 0.9, beta2 = 0.95,
+ * weight decay 0.05, a learning rate decaying from 1e-3 to 1e-4; the weights
+ * stay frozen).  With g = dL/dlogits of this step, every logit becomes
+ *   phi' = phi (1 - lr wd) - (lr / (1 - beta1^t)) m' / (sqrt(v' / (1 - beta2^t)) + eps),
+ *   m'   = beta1 m + (1 - beta1) g,   v' = beta2 v + (1 - beta2) g^2
+ * (decoupled weight decay, Loshchilov & Hutter; bias-corrected moments,
+ * Kingma & Ba), in fp32.  The keys use the logits as they were before the
+ * step.  The gradient is never stored unless grad_logits is given, so the
+ * step moves 28 bytes per weight instead of 12 (backward) + 28 (optimizer).
+ *
+ *  logits      fp32 [rows, cols]  read, then overwritten with phi'
+ *  exp_avg     fp32 [rows, cols]  m, overwritten with m'
+ *  exp_avg_sq  fp32 [rows, cols]  v, overwritten with v'
+ *  grad_logits fp32 [rows, cols]  or NULL: also written with g
+ *  opt         host struct: lr >= 0, 0 <= beta1, beta2 < 1, eps > 0,
+ *              weight_decay >= 0 (all finite), t >= 1 = this step's 1-based
+ *              optimizer step count; the caller schedules lr (e.g. with
+ *              roi_anneal).
+ *  Other arguments as in roi_mask_bwd.  The moments and grad_logits must not
+ *  overlap each other, the logits or the inputs.
+ */
+typedef struct {
+    float lr;
+    float beta1, beta2;
+    float eps;
+    float weight_decay;
+    int64_t t;
+} roi_adamw_params;
+
+int roi_mask_bwd_adamw(const uint16_t* grad_W_masked, const uint16_t* W, float* logits,
+                       float* exp_avg, float* exp_avg_sq, float* grad_logits, int64_t rows,
+                       int64_t cols, int n, int m, float tau, float lambda, uint64_t seed,
+                       uint64_t step, uint64_t elem_offset, const roi_adamw_params* opt,
+                       hipStream_t stream);
+
+/* roi_mask_bwd_adamw over `count` tensors (grouped-call conventions above). */
+typedef struct {
+    const uint16_t* grad_W_masked; /* bf16 [rows, cols] (read) */
+    const uint16_t* W;             /* bf16 [rows, cols] (read) */
+    float* logits;                 /* fp32 [rows, cols] (read, overwritten) */
+    float* exp_avg;                /* fp32 [rows, cols] (read, overwritten) */
+    float* exp_avg_sq;             /* fp32 [rows, cols] (read, overwritten) */
+    float* grad_logits;            /* fp32 [rows, cols] or NULL */
+    int64_t rows, cols;
+    uint64_t elem_offset;
+} roi_adamw_tensor;
+
+int roi_mask_bwd_adamw_grouped(const roi_adamw_tensor* tensors, int count, int n, int m,
+                               float tau, float lambda, uint64_t seed, uint64_t step,
+                               const roi_adamw_params* opt, hipStream_t stream);
+
+/*
  * roi_gumbel_noise -- the noise of `count` consecutive elements starting at
  * global index elem_offset (elem_offset % 4 == 0): the raw Philox words
  * and/or g = -L(-L(u)) (Algorithm 1).  Either output may be NULL, not both.

@@ -38,6 +38,21 @@ class FwdTensor(ctypes.Structure):
                 ("elem_offset", ctypes.c_uint64)]
 
 
+class AdamWParams(ctypes.Structure):
+    """roi_adamw_params (include/roi.h)."""
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float), ("t", ctypes.c_int64)]
+
+
+class AdamWTensor(ctypes.Structure):
+    """roi_adamw_tensor (include/roi.h)."""
+    _fields_ = [("grad_W_masked", ctypes.c_void_p), ("W", ctypes.c_void_p),
+                ("logits", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p),
+                ("exp_avg_sq", ctypes.c_void_p), ("grad_logits", ctypes.c_void_p),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("elem_offset", ctypes.c_uint64)]
+
+
 class BwdTensor(ctypes.Structure):
     """roi_bwd_tensor (include/roi.h)."""
     _fields_ = [("grad_W_masked", ctypes.c_void_p), ("W", ctypes.c_void_p),
@@ -71,6 +86,12 @@ def lib() -> ctypes.CDLL:
         for name in ("roi_mask_fwd_grouped", "roi_mask_fwd_soft_grouped", "roi_mask_bwd_grouped"):
             getattr(L, name).argtypes = grouped
             getattr(L, name).restype = _int
+        L.roi_mask_bwd_adamw.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _int, _int,
+                                         _f32, _f32, _u64, _u64, _u64, _vp, _vp]
+        L.roi_mask_bwd_adamw.restype = _int
+        L.roi_mask_bwd_adamw_grouped.argtypes = [_vp, _int, _int, _int, _f32, _f32, _u64, _u64,
+                                                 _vp, _vp]
+        L.roi_mask_bwd_adamw_grouped.restype = _int
         L.roi_gumbel_noise.argtypes = [_u64, _u64, _u64, _i64, _vp, _vp, _vp]
         L.roi_gumbel_noise.restype = _int
         L.roi_gumbel_from_words.argtypes = [_vp, _i64, _vp, _vp]
@@ -169,6 +190,61 @@ def mask_bwd(grad_W_masked, W, logits, n: int, m: int, tau: float = 1.0, lam: fl
                             seed, step, elem_offset, _ptr(d), _stream(W))
     _raise_on(st)
     return d
+
+
+def adamw_params(lr: float, betas=(0.9, 0.95), eps: float = 1e-8, weight_decay: float = 0.05,
+                 t: int = 1) -> AdamWParams:
+    """AdamW settings of one step (defaults: the appendix's betas and weight decay)."""
+    return AdamWParams(lr, betas[0], betas[1], eps, weight_decay, t)
+
+
+def mask_bwd_adamw(grad_W_masked, W, logits, exp_avg, exp_avg_sq, n: int, m: int,
+                   tau: float = 1.0, lam: float = 1.0, seed: int = 0, step: int = 0,
+                   elem_offset: int = 0, opt: AdamWParams | None = None, grad_out=None):
+    """Backward with the AdamW step on the logits fused in: logits, exp_avg and
+    exp_avg_sq (fp32, shaped like W) are updated in place; grad_out (fp32,
+    optional) also receives dL/dlogits.  Returns grad_out."""
+    import torch
+    _check_tensor(grad_W_masked, torch.bfloat16, "grad_W_masked")
+    _check_tensor(W, torch.bfloat16, "W", like=grad_W_masked)
+    for t, name in ((logits, "logits"), (exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq")):
+        _check_tensor(t, torch.float32, name, like=grad_W_masked)
+    if grad_out is not None:
+        _check_tensor(grad_out, torch.float32, "grad_out", like=grad_W_masked)
+    if opt is None:
+        raise ValueError("opt (AdamWParams) is required")
+    rows, cols = _shape2d(W)
+    st = lib().roi_mask_bwd_adamw(_ptr(grad_W_masked), _ptr(W), _ptr(logits), _ptr(exp_avg),
+                                  _ptr(exp_avg_sq), _ptr(grad_out), rows, cols, n, m, tau, lam,
+                                  seed, step, elem_offset, ctypes.addressof(opt), _stream(W))
+    _raise_on(st)
+    return grad_out
+
+
+def mask_bwd_adamw_grouped(tensors, n: int, m: int, tau: float = 1.0, lam: float = 1.0,
+                           seed: int = 0, step: int = 0, offsets=None,
+                           opt: AdamWParams | None = None, grad_outs=None):
+    """mask_bwd_adamw over a list of (grad_W_masked, W, logits, exp_avg,
+    exp_avg_sq) in one call (in place); grad_outs: optional list of fp32
+    tensors receiving dL/dlogits."""
+    import torch
+    if opt is None:
+        raise ValueError("opt (AdamWParams) is required")
+    descs = []
+    offs = _offsets([W.numel() for _, W, *_ in tensors], offsets)
+    for i, ((G, W, logits, ea, eas), off) in enumerate(zip(tensors, offs)):
+        _check_tensor(G, torch.bfloat16, "grad_W_masked")
+        _check_tensor(W, torch.bfloat16, "W", like=G)
+        for t, name in ((logits, "logits"), (ea, "exp_avg"), (eas, "exp_avg_sq")):
+            _check_tensor(t, torch.float32, name, like=G)
+        d = grad_outs[i] if grad_outs is not None else None
+        rows, cols = _shape2d(W)
+        descs.append(AdamWTensor(_ptr(G), _ptr(W), _ptr(logits), _ptr(ea), _ptr(eas), _ptr(d),
+                                 rows, cols, off))
+    arr = (AdamWTensor * max(1, len(descs)))(*descs)
+    stream = _stream(tensors[0][1]) if tensors else 0
+    _raise_on(lib().roi_mask_bwd_adamw_grouped(ctypes.addressof(arr), len(descs), n, m, tau, lam,
+                                               seed, step, ctypes.addressof(opt), stream))
 
 
 def _offsets(sizes, offsets):

@@ -48,10 +48,24 @@ struct BwdPiece {
     const uint16_t* G;
     const uint16_t* W;
     const float* phi;
-    float* dphi;
+    float* dphi;   // dL/dphi (may be NULL when the optimizer step is fused)
+    float* m;      // AdamW first and second moments (fused optimizer step only);
+    float* v;      // the updated logits are written over phi
     int64_t ngroups;
     uint32_t block0, block_hi;
     uint32_t first_block, nblocks;
+};
+
+// One AdamW step folded into constants (host, fp64, rounded once):
+// phi <- phi * decay - step_size * m' / (sqrt(v') * inv_sqrt_bc2 + eps),
+// m' = beta1 m + (1 - beta1) g, v' = beta2 v + (1 - beta2) g^2.
+struct AdamStep {
+    float decay;        // 1 - lr * weight_decay
+    float beta1, beta2;
+    float one_m_beta1, one_m_beta2;
+    float step_size;    // lr / (1 - beta1^t)
+    float inv_sqrt_bc2; // 1 / sqrt(1 - beta2^t)
+    float eps;
 };
 
 struct BwdBatch {
@@ -62,7 +76,19 @@ struct BwdBatch {
     float inv_lambda;
     float tau;
     float inv_tau;
+    AdamStep adam;
 };
+
+// The fused AdamW update of one logit from its gradient g (fp32, fast
+// reciprocal and square root: the result is held to the float tolerance).
+__device__ __forceinline__ void adamw_update(const AdamStep& a, float g, float& phi, float& m,
+                                             float& v)
+{
+    m = __builtin_fmaf(a.beta1, m, a.one_m_beta1 * g);
+    v = __builtin_fmaf(a.beta2, v, a.one_m_beta2 * (g * g));
+    const float den = __builtin_fmaf(__builtin_amdgcn_sqrtf(v), a.inv_sqrt_bc2, a.eps);
+    phi = __builtin_fmaf(-a.step_size * m, __builtin_amdgcn_rcpf(den), phi * a.decay);
+}
 
 // The piece that owns this block (the table is in the kernel arguments; the
 // scan is uniform over the block).
@@ -138,12 +164,24 @@ __device__ __forceinline__ void load_bf16(const uint16_t* p, uint32_t (&w)[M])
     }
 }
 
+// m fp32 values of a group, stored as m/4 16-byte vectors.
+template <int M>
+__device__ __forceinline__ void store_f32(float* p, const float (&x)[M])
+{
+    f32x4* p4 = reinterpret_cast<f32x4*>(p);
+#pragma unroll
+    for (int t = 0; t < M / 4; ++t) {
+        const f32x4 v = {x[4 * t], x[4 * t + 1], x[4 * t + 2], x[4 * t + 3]};
+        stream_store(v, p4 + t);
+    }
+}
+
 using FwdFn = void (*)(FwdBatch);
 using BwdFn = void (*)(BwdBatch);
 
 // Kernels for m = 16 and 32 (wide.hip): four consecutive elements per lane,
 // a group spread over m / 4 adjacent lanes.
 FwdFn select_wide_fwd(int m, int n);
-BwdFn select_wide_bwd(int m, int n);
+BwdFn select_wide_bwd(int m, int n, bool adam);
 
 } // namespace roi

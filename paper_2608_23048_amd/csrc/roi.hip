@@ -251,7 +251,10 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
     }
 }
 
-template <int M, int N, bool kLambdaOne>
+// Backward; with kAdam the AdamW step on the logits is fused in: the moments
+// are read with the group's other inputs, and the updated logits and moments
+// are written instead of (or besides, when pc.dphi is set) the gradient.
+template <int M, int N, bool kLambdaOne, bool kAdam>
 __global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
 {
     const BwdPiece& pc = a.p[find_piece(a)];
@@ -264,6 +267,7 @@ __global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
          base += (int64_t)pc.nblocks * chunk) {
         float phi[U][M];
         uint32_t w[U][M], g[U][M];
+        float mom[kAdam ? U : 1][kAdam ? M : 1], sec[kAdam ? U : 1][kAdam ? M : 1];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kLaneBlock + threadIdx.x;
@@ -271,6 +275,10 @@ __global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
                 load_logits<M>(pc.phi + q * M, phi[u]);
                 load_bf16<M>(pc.W + q * M, w[u]);
                 load_bf16<M>(pc.G + q * M, g[u]);
+                if constexpr (kAdam) {
+                    load_logits<M>(pc.m + q * M, mom[u]);
+                    load_logits<M>(pc.v + q * M, sec[u]);
+                }
             }
         }
 #pragma unroll
@@ -292,15 +300,17 @@ __global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
             relax_forward<M, N, false, true>(kappa, a.inv_tau, a.inv_tau, S_unused, rec);
             float abar[M];
             relax_backward<M, N>(rec, sbar, a.tau, a.inv_tau, abar);
-            f32x4* d4 = reinterpret_cast<f32x4*>(pc.dphi + q * M);
+            float grad[M]; // dL/dphi = dL/dkappa / lambda
 #pragma unroll
-            for (int t = 0; t < M / 4; ++t) {
-                f32x4 v;
-                v.x = kLambdaOne ? abar[4 * t + 0] : abar[4 * t + 0] * a.inv_lambda;
-                v.y = kLambdaOne ? abar[4 * t + 1] : abar[4 * t + 1] * a.inv_lambda;
-                v.z = kLambdaOne ? abar[4 * t + 2] : abar[4 * t + 2] * a.inv_lambda;
-                v.w = kLambdaOne ? abar[4 * t + 3] : abar[4 * t + 3] * a.inv_lambda;
-                stream_store(v, d4 + t);
+            for (int j = 0; j < M; ++j) grad[j] = kLambdaOne ? abar[j] : abar[j] * a.inv_lambda;
+            if (!kAdam || pc.dphi) store_f32<M>(pc.dphi + q * M, grad);
+            if constexpr (kAdam) {
+#pragma unroll
+                for (int j = 0; j < M; ++j)
+                    adamw_update(a.adam, grad[j], phi[u][j], mom[u][j], sec[u][j]);
+                store_f32<M>(const_cast<float*>(pc.phi) + q * M, phi[u]);
+                store_f32<M>(pc.m + q * M, mom[u]);
+                store_f32<M>(pc.v + q * M, sec[u]);
             }
         }
     }
@@ -480,9 +490,10 @@ FwdFn pick_fwd(bool want_s, bool want_idx, bool lam1)
 }
 
 template <int M, int N>
-BwdFn pick_bwd(bool lam1)
+BwdFn pick_bwd(bool lam1, bool adam)
 {
-    return lam1 ? bwd_lane_kernel<M, N, true> : bwd_lane_kernel<M, N, false>;
+    if (adam) return lam1 ? bwd_lane_kernel<M, N, true, true> : bwd_lane_kernel<M, N, false, true>;
+    return lam1 ? bwd_lane_kernel<M, N, true, false> : bwd_lane_kernel<M, N, false, false>;
 }
 
 template <int M, int... Ns>
@@ -494,10 +505,10 @@ FwdFn fwd_for_n(int n, bool s, bool i, bool l, std::integer_sequence<int, Ns...>
 }
 
 template <int M, int... Ns>
-BwdFn bwd_for_n(int n, bool l, std::integer_sequence<int, Ns...>)
+BwdFn bwd_for_n(int n, bool l, bool adam, std::integer_sequence<int, Ns...>)
 {
     BwdFn f = nullptr;
-    ((n == Ns + 1 ? (f = pick_bwd<M, Ns + 1>(l), 0) : 0), ...);
+    ((n == Ns + 1 ? (f = pick_bwd<M, Ns + 1>(l, adam), 0) : 0), ...);
     return f;
 }
 
@@ -508,11 +519,11 @@ FwdFn select_fwd(int m, int n, bool s, bool i, bool l)
     return select_wide_fwd(m, n);
 }
 
-BwdFn select_bwd(int m, int n, bool l)
+BwdFn select_bwd(int m, int n, bool l, bool adam)
 {
-    if (m == 4) return bwd_for_n<4>(n, l, std::make_integer_sequence<int, 4>{});
-    if (m == 8) return bwd_for_n<8>(n, l, std::make_integer_sequence<int, 8>{});
-    return select_wide_bwd(m, n);
+    if (m == 4) return bwd_for_n<4>(n, l, adam, std::make_integer_sequence<int, 4>{});
+    if (m == 8) return bwd_for_n<8>(n, l, adam, std::make_integer_sequence<int, 8>{});
+    return select_wide_bwd(m, n, adam);
 }
 
 } // namespace
@@ -615,12 +626,18 @@ int check_common(int n, int m, float tau, float lambda)
     return ROI_OK;
 }
 
+int check_count(const void* t, int count)
+{
+    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
+    if (count > 0 && !t) return fail(ROI_E_INVAL, "tensors must not be NULL");
+    return ROI_OK;
+}
+
 int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count, int n, int m,
                  float tau, float lambda, uint64_t seed, uint64_t step, hipStream_t stream)
 {
     if (int st = check_common(n, m, tau, lambda)) return st;
-    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
-    if (count > 0 && !t) return fail(ROI_E_INVAL, "tensors must not be NULL");
+    if (int st = check_count(t, count)) return st;
     std::vector<Range> ranges;
     int with_s = -1, with_idx = -1; // -1: no nonempty tensor seen yet
     for (int i = 0; i < count; ++i) {
@@ -684,35 +701,85 @@ int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count
     return L.flush();
 }
 
-int mask_bwd_run(const roi_bwd_tensor* t, int count, int n, int m, float tau, float lambda,
-                 uint64_t seed, uint64_t step, hipStream_t stream)
+// One tensor of a backward call; phi is overwritten with the updated logits
+// when the AdamW step is fused (m and v set).
+struct BwdDesc {
+    const uint16_t* G;
+    const uint16_t* W;
+    const float* phi;
+    float* dphi;
+    float* m;
+    float* v;
+    int64_t rows, cols;
+    uint64_t off;
+};
+
+int check_adamw(const roi_adamw_params* o, AdamStep* st)
+{
+    if (!o) return fail(ROI_E_INVAL, "the AdamW parameters must not be NULL");
+    if (!(o->lr >= 0.0f) || !std::isfinite(o->lr))
+        return fail(ROI_E_INVAL, "AdamW lr must be finite and >= 0");
+    if (!(o->beta1 >= 0.0f && o->beta1 < 1.0f) || !(o->beta2 >= 0.0f && o->beta2 < 1.0f))
+        return fail(ROI_E_INVAL, "AdamW betas must lie in [0, 1)");
+    if (!(o->eps > 0.0f) || !std::isfinite(o->eps))
+        return fail(ROI_E_INVAL, "AdamW eps must be finite and > 0");
+    if (!(o->weight_decay >= 0.0f) || !std::isfinite(o->weight_decay))
+        return fail(ROI_E_INVAL, "AdamW weight_decay must be finite and >= 0");
+    if (o->t < 1) return fail(ROI_E_INVAL, "AdamW step count t must be >= 1");
+    const double lr = o->lr, b1 = o->beta1, b2 = o->beta2;
+    const double bc1 = 1.0 - std::pow(b1, (double)o->t);
+    const double bc2 = 1.0 - std::pow(b2, (double)o->t);
+    st->decay = (float)(1.0 - lr * (double)o->weight_decay);
+    st->beta1 = o->beta1;
+    st->beta2 = o->beta2;
+    st->one_m_beta1 = (float)(1.0 - b1);
+    st->one_m_beta2 = (float)(1.0 - b2);
+    st->step_size = (float)(lr / bc1);
+    st->inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+    st->eps = o->eps;
+    return ROI_OK;
+}
+
+int mask_bwd_core(const char* what, const BwdDesc* t, int count, int n, int m, float tau,
+                  float lambda, uint64_t seed, uint64_t step, const roi_adamw_params* opt,
+                  hipStream_t stream)
 {
     if (int st = check_common(n, m, tau, lambda)) return st;
-    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
-    if (count > 0 && !t) return fail(ROI_E_INVAL, "tensors must not be NULL");
+    const bool adam = opt != nullptr;
+    AdamStep astep{};
+    if (adam)
+        if (int st = check_adamw(opt, &astep)) return st;
     std::vector<Range> ranges;
     bool any = false;
     for (int i = 0; i < count; ++i) {
         Shape sh;
-        if (int st = check_shape(t[i].rows, t[i].cols, n, m, tau, lambda, t[i].elem_offset, &sh))
+        if (int st = check_shape(t[i].rows, t[i].cols, n, m, tau, lambda, t[i].off, &sh))
             return count > 1 ? fail(st, "tensor %d: %s", i, g_last_error.c_str()) : st;
         if (sh.numel == 0) continue;
-        if (!t[i].grad_W_masked || !t[i].W || !t[i].logits || !t[i].grad_logits)
-            return fail(ROI_E_INVAL,
-                        "tensor %d: grad_W_masked, W, logits and grad_logits must not be NULL", i);
-        if (!aligned16(t[i].grad_W_masked) || !aligned16(t[i].W) || !aligned16(t[i].logits) ||
-            !aligned16(t[i].grad_logits))
+        if (!t[i].G || !t[i].W || !t[i].phi || (!adam && !t[i].dphi) ||
+            (adam && (!t[i].m || !t[i].v)))
+            return fail(ROI_E_INVAL, adam ? "tensor %d: grad_W_masked, W, logits, exp_avg and "
+                                            "exp_avg_sq must not be NULL"
+                                          : "tensor %d: grad_W_masked, W, logits and grad_logits "
+                                            "must not be NULL", i);
+        if (!aligned16(t[i].G) || !aligned16(t[i].W) || !aligned16(t[i].phi) ||
+            (t[i].dphi && !aligned16(t[i].dphi)) || (t[i].m && !aligned16(t[i].m)) ||
+            (t[i].v && !aligned16(t[i].v)))
             return fail(ROI_E_INVAL, "tensor %d: device pointers must be 16-byte aligned", i);
         const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
-        add_range(ranges, t[i].grad_W_masked, nb2, false);
+        add_range(ranges, t[i].G, nb2, false);
         add_range(ranges, t[i].W, nb2, false);
-        add_range(ranges, t[i].logits, nb4, false);
-        add_range(ranges, t[i].grad_logits, nb4, true);
+        add_range(ranges, t[i].phi, nb4, adam); // updated in place by the AdamW step
+        add_range(ranges, t[i].dphi, nb4, true);
+        if (adam) {
+            add_range(ranges, t[i].m, nb4, true);
+            add_range(ranges, t[i].v, nb4, true);
+        }
         any = true;
     }
     if (!any) return ok();
     if (int st = check_overlaps(ranges)) return st;
-    BwdFn fn = select_bwd(m, n, lambda == 1.0f);
+    BwdFn fn = select_bwd(m, n, lambda == 1.0f, adam);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     Launcher<BwdBatch, BwdPiece, BwdFn> L{};
     L.fn = fn;
@@ -720,22 +787,25 @@ int mask_bwd_run(const roi_bwd_tensor* t, int count, int n, int m, float tau, fl
     L.m = m;
     L.fwd = false;
     L.stream = stream;
-    L.what = "roi_mask_bwd";
+    L.what = what;
     L.batch.key_base = make_key(seed, step, 0);
     L.batch.key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
     L.batch.inv_lambda = (float)(1.0 / (double)lambda);
     L.batch.tau = tau;
     L.batch.inv_tau = (float)(1.0 / (double)tau);
+    L.batch.adam = astep;
     for (int i = 0; i < count; ++i) {
         const int64_t ngroups = t[i].rows * t[i].cols / m;
         if (ngroups == 0) continue;
-        const int st = for_each_piece(t[i].elem_offset, ngroups, m,
+        const int st = for_each_piece(t[i].off, ngroups, m,
                                       [&](int64_t g0, int64_t ng, uint64_t e0) {
             BwdPiece pc{};
-            pc.G = t[i].grad_W_masked + g0 * m;
+            pc.G = t[i].G + g0 * m;
             pc.W = t[i].W + g0 * m;
-            pc.phi = t[i].logits + g0 * m;
-            pc.dphi = t[i].grad_logits + g0 * m;
+            pc.phi = t[i].phi + g0 * m;
+            pc.dphi = t[i].dphi ? t[i].dphi + g0 * m : nullptr;
+            pc.m = adam ? t[i].m + g0 * m : nullptr;
+            pc.v = adam ? t[i].v + g0 * m : nullptr;
             pc.ngroups = ng;
             pc.block0 = (uint32_t)(e0 / 4);
             pc.block_hi = (uint32_t)((e0 / 4) >> 32);
@@ -745,6 +815,7 @@ int mask_bwd_run(const roi_bwd_tensor* t, int count, int n, int m, float tau, fl
     }
     return L.flush();
 }
+
 } // namespace
 } // namespace roi
 
@@ -788,15 +859,53 @@ extern "C" int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, co
                             uint64_t seed, uint64_t step, uint64_t elem_offset, float* grad_logits,
                             hipStream_t stream)
 {
-    const roi_bwd_tensor t = {grad_W_masked, W, logits, grad_logits, rows, cols, elem_offset};
-    return mask_bwd_run(&t, 1, n, m, tau, lambda, seed, step, stream);
+    const BwdDesc t = {grad_W_masked, W, logits, grad_logits, nullptr, nullptr,
+                       rows, cols, elem_offset};
+    return mask_bwd_core("roi_mask_bwd", &t, 1, n, m, tau, lambda, seed, step, nullptr, stream);
 }
 
 extern "C" int roi_mask_bwd_grouped(const roi_bwd_tensor* tensors, int count, int n, int m,
                                     float tau, float lambda, uint64_t seed, uint64_t step,
                                     hipStream_t stream)
 {
-    return mask_bwd_run(tensors, count, n, m, tau, lambda, seed, step, stream);
+    if (int st = check_count(tensors, count)) return st;
+    std::vector<BwdDesc> d((size_t)count);
+    for (int i = 0; i < count; ++i)
+        d[i] = {tensors[i].grad_W_masked, tensors[i].W, tensors[i].logits,
+                tensors[i].grad_logits, nullptr, nullptr, tensors[i].rows, tensors[i].cols,
+                tensors[i].elem_offset};
+    return mask_bwd_core("roi_mask_bwd_grouped", d.data(), count, n, m, tau, lambda, seed, step,
+                         nullptr, stream);
+}
+
+extern "C" int roi_mask_bwd_adamw(const uint16_t* grad_W_masked, const uint16_t* W,
+                                  float* logits, float* exp_avg, float* exp_avg_sq,
+                                  float* grad_logits, int64_t rows, int64_t cols, int n, int m,
+                                  float tau, float lambda, uint64_t seed, uint64_t step,
+                                  uint64_t elem_offset, const roi_adamw_params* opt,
+                                  hipStream_t stream)
+{
+    const BwdDesc t = {grad_W_masked, W, logits, grad_logits, exp_avg, exp_avg_sq,
+                       rows, cols, elem_offset};
+    if (!opt) return fail(ROI_E_INVAL, "the AdamW parameters must not be NULL");
+    return mask_bwd_core("roi_mask_bwd_adamw", &t, 1, n, m, tau, lambda, seed, step, opt,
+                         stream);
+}
+
+extern "C" int roi_mask_bwd_adamw_grouped(const roi_adamw_tensor* tensors, int count, int n,
+                                          int m, float tau, float lambda, uint64_t seed,
+                                          uint64_t step, const roi_adamw_params* opt,
+                                          hipStream_t stream)
+{
+    if (int st = check_count(tensors, count)) return st;
+    if (!opt) return fail(ROI_E_INVAL, "the AdamW parameters must not be NULL");
+    std::vector<BwdDesc> d((size_t)count);
+    for (int i = 0; i < count; ++i)
+        d[i] = {tensors[i].grad_W_masked, tensors[i].W, tensors[i].logits,
+                tensors[i].grad_logits, tensors[i].exp_avg, tensors[i].exp_avg_sq,
+                tensors[i].rows, tensors[i].cols, tensors[i].elem_offset};
+    return mask_bwd_core("roi_mask_bwd_adamw_grouped", d.data(), count, n, m, tau, lambda, seed,
+                         step, opt, stream);
 }
 
 extern "C" int roi_gumbel_noise(uint64_t seed, uint64_t step, uint64_t elem_offset, int64_t count,

@@ -257,7 +257,9 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
     }
 }
 
-template <int M, int N>
+// Backward; with kAdam the AdamW step on the logits is fused in (as in the
+// per-lane kernels).
+template <int M, int N, bool kAdam>
 __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
 {
     constexpr int L = M / 4;
@@ -271,7 +273,12 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
         const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
         const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
         const u32x2 gv = stream_load(reinterpret_cast<const u32x2*>(pc.G + slot * 4));
-        const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
+        f32x4 mv, vv;
+        if constexpr (kAdam) {
+            mv = stream_load(reinterpret_cast<const f32x4*>(pc.m + slot * 4));
+            vv = stream_load(reinterpret_cast<const f32x4*>(pc.v + slot * 4));
+        }
+        float phi[4] = {pv.x, pv.y, pv.z, pv.w};
         // keys from the hardware logarithm, in log2 units (noise.hpp)
         const uint4 x = philox_block(pc.block0 + (uint32_t)slot, key);
         const float kappa[4] = {fast_key_log2(phi[0], a.key_c, x.x),
@@ -290,9 +297,17 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
         float abar[4];
         wide_relax_backward<L, N>(rec, sbar, a.tau, a.inv_tau, abar);
         // dL/dphi = dL/dkappa / lambda (the product is exact for lambda = 1)
-        const f32x4 dv = {abar[0] * a.inv_lambda, abar[1] * a.inv_lambda,
-                          abar[2] * a.inv_lambda, abar[3] * a.inv_lambda};
-        stream_store(dv, reinterpret_cast<f32x4*>(pc.dphi + slot * 4));
+        const float grad[4] = {abar[0] * a.inv_lambda, abar[1] * a.inv_lambda,
+                               abar[2] * a.inv_lambda, abar[3] * a.inv_lambda};
+        if (!kAdam || pc.dphi) store_f32<4>(pc.dphi + slot * 4, grad);
+        if constexpr (kAdam) {
+            float mo[4] = {mv.x, mv.y, mv.z, mv.w}, se[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) adamw_update(a.adam, grad[e], phi[e], mo[e], se[e]);
+            store_f32<4>(const_cast<float*>(pc.phi) + slot * 4, phi);
+            store_f32<4>(pc.m + slot * 4, mo);
+            store_f32<4>(pc.v + slot * 4, se);
+        }
     }
 }
 
@@ -305,10 +320,13 @@ FwdFn wide_fwd_for_n(int n, std::integer_sequence<int, Ns...>)
 }
 
 template <int M, int... Ns>
-BwdFn wide_bwd_for_n(int n, std::integer_sequence<int, Ns...>)
+BwdFn wide_bwd_for_n(int n, bool adam, std::integer_sequence<int, Ns...>)
 {
     BwdFn f = nullptr;
-    ((n == Ns + 1 ? (f = bwd_wide_kernel<M, Ns + 1>, 0) : 0), ...);
+    ((n == Ns + 1 ? (f = adam ? bwd_wide_kernel<M, Ns + 1, true> : bwd_wide_kernel<M, Ns + 1, false>,
+                     0)
+                  : 0),
+     ...);
     return f;
 }
 
@@ -321,10 +339,10 @@ FwdFn select_wide_fwd(int m, int n)
     return nullptr;
 }
 
-BwdFn select_wide_bwd(int m, int n)
+BwdFn select_wide_bwd(int m, int n, bool adam)
 {
-    if (m == 16) return wide_bwd_for_n<16>(n, std::make_integer_sequence<int, 16>{});
-    if (m == 32) return wide_bwd_for_n<32>(n, std::make_integer_sequence<int, 32>{});
+    if (m == 16) return wide_bwd_for_n<16>(n, adam, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_bwd_for_n<32>(n, adam, std::make_integer_sequence<int, 32>{});
     return nullptr;
 }
 

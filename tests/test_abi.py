@@ -33,6 +33,7 @@ def test_exports_every_declared_symbol(L):
     assert {"roi_mask_fwd", "roi_mask_fwd_soft", "roi_mask_bwd", "roi_gumbel_noise",
             "roi_gumbel_from_words", "roi_fast_noise_from_words",
             "roi_mask_fwd_grouped", "roi_mask_fwd_soft_grouped", "roi_mask_bwd_grouped",
+            "roi_mask_bwd_adamw", "roi_mask_bwd_adamw_grouped",
             "roi_anneal", "roi_status_string", "roi_last_error", "roi_abi_version"} <= set(names)
     for name in names:
         assert hasattr(L, name), name
@@ -188,6 +189,70 @@ def test_bwd_grouped_rejects_before_launch(L):
     assert grouped(L, "roi_mask_bwd_grouped", cases[-1][0], m=64, n=2) == roi.ROI_E_UNSUPPORTED
     assert L.roi_mask_bwd_grouped(None, 0, 2, 4, 1.0, 1.0, 0, 0, None) == roi.ROI_OK
     assert L.roi_mask_bwd_grouped(None, 3, 2, 4, 1.0, 1.0, 0, 0, None) == roi.ROI_E_INVAL
+
+
+def adamw(L, opt, **kw):
+    a = dict(G=FAKE, W=FAKE + GB, logits=FAKE + 2 * GB, ea=FAKE + 3 * GB, eas=FAKE + 4 * GB,
+             d=None, rows=4, cols=8, n=2, m=4, tau=1.0, lam=1.0, off=0)
+    a.update(kw)
+    return L.roi_mask_bwd_adamw(a["G"], a["W"], a["logits"], a["ea"], a["eas"], a["d"],
+                                a["rows"], a["cols"], a["n"], a["m"], a["tau"], a["lam"], 0, 0,
+                                a["off"], None if opt is None else ctypes.addressof(opt), None)
+
+
+@pytest.mark.parametrize("okw,kw,status", [
+    (None, {}, roi.ROI_E_INVAL),                               # no parameters
+    (dict(lr=-1e-3), {}, roi.ROI_E_INVAL),
+    (dict(lr=math.nan), {}, roi.ROI_E_INVAL),
+    (dict(lr=math.inf), {}, roi.ROI_E_INVAL),
+    (dict(betas=(1.0, 0.95)), {}, roi.ROI_E_INVAL),
+    (dict(betas=(0.9, -0.1)), {}, roi.ROI_E_INVAL),
+    (dict(eps=0.0), {}, roi.ROI_E_INVAL),
+    (dict(weight_decay=-0.05), {}, roi.ROI_E_INVAL),
+    (dict(t=0), {}, roi.ROI_E_INVAL),
+    ({}, dict(ea=None), roi.ROI_E_INVAL),
+    ({}, dict(eas=None), roi.ROI_E_INVAL),
+    ({}, dict(logits=None), roi.ROI_E_INVAL),
+    ({}, dict(ea=FAKE + 3 * GB + 4), roi.ROI_E_INVAL),         # misaligned
+    ({}, dict(ea=FAKE + 2 * GB + 16), roi.ROI_E_INVAL),        # moments overlap the logits
+    ({}, dict(d=FAKE + 4 * GB), roi.ROI_E_INVAL),              # gradient over the second moment
+    ({}, dict(W=FAKE + 2 * GB + 32), roi.ROI_E_INVAL),         # input inside the updated logits
+    ({}, dict(cols=6), roi.ROI_E_INVAL),
+    ({}, dict(m=64, n=2, cols=64), roi.ROI_E_UNSUPPORTED),
+])
+def test_bwd_adamw_rejects_before_launch(L, okw, kw, status):
+    opt = None if okw is None else roi.adamw_params(**{"lr": 1e-3, **okw})
+    assert adamw(L, opt, **kw) == status
+    assert L.roi_last_error()
+
+
+def test_bwd_adamw_grouped_rejects_before_launch(L):
+    opt = roi.adamw_params(1e-3)
+    bad = roi.adamw_params(1e-3, t=0)
+
+    def desc(i, **kw):
+        base = FAKE + i * 8 * GB
+        a = dict(G=base, W=base + GB, logits=base + 2 * GB, ea=base + 3 * GB, eas=base + 4 * GB,
+                 d=None, rows=4, cols=8, off=i * 32)
+        a.update(kw)
+        return roi.AdamWTensor(a["G"], a["W"], a["logits"], a["ea"], a["eas"], a["d"], a["rows"],
+                               a["cols"], a["off"])
+
+    def call(descs, o):
+        arr = (roi.AdamWTensor * max(1, len(descs)))(*descs)
+        return L.roi_mask_bwd_adamw_grouped(ctypes.addressof(arr), len(descs), 2, 4, 1.0, 1.0, 0,
+                                            0, None if o is None else ctypes.addressof(o), None)
+
+    assert call([desc(0), desc(1)], None) == roi.ROI_E_INVAL
+    assert call([desc(0), desc(1)], bad) == roi.ROI_E_INVAL
+    assert call([desc(0), desc(1, eas=None)], opt) == roi.ROI_E_INVAL
+    assert "tensor 1" in L.roi_last_error().decode()
+    assert call([desc(0), desc(1, ea=FAKE + 3 * GB)], opt) == roi.ROI_E_INVAL  # shared moment
+    assert "overlap" in L.roi_last_error().decode()
+    assert L.roi_mask_bwd_adamw_grouped(None, 0, 2, 4, 1.0, 1.0, 0, 0, ctypes.addressof(opt),
+                                        None) == roi.ROI_OK
+    assert L.roi_mask_bwd_adamw_grouped(None, -1, 2, 4, 1.0, 1.0, 0, 0, ctypes.addressof(opt),
+                                        None) == roi.ROI_E_INVAL
 
 
 def test_empty_input_is_a_no_op(L):

@@ -352,6 +352,124 @@ def test_grouped_against_oracle(dev):
         assert_close(f32(d), d_o, "grad_logits (grouped)")
 
 
+# --------------------------------------------------------------------------- fused AdamW
+ADAMW = [(37, 36, 2, 4, 1.0, 1.0, 1, 1e-3), (64, 96, 2, 4, 0.1, 1.0, 7, 4e-4),
+         (33, 64, 3, 4, 0.7, 0.6, 3, 1e-3), (61, 88, 4, 8, 0.5, 1.0, 2, 1e-3),
+         (37, 48, 8, 16, 1.0, 1.0, 1, 1e-3), (13, 64, 5, 32, 0.3, 0.8, 12, 2e-4)]
+
+
+def adamw_state(rows, cols, seed):
+    rng = np.random.default_rng(seed)
+    m = rng.normal(0.0, 2e-5, (rows, cols)).astype(np.float32)
+    v = (rng.random((rows, cols)) * 1e-9).astype(np.float32)
+    return m, v
+
+
+@pytest.mark.parametrize("case", ADAMW, ids=lambda c: "x".join(map(str, c[:4])) + f"-t{c[6]}")
+def test_bwd_adamw_against_oracle(dev, case):
+    """The fused backward + AdamW step against the oracle's backward followed by
+    its AdamW step; the gradient it also writes equals roi_mask_bwd's bit for
+    bit."""
+    import torch
+    rows, cols, n, m, tau, lam, t, lr = case
+    seed, step, off = 17, 3, 64
+    say(f"bwd+adamw {rows}x{cols} {n}:{m} tau={tau} lam={lam} t={t} lr={lr}")
+    W, L, G = wl.small_case(rows, cols, rows + cols, device=dev)
+    m0, v0 = adamw_state(rows, cols, t)
+    opt = roi.adamw_params(lr, t=t)
+    Lg, mg, vg = L.clone(), torch.from_numpy(m0).to(dev), torch.from_numpy(v0).to(dev)
+    d = torch.empty_like(L)
+    roi.mask_bwd_adamw(G, W, Lg, mg, vg, n, m, tau, lam, seed, step, off, opt=opt, grad_out=d)
+    d_ref = roi.mask_bwd(G, W, L, n, m, tau, lam, seed, step, off)
+    torch.cuda.synchronize()
+    assert torch.equal(d.view(torch.int32), d_ref.view(torch.int32))
+    tau32, lam32 = float(np.float32(tau)), float(np.float32(lam))
+    d_o = oracle.mask_bwd(bf16_bits(G), bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
+    p_o, m_o, v_o = oracle.adamw(d_o, f32(L), m0, v0, float(np.float32(lr)), float(np.float32(0.9)),
+                                 float(np.float32(0.95)), float(np.float32(1e-8)),
+                                 float(np.float32(0.05)), t)
+    assert_close(f32(d), d_o, "grad_logits (fused)")
+    assert_close(f32(mg), m_o, "exp_avg")
+    assert_close(f32(vg), v_o, "exp_avg_sq")
+    assert_close(f32(Lg), p_o, "logits after AdamW")
+    # The update term itself (beyond the decay) against the oracle's.  Its
+    # allowance: the worst change of the oracle's update when the gradient
+    # moves within the gradient's own tolerance, plus 1% for the fp32 step and
+    # one ulp of the stored logit.  A wrong step formula (a missing bias
+    # correction, swapped betas) moves the update by tens of percent.
+    hp = [float(np.float32(x)) for x in (lr, 0.9, 0.95, 1e-8, 0.05)]
+    decayed = f32(L).astype(np.float64).reshape(-1) * (1.0 - hp[0] * hp[4])
+    got_upd = f32(Lg).astype(np.float64).reshape(-1) - decayed
+    ref_upd = p_o.reshape(-1) - decayed
+    tol_g = 1e-6 + 1e-5 * np.abs(d_o)
+    spread = np.zeros_like(ref_upd)
+    for sign in (-1.0, 1.0):
+        p_s, _, _ = oracle.adamw(d_o + sign * tol_g, f32(L), m0, v0, *hp, t)
+        spread = np.maximum(spread, np.abs(p_s.reshape(-1) - decayed - ref_upd))
+    ulp = np.spacing(np.abs(f32(Lg).reshape(-1))).astype(np.float64)
+    bad = np.abs(got_upd - ref_upd) > spread + 1e-2 * np.abs(ref_upd) + ulp
+    assert not bad.any(), f"{int(bad.sum())} update terms off"
+    # and the allowance is tight enough to see a missing bias correction
+    p_nb, _, _ = oracle.adamw(d_o, f32(L), m0, v0, *hp, 1)
+    wrong = np.abs(p_nb.reshape(-1) - decayed - ref_upd) > spread + 1e-2 * np.abs(ref_upd) + ulp
+    assert t == 1 or wrong.mean() > 0.5
+
+
+def test_bwd_adamw_three_steps(dev):
+    """Three training steps (forward, fused backward + AdamW) with the
+    temperatures and the learning rate annealed: the GPU state against the
+    oracle carrying its own state, rounded to fp32 after each step."""
+    import torch
+    rows, cols, n, m = 96, 128, 2, 4
+    W, L, _ = wl.small_case(rows, cols, 5, device=dev)
+    Lg = L.clone()
+    mg = torch.zeros_like(L)
+    vg = torch.zeros_like(L)
+    p_o = f32(L)
+    m_o = np.zeros_like(p_o)
+    v_o = np.zeros_like(p_o)
+    gen = torch.Generator(device="cpu").manual_seed(8)
+    for t in range(1, 4):
+        tau = roi.anneal(1.0, 0.05, t - 1, 3)
+        lam = roi.anneal(1.0, 0.5, t - 1, 3)
+        lr = roi.anneal(1e-3, 1e-4, t - 1, 3)
+        say(f"adamw chain t={t} tau={tau:.4f} lam={lam:.4f} lr={lr:.2e}")
+        G = (torch.randn(rows, cols, generator=gen) * 1e-3).to(torch.bfloat16).to(dev)
+        roi.mask_bwd_adamw(G, W, Lg, mg, vg, n, m, tau, lam, 0, t, 0,
+                           opt=roi.adamw_params(lr, t=t))
+        torch.cuda.synchronize()
+        d_o = oracle.mask_bwd(bf16_bits(G), bf16_bits(W), p_o, n, m, tau, lam, 0, t, 0)
+        p64, m64, v64 = oracle.adamw(d_o, p_o, m_o, v_o, lr, float(np.float32(0.9)),
+                                     float(np.float32(0.95)), float(np.float32(1e-8)),
+                                     float(np.float32(0.05)), t)
+        assert_close(f32(Lg), p64, f"logits after step {t}")
+        assert_close(f32(mg), m64, f"exp_avg after step {t}")
+        assert_close(f32(vg), v64, f"exp_avg_sq after step {t}")
+        p_o, m_o, v_o = (x.astype(np.float32) for x in (p64, m64, v64))
+
+
+def test_bwd_adamw_grouped_equals_single(dev):
+    import torch
+    say("bwd+adamw grouped vs single")
+    tensors, offs = grouped_inputs(dev, 4, count=18, seed=21)
+    opt = roi.adamw_params(1e-3, t=4)
+    states = []
+    for W, L, G in tensors:
+        m0, v0 = adamw_state(W.shape[0], W.shape[1], W.numel())
+        states.append((torch.from_numpy(m0).to(dev), torch.from_numpy(v0).to(dev)))
+    grouped_state = [(L.clone(), mm.clone(), vv.clone()) for (_, L, _), (mm, vv) in
+                     zip(tensors, states)]
+    roi.mask_bwd_adamw_grouped([(G, W, p, mm, vv) for (W, _, G), (p, mm, vv) in
+                                zip(tensors, grouped_state)], 2, 4, 0.5, 1.0, 9, 2,
+                               offsets=offs, opt=opt)
+    for (W, L, G), off, (mm, vv), (pg, mgr, vgr) in zip(tensors, offs, states, grouped_state):
+        p1, m1, v1 = L.clone(), mm.clone(), vv.clone()
+        roi.mask_bwd_adamw(G, W, p1, m1, v1, 2, 4, 0.5, 1.0, 9, 2, off, opt=opt)
+        torch.cuda.synchronize()
+        for a, b in ((pg, p1), (mgr, m1), (vgr, v1)):
+            assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
 def test_every_output_written_and_deterministic(dev):
     import torch
     W, L, G = wl.small_case(333, 64, 1, device=dev)
