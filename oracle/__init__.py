@@ -97,6 +97,9 @@ def lib():
         L.oracle_adamw.argtypes = [_f64p, _i64, _f64, _f64, _f64, _f64, _f64, _i64, _f32p, _f32p,
                                    _f32p, _f64p, _f64p, _f64p]
         L.oracle_adamw.restype = _int
+        L.oracle_export.argtypes = [_f32p, _u16p, _i64, _int, _int, _u16p, _u16p, _u8p,
+                                    ctypes.POINTER(ctypes.c_uint32)]
+        L.oracle_export.restype = _int
         _lib = L
     return _lib
 
@@ -208,6 +211,23 @@ def adamw(grad, phi, m, v, lr: float, beta1: float, beta2: float, eps: float,
                               _ptr(vv, ctypes.c_float), _ptr(po, ctypes.c_double),
                               _ptr(mo, ctypes.c_double), _ptr(vo, ctypes.c_double)), "adamw")
     return po, mo, vo
+
+
+def export(logits, W_bits, n: int, m: int, want_meta: bool = False):
+    """Final mask: top-n of the logits per group.  Returns (W_masked bits,
+    values bits [G, n], idx [G, n] ascending, meta uint32 [ceil(G/8)] or None)."""
+    p = np.ascontiguousarray(logits, dtype=np.float32).reshape(-1)
+    W = np.ascontiguousarray(W_bits, dtype=np.uint16).reshape(-1)
+    assert p.size == W.size
+    G = p.size // m
+    Wm = np.empty(p.size, dtype=np.uint16)
+    vals = np.empty((G, n), dtype=np.uint16)
+    idx = np.empty((G, n), dtype=np.uint8)
+    meta = np.empty((G + 7) // 8, dtype=np.uint32) if want_meta else None
+    _check(lib().oracle_export(_ptr(p, ctypes.c_float), _ptr(W, ctypes.c_uint16), p.size, n, m,
+                               _ptr(Wm, ctypes.c_uint16), _ptr(vals, ctypes.c_uint16),
+                               _ptr(idx, ctypes.c_uint8), _ptr(meta, ctypes.c_uint32)), "export")
+    return Wm, vals, idx, meta
 
 
 # --------------------------------------------------------------------------- whole arrays

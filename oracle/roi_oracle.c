@@ -532,3 +532,37 @@ int oracle_adamw(const double* grad, int64_t numel, double lr, double beta1, dou
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------------- *
+ * 9. Final mask after training.  The paper anneals the sampling temperature
+ *    lambda towards 0 (§4.2.3); as lambda -> 0 the keys phi/lambda + g order
+ *    exactly as the logits do, so the sampler's limit is the n largest logits
+ *    of each group (ties to the lower index, as in the sampler).  Exported
+ *    in the compressed form of a sparse weight: per group the kept weights
+ *    and their indices in increasing index order, and for 2:4 the indices as
+ *    2-bit fields (group q occupies bits 4(q%8) .. 4(q%8)+3 of word q/8, the
+ *    lower kept index in the low two bits).
+ * ------------------------------------------------------------------------- */
+int oracle_export(const float* logits, const uint16_t* W, int64_t numel, int n, int m,
+                  uint16_t* W_masked, uint16_t* values, uint8_t* idx, uint32_t* meta)
+{
+    if (numel < 0 || m < 1 || m > ORACLE_MAX_M || n < 1 || n > m || numel % m != 0) return -1;
+    if (meta && !(n == 2 && m == 4)) return -1;
+    const int64_t groups = numel / m;
+    if (meta)
+        for (int64_t w = 0; w < (groups + 7) / 8; ++w) meta[w] = 0;
+    for (int64_t q = 0; q < groups; ++q) {
+        uint8_t order[ORACLE_MAX_M], hard[ORACLE_MAX_M];
+        oracle_topn(logits + q * m, m, n, order, hard);
+        int k = 0;
+        for (int j = 0; j < m; ++j) {
+            if (W_masked) W_masked[q * m + j] = hard[j] ? W[q * m + j] : (uint16_t)0;
+            if (!hard[j]) continue;
+            if (values) values[q * n + k] = W[q * m + j];
+            if (idx) idx[q * n + k] = (uint8_t)j;
+            if (meta) meta[q / 8] |= (uint32_t)j << (4 * (q % 8) + 2 * k);
+            ++k;
+        }
+    }
+    return 0;
+}

@@ -56,6 +56,11 @@ int roi_oracle_bwd_groups(const uint16_t* grad_W_masked, const uint16_t* W, cons
 /* Exponential annealing of a temperature. */
 double oracle_anneal(double v_init, double v_end, double t, double t_anneal);
 
+/* Final mask (top-n of the logits) in dense and compressed form; meta only
+ * for 2:4.  Any output may be NULL. */
+int oracle_export(const float* logits, const uint16_t* W, int64_t numel, int n, int m,
+                  uint16_t* W_masked, uint16_t* values, uint8_t* idx, uint32_t* meta);
+
 /* AdamW step on numel logits from an fp64 gradient (fp64 outputs). */
 int oracle_adamw(const double* grad, int64_t numel, double lr, double beta1, double beta2,
                  double eps, double weight_decay, int64_t t, const float* phi, const float* m,

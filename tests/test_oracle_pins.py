@@ -616,3 +616,49 @@ def test_adamw_closed_forms():
     np.testing.assert_array_equal(p, phi.astype(np.float64))
     with pytest.raises(ValueError):
         oracle.adamw(g, phi, z, z, lr, 0.9, 0.95, eps, wd, 0)
+
+
+# --------------------------------------------------------------------------- final-mask export
+def test_export_worked_example():
+    """Hand-computed: phi = (0.1, 0.9, 0.5, 0.2) keeps {1, 2} (nibble 1 | 2 << 2 = 9);
+    phi = (3, 3, 1, 3) ties at 3 and keeps the lower indices {0, 1} (nibble 4,
+    in bits 4..7): one metadata word 9 + 64 = 73."""
+    phi = np.array([0.1, 0.9, 0.5, 0.2, 3, 3, 1, 3], np.float32)
+    W = np.arange(1, 9, dtype=np.uint16)
+    Wm, vals, idx, meta = oracle.export(phi, W, 2, 4, want_meta=True)
+    assert Wm.tolist() == [0, 2, 3, 0, 5, 6, 0, 0]
+    assert vals.tolist() == [[2, 3], [5, 6]] and idx.tolist() == [[1, 2], [0, 1]]
+    assert meta.tolist() == [73]
+
+
+def decompress(vals, idx, m):
+    """Dense [G, m] from the compressed values and their indices."""
+    G, n = vals.shape
+    dense = np.zeros((G, m), dtype=vals.dtype)
+    np.put_along_axis(dense, idx.astype(np.int64), vals, axis=1)
+    return dense.reshape(-1)
+
+
+@pytest.mark.parametrize("n,m", [(2, 4), (1, 4), (3, 4), (4, 8), (2, 8), (8, 16), (16, 32)])
+def test_export_is_the_lambda_to_zero_limit_of_the_sampler(n, m):
+    """§4.2.3 anneals lambda towards 0.  With lambda = 2^-40 and |phi| >= 2^-10,
+    phi / lambda is exact and one ulp of it exceeds twice any |g|, so the
+    sampler's keys equal phi * 2^40 exactly: its selection (ties included) must
+    be the exported top-n of the logits, and its masked weights the exported
+    dense mask."""
+    rng = np.random.default_rng(n * 64 + m)
+    G = 4000
+    phi = rng.normal(0, 1, (G, m))
+    phi = np.sign(phi) * np.maximum(np.abs(phi), 2.0 ** -10)
+    phi[::3] = np.round(phi[::3] * 2) / 2 + 0.25  # many exact ties, all nonzero
+    phi = phi.astype(np.float32).reshape(-1)
+    W = rng.integers(1, 0x7F00, phi.size, dtype=np.uint16)
+    Wm_s, _, idx_s = oracle.mask_fwd(W, phi, n, m, 1.0, 2.0 ** -40, 7, 3, 0, want_soft=False)
+    Wm, vals, idx, meta = oracle.export(phi, W, n, m, want_meta=(n == 2 and m == 4))
+    assert np.array_equal(np.sort(idx_s, axis=1), idx)
+    assert np.array_equal(Wm_s, Wm)
+    assert np.array_equal(decompress(vals, idx, m), Wm)
+    if meta is not None:  # 2:4 metadata: two 2-bit fields per group, 8 groups per word
+        q = np.arange(G)
+        nib = (meta[q // 8] >> (4 * (q % 8))) & 0xF
+        assert np.array_equal(np.stack([nib & 3, nib >> 2], axis=1), idx)
