@@ -262,6 +262,55 @@ def run_adamw(args) -> int:
     return 0
 
 
+def run_export(args) -> int:
+    """--mode export: the final-mask export after training over the whole stack
+    (top-n of the logits; compressed bf16 values and, for 2:4, the 2-bit index
+    metadata: what a 2:4 sparse deployment loads)."""
+    import torch
+
+    import paper_2608_23048_amd as roi
+    from paper_2608_23048_amd import workloads as wl
+
+    roi.lib()
+    work = wl.WORKLOADS[args.workload]
+    n, m = work.n, work.m
+    numel = work.numel
+    W, L, G = wl.fill_slab(work, torch.device("cuda:0"))
+    del G
+    meta = n == 2 and m == 4
+    print(f"# export mode, workload {work.name}: {numel} weights, {n}:{m}", file=sys.stderr,
+          flush=True)
+    for _ in range(max(args.warmup, 1)):
+        out = roi.mask_export(L, W, n, m, want_dense=False, want_idx=False, want_meta=meta)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    keep = []
+    for e0, e1 in evs:
+        e0.record()
+        keep.append(roi.mask_export(L, W, n, m, want_dense=False, want_idx=False,
+                                    want_meta=meta))
+        e1.record()
+        keep = keep[-1:]
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+    bpw = 4 + 2 + 2 * n / m + (1.0 / 8 if meta else 0.0)
+    gbps = bpw * numel / (ms * 1e-3) / 1e9
+    print(f"# export: {ms:.3f} ms ({gbps:.0f} GB/s)", file=sys.stderr, flush=True)
+    out = {"metric": "masked weights/sec (final-mask export: compressed values + metadata)",
+           "value": numel / (ms * 1e-3), "unit": "masked weights/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic (as the default mode)",
+           "config": {"workload": work.name, "masked_weights": numel, "pattern": f"{n}:{m}",
+                      "outputs": "values bf16 [G, n]" + (" + meta uint32" if meta else "")},
+           "roofline": {"kernel": "roi_mask_export", "bound": "hbm", "achieved": gbps,
+                        "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS,
+                        "traffic": None, "algorithmic_bytes_per_weight": bpw}}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -269,9 +318,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="qwen2.5-7b-stack-2:4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("st", "adamw"), default="st",
+    ap.add_argument("--mode", choices=("st", "adamw", "export"), default="st",
                     help="st: forward + backward (the headline); adamw: forward + backward "
-                         "with the AdamW step on the logits fused in")
+                         "with the AdamW step on the logits fused in; export: the final-mask "
+                         "export after training")
     ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
                     help="only run a plain device copy of BYTES (PMC calibration)")
     ap.add_argument("--pmc-summary", nargs=5,
@@ -291,6 +341,8 @@ def main() -> int:
 
     if args.mode == "adamw":
         return run_adamw(args)
+    if args.mode == "export":
+        return run_export(args)
 
     import torch
 

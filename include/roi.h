@@ -225,6 +225,28 @@ int roi_mask_bwd_adamw_grouped(const roi_adamw_tensor* tensors, int count, int n
                                const roi_adamw_params* opt, hipStream_t stream);
 
 /*
+ * roi_mask_export -- the final mask after training, in dense and compressed
+ * form.  §4.2.3 anneals the sampling temperature lambda towards 0; the
+ * sampler's lambda -> 0 limit keeps the n largest logits of each group (ties
+ * to the lower index, as in the sampler), with no noise.  This call writes
+ * that mask:
+ *  W_masked bf16 [rows, cols] or NULL: W where kept, +0.0 elsewhere;
+ *  values   bf16 [rows*cols/m, n] or NULL: the kept weights of each group in
+ *           increasing index order (the compressed sparse weight);
+ *  idx      uint8 [rows*cols/m, n] or NULL: their indices, increasing;
+ *  meta     uint32 [ceil(rows*cols/m / 8)] or NULL, 2:4 only: group q's two
+ *           indices as 2-bit fields in bits 4(q%8) .. 4(q%8)+3 of word q/8,
+ *           the lower index in the low two bits (the index metadata that
+ *           accompanies 2:4-compressed values).
+ * At least one output must be requested.  W may be NULL when only idx and
+ * meta are.  logits, W, rows, cols, n, m as in roi_mask_fwd (no temperatures,
+ * seed or step).
+ */
+int roi_mask_export(const float* logits, const uint16_t* W, int64_t rows, int64_t cols, int n,
+                    int m, uint16_t* W_masked, uint16_t* values, uint8_t* idx, uint32_t* meta,
+                    hipStream_t stream);
+
+/*
  * roi_gumbel_noise -- the noise of `count` consecutive elements starting at
  * global index elem_offset (elem_offset % 4 == 0): the raw Philox words
  * and/or g = -L(-L(u)) (Algorithm 1).  Either output may be NULL, not both.

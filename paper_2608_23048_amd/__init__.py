@@ -92,6 +92,8 @@ def lib() -> ctypes.CDLL:
         L.roi_mask_bwd_adamw_grouped.argtypes = [_vp, _int, _int, _int, _f32, _f32, _u64, _u64,
                                                  _vp, _vp]
         L.roi_mask_bwd_adamw_grouped.restype = _int
+        L.roi_mask_export.argtypes = [_vp, _vp, _i64, _i64, _int, _int, _vp, _vp, _vp, _vp, _vp]
+        L.roi_mask_export.restype = _int
         L.roi_gumbel_noise.argtypes = [_u64, _u64, _u64, _i64, _vp, _vp, _vp]
         L.roi_gumbel_noise.restype = _int
         L.roi_gumbel_from_words.argtypes = [_vp, _i64, _vp, _vp]
@@ -245,6 +247,27 @@ def mask_bwd_adamw_grouped(tensors, n: int, m: int, tau: float = 1.0, lam: float
     stream = _stream(tensors[0][1]) if tensors else 0
     _raise_on(lib().roi_mask_bwd_adamw_grouped(ctypes.addressof(arr), len(descs), n, m, tau, lam,
                                                seed, step, ctypes.addressof(opt), stream))
+
+
+def mask_export(logits, W, n: int, m: int, want_dense: bool = True, want_values: bool = True,
+                want_idx: bool = True, want_meta: bool = False):
+    """Final mask (top-n of the logits per group): returns (W_masked, values
+    [G, n], idx [G, n] increasing, meta uint32 [ceil(G/8)] for 2:4), each
+    None unless requested."""
+    import torch
+    _check_tensor(logits, torch.float32, "logits")
+    if W is not None:
+        _check_tensor(W, torch.bfloat16, "W", like=logits)
+    rows, cols = _shape2d(logits)
+    G = logits.numel() // m if m > 0 else 0
+    dev = logits.device
+    Wm = torch.empty_like(W) if want_dense else None
+    vals = torch.empty((G, n), dtype=torch.bfloat16, device=dev) if want_values else None
+    idx = torch.empty((G, n), dtype=torch.uint8, device=dev) if want_idx else None
+    meta = torch.empty(((G + 7) // 8,), dtype=torch.int32, device=dev) if want_meta else None
+    _raise_on(lib().roi_mask_export(_ptr(logits), _ptr(W), rows, cols, n, m, _ptr(Wm), _ptr(vals),
+                                    _ptr(idx), _ptr(meta), _stream(logits)))
+    return Wm, vals, idx, meta
 
 
 def _offsets(sizes, offsets):

@@ -19,7 +19,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libroi.so")
-SOURCES = [os.path.join(CSRC, "roi.hip"), os.path.join(CSRC, "wide.hip")]
+SOURCES = [os.path.join(CSRC, "roi.hip"), os.path.join(CSRC, "wide.hip"),
+           os.path.join(CSRC, "export.hip")]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

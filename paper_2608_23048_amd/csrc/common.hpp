@@ -179,6 +179,19 @@ __device__ __forceinline__ void store_f32(float* p, const float (&x)[M])
 using FwdFn = void (*)(FwdBatch);
 using BwdFn = void (*)(BwdBatch);
 
+// Final-mask export (export.hip): top-n of the logits of each group.
+struct ExportArgs {
+    const float* phi;
+    const uint16_t* W;
+    uint16_t* Wm;   // dense masked weights or NULL
+    uint16_t* vals; // [groups, n] kept weights, increasing index, or NULL
+    uint8_t* idx;   // [groups, n] their indices, or NULL
+    uint32_t* meta; // [ceil(groups / 8)] 2:4 index fields, or NULL
+    int64_t ngroups;
+};
+using ExportFn = void (*)(ExportArgs);
+ExportFn select_export(int m, int n);
+
 // Kernels for m = 16 and 32 (wide.hip): four consecutive elements per lane,
 // a group spread over m / 4 adjacent lanes.
 FwdFn select_wide_fwd(int m, int n);

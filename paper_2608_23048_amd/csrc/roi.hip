@@ -908,6 +908,42 @@ extern "C" int roi_mask_bwd_adamw_grouped(const roi_adamw_tensor* tensors, int c
                          step, opt, stream);
 }
 
+extern "C" int roi_mask_export(const float* logits, const uint16_t* W, int64_t rows,
+                               int64_t cols, int n, int m, uint16_t* W_masked, uint16_t* values,
+                               uint8_t* idx, uint32_t* meta, hipStream_t stream)
+{
+    Shape sh;
+    if (int st = check_shape(rows, cols, n, m, 1.0f, 1.0f, 0, &sh)) return st;
+    if (meta && !(n == 2 && m == 4))
+        return fail(ROI_E_INVAL, "meta is defined for 2:4 only (got %d:%d)", n, m);
+    if (!W_masked && !values && !idx && !meta)
+        return fail(ROI_E_INVAL, "no output requested");
+    if (sh.numel == 0) return ok();
+    if (!logits || (!W && (W_masked || values)))
+        return fail(ROI_E_INVAL, "logits (and W, for weight outputs) must not be NULL");
+    if (!aligned16(logits) || (W && !aligned16(W)) || (W_masked && !aligned16(W_masked)) ||
+        (values && !aligned16(values)) || (idx && !aligned16(idx)) || (meta && !aligned16(meta)))
+        return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
+    const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
+    const size_t nkept = (size_t)sh.ngroups * (size_t)n;
+    std::vector<Range> ranges;
+    add_range(ranges, logits, nb4, false);
+    add_range(ranges, W, nb2, false);
+    add_range(ranges, W_masked, nb2, true);
+    add_range(ranges, values, nkept * 2, true);
+    add_range(ranges, idx, nkept, true);
+    add_range(ranges, meta, (size_t)((sh.ngroups + 7) / 8) * 4, true);
+    if (int st = check_overlaps(ranges)) return st;
+    ExportFn fn = select_export(m, n);
+    if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
+    ExportArgs a{logits, W, W_masked, values, idx, meta, sh.ngroups};
+    void* args[] = {&a};
+    if (hipLaunchKernel((const void*)fn, dim3(grid_for(sh.ngroups)), dim3(kBlock), args, 0,
+                        stream) != hipSuccess)
+        return launch_status("roi_mask_export");
+    return launch_status("roi_mask_export");
+}
+
 extern "C" int roi_gumbel_noise(uint64_t seed, uint64_t step, uint64_t elem_offset, int64_t count,
                                 uint32_t* words, float* gumbel, hipStream_t stream)
 {

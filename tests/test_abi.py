@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(L):
     assert {"roi_mask_fwd", "roi_mask_fwd_soft", "roi_mask_bwd", "roi_gumbel_noise",
             "roi_gumbel_from_words", "roi_fast_noise_from_words",
             "roi_mask_fwd_grouped", "roi_mask_fwd_soft_grouped", "roi_mask_bwd_grouped",
-            "roi_mask_bwd_adamw", "roi_mask_bwd_adamw_grouped",
+            "roi_mask_bwd_adamw", "roi_mask_bwd_adamw_grouped", "roi_mask_export",
             "roi_anneal", "roi_status_string", "roi_last_error", "roi_abi_version"} <= set(names)
     for name in names:
         assert hasattr(L, name), name
@@ -253,6 +253,36 @@ def test_bwd_adamw_grouped_rejects_before_launch(L):
                                         None) == roi.ROI_OK
     assert L.roi_mask_bwd_adamw_grouped(None, -1, 2, 4, 1.0, 1.0, 0, 0, ctypes.addressof(opt),
                                         None) == roi.ROI_E_INVAL
+
+
+def export(L, **kw):
+    a = dict(logits=FAKE, W=FAKE + GB, rows=4, cols=8, n=2, m=4, Wm=FAKE + 2 * GB,
+             vals=FAKE + 3 * GB, idx=FAKE + 4 * GB, meta=None)
+    a.update(kw)
+    return L.roi_mask_export(a["logits"], a["W"], a["rows"], a["cols"], a["n"], a["m"], a["Wm"],
+                             a["vals"], a["idx"], a["meta"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(meta=FAKE + 5 * GB, n=4, m=8), roi.ROI_E_INVAL),   # metadata only for 2:4
+    (dict(Wm=None, vals=None, idx=None), roi.ROI_E_INVAL),  # nothing requested
+    (dict(logits=None), roi.ROI_E_INVAL),
+    (dict(W=None), roi.ROI_E_INVAL),                        # W needed for weight outputs
+    (dict(W=FAKE + GB + 2), roi.ROI_E_INVAL),
+    (dict(vals=FAKE + GB + 8), roi.ROI_E_INVAL),            # overlaps W
+    (dict(idx=FAKE + 3 * GB + 4 * 2), roi.ROI_E_INVAL),    # misaligned
+    (dict(idx=FAKE + 3 * GB), roi.ROI_E_INVAL),             # same address as the values
+    (dict(cols=6), roi.ROI_E_INVAL),
+    (dict(m=12, n=2, cols=12), roi.ROI_E_UNSUPPORTED),
+    (dict(n=0), roi.ROI_E_INVAL),
+])
+def test_export_rejects_before_launch(L, kw, status):
+    assert export(L, **kw) == status
+    assert L.roi_last_error()
+
+
+def test_export_empty_is_a_no_op(L):
+    assert export(L, rows=0, logits=None, W=None, Wm=None, vals=None, idx=FAKE) == roi.ROI_OK
 
 
 def test_empty_input_is_a_no_op(L):

@@ -470,6 +470,73 @@ def test_bwd_adamw_grouped_equals_single(dev):
             assert torch.equal(a.view(torch.int32), b.view(torch.int32))
 
 
+# --------------------------------------------------------------------------- final-mask export
+EXPORT = [(37, 36, 2, 4), (5, 12, 2, 4), (64, 256, 2, 4), (33, 64, 1, 4), (33, 64, 3, 4),
+          (21, 64, 4, 4), (61, 88, 4, 8), (61, 88, 2, 8), (61, 88, 7, 8), (37, 48, 8, 16),
+          (21, 80, 1, 16), (13, 64, 5, 32), (7, 32, 31, 32), (9, 64, 16, 32)]
+
+
+@pytest.mark.parametrize("case", EXPORT, ids=lambda c: "x".join(map(str, c)))
+def test_export_bit_exact(dev, case):
+    """The final mask (top-n of the logits) in every form, bit for bit against
+    the oracle, with many exact ties; the 2:4 metadata over group counts that
+    leave a partial last word."""
+    import torch
+    rows, cols, n, m = case
+    say(f"export {rows}x{cols} {n}:{m}")
+    W, L, _ = wl.small_case(rows, cols, rows * cols + n, device=dev)
+    L = L.clone()
+    L.view(-1, m)[::3] = torch.round(L.view(-1, m)[::3] * 2) / 2  # exact ties
+    meta = n == 2 and m == 4
+    Wm, vals, idx, mt = roi.mask_export(L, W, n, m, want_meta=meta)
+    _, _, idx_only, mt_only = roi.mask_export(L, None, n, m, want_dense=False, want_values=False,
+                                              want_meta=meta)
+    torch.cuda.synchronize()
+    Wm_o, vals_o, idx_o, mt_o = oracle.export(f32(L), bf16_bits(W), n, m, want_meta=meta)
+    assert np.array_equal(bf16_bits(Wm).reshape(-1), Wm_o)
+    assert np.array_equal(bf16_bits(vals), vals_o)
+    assert np.array_equal(idx.cpu().numpy(), idx_o)
+    assert np.array_equal(idx_only.cpu().numpy(), idx_o)
+    if meta:
+        assert np.array_equal(mt.cpu().numpy().view(np.uint32), mt_o)
+        assert np.array_equal(mt_only.cpu().numpy().view(np.uint32), mt_o)
+
+
+def test_export_full_7b_stack(dev):
+    """The 7B-class stack at 2:4 in one call: sampled groups against the oracle,
+    and on every group the metadata equals the indices and the compressed
+    values equal the dense mask."""
+    import torch
+    work = wl.WORKLOADS["qwen2.5-7b-stack-2:4"]
+    say(f"export full stack: {work.numel} weights")
+    W, L, G = wl.fill_slab(work, dev)
+    del G
+    Wm, vals, idx, mt = roi.mask_export(L, W, 2, 4, want_meta=True)
+    torch.cuda.synchronize()
+    ng = work.numel // 4
+    chunk = 1 << 26
+    for g0 in range(0, ng, chunk):
+        g1 = min(ng, g0 + chunk)
+        ii = idx[g0:g1].long()
+        assert bool((ii[:, 0] < ii[:, 1]).all())
+        words = mt[g0 // 8:(g1 + 7) // 8].view(torch.int32)
+        q = torch.arange(g0, g1, device=dev)
+        nib = (words[(q - g0) // 8] >> (4 * (q % 8))) & 0xF
+        assert torch.equal(nib & 3, ii[:, 0]) and torch.equal(nib >> 2, ii[:, 1])
+        dense = torch.zeros((g1 - g0, 4), dtype=torch.int16, device=dev)
+        dense.scatter_(1, ii, vals[g0:g1].view(torch.int16))
+        assert torch.equal(dense, Wm[g0 * 4:g1 * 4].view(-1, 4).view(torch.int16))
+        del ii, words, q, nib, dense
+    picks = sample_groups(work, ng, 4, np.random.default_rng(77), 30000)
+    pt = torch.from_numpy(picks).to(dev)
+    take = lambda t: t.view(-1, 4).index_select(0, pt)
+    _, vals_o, idx_o, _ = oracle.export(f32(take(L)), bf16_bits(take(W)), 2, 4)
+    assert np.array_equal(idx.index_select(0, pt).cpu().numpy(), idx_o)
+    assert np.array_equal(bf16_bits(vals.index_select(0, pt)), vals_o)
+    del W, L, Wm, vals, idx, mt
+    torch.cuda.empty_cache()
+
+
 def test_every_output_written_and_deterministic(dev):
     import torch
     W, L, G = wl.small_case(333, 64, 1, device=dev)
