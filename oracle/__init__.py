@@ -100,6 +100,14 @@ def lib():
         L.oracle_export.argtypes = [_f32p, _u16p, _i64, _int, _int, _u16p, _u16p, _u8p,
                                     ctypes.POINTER(ctypes.c_uint32)]
         L.oracle_export.restype = _int
+        L.oracle_cat_candidates.argtypes = [_int, _int, ctypes.POINTER(ctypes.c_uint32)]
+        L.oracle_cat_candidates.restype = _int
+        L.oracle_cat_fwd.argtypes = [_u16p, _f32p, _i64, _int, _int, _f32, _f32, _u64, _u64, _u64,
+                                     _u16p, _f64p, _u8p]
+        L.oracle_cat_fwd.restype = _int
+        L.oracle_cat_bwd.argtypes = [_u16p, _u16p, _f32p, _i64, _int, _int, _f32, _f32, _u64,
+                                     _u64, _u64, _f64p]
+        L.oracle_cat_bwd.restype = _int
         _lib = L
     return _lib
 
@@ -228,6 +236,44 @@ def export(logits, W_bits, n: int, m: int, want_meta: bool = False):
                                _ptr(Wm, ctypes.c_uint16), _ptr(vals, ctypes.c_uint16),
                                _ptr(idx, ctypes.c_uint8), _ptr(meta, ctypes.c_uint32)), "export")
     return Wm, vals, idx, meta
+
+
+def cat_candidates(n: int, m: int) -> np.ndarray:
+    """The candidate masks of the categorical sampler (bitmasks, lexicographic)."""
+    out = np.zeros(70, dtype=np.uint32)
+    C = lib().oracle_cat_candidates(n, m, _ptr(out, ctypes.c_uint32))
+    _check(0 if C > 0 else -1, "cat_candidates")
+    return out[:C].copy()
+
+
+def cat_fwd(W_bits, alpha, n: int, m: int, tau: float, lam: float, seed: int, step: int,
+            group_offset: int = 0, want_soft: bool = True):
+    """Categorical sampler forward: (W_masked bits, S fp64 or None, choice uint8 [G])."""
+    C = cat_candidates(n, m).size
+    W = np.ascontiguousarray(W_bits, dtype=np.uint16).reshape(-1)
+    a = np.ascontiguousarray(alpha, dtype=np.float32).reshape(-1)
+    G = W.size // m
+    assert a.size == G * C
+    Wm = np.empty(W.size, dtype=np.uint16)
+    S = np.empty(W.size, dtype=np.float64) if want_soft else None
+    ch = np.empty(G, dtype=np.uint8)
+    _check(lib().oracle_cat_fwd(_ptr(W, ctypes.c_uint16), _ptr(a, ctypes.c_float), G, n, m, tau,
+                                lam, seed, step, group_offset, _ptr(Wm, ctypes.c_uint16),
+                                _ptr(S, ctypes.c_double), _ptr(ch, ctypes.c_uint8)), "cat_fwd")
+    return Wm, S, ch
+
+
+def cat_bwd(G_bits, W_bits, alpha, n: int, m: int, tau: float, lam: float, seed: int, step: int,
+            group_offset: int = 0) -> np.ndarray:
+    """Categorical sampler backward: dL/dalpha (fp64, [G * C])."""
+    Gb = np.ascontiguousarray(G_bits, dtype=np.uint16).reshape(-1)
+    W = np.ascontiguousarray(W_bits, dtype=np.uint16).reshape(-1)
+    a = np.ascontiguousarray(alpha, dtype=np.float32).reshape(-1)
+    d = np.empty(a.size, dtype=np.float64)
+    _check(lib().oracle_cat_bwd(_ptr(Gb, ctypes.c_uint16), _ptr(W, ctypes.c_uint16),
+                                _ptr(a, ctypes.c_float), W.size // m, n, m, tau, lam, seed, step,
+                                group_offset, _ptr(d, ctypes.c_double)), "cat_bwd")
+    return d
 
 
 # --------------------------------------------------------------------------- whole arrays

@@ -566,3 +566,130 @@ int oracle_export(const float* logits, const uint16_t* W, int64_t numel, int n, 
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------------- *
+ * 10. The categorical mask sampler the paper compares with (appendix,
+ *     "Optimization Efficiency": one logit alpha_c per feasible n-hot mask c
+ *     of a group, Pr(c) = softmax(alpha)_c, sampled by Gumbel-Softmax).
+ *     Readings (shared with the kernels):
+ *     - the C = binom(m, n) candidates are the n-subsets of {0..m-1} in
+ *       lexicographic order;
+ *     - keys kappa_c = fl(fl(alpha_c / lambda) + g_c), as for the item
+ *       logits; candidate c of global group Q draws the noise of element
+ *       index 4 B Q + c, B = ceil(C / 4) (each group starts a Philox block);
+ *     - the hard sample is the candidate of largest key (ties to the lower
+ *       candidate index); W_masked = W (.) that mask;
+ *     - relaxed: y = softmax(kappa / tau) and S_j = sum_c y_c [j in c];
+ *     - backward (straight-through, as for the item logits): sbar = G (.) W,
+ *       ybar_c = sum_{j in c} sbar_j, dL/dkappa = y (.) (ybar - <y, ybar>) / tau,
+ *       dL/dalpha = dL/dkappa / lambda.
+ * ------------------------------------------------------------------------- */
+#define ORACLE_MAX_CAT 70
+
+int oracle_cat_candidates(int n, int m, uint32_t* masks)
+{
+    if (m < 1 || m > 8 || n < 1 || n > m) return -1;
+    int count = 0;
+    for (uint32_t bits = 0; bits < (1u << m); ++bits) {
+        int pop = 0;
+        for (int j = 0; j < m; ++j) pop += (bits >> j) & 1u;
+        if (pop == n) ++count;
+    }
+    /* lexicographic order of the index sets: walk the combinations directly */
+    int idx[8], c = 0;
+    for (int k = 0; k < n; ++k) idx[k] = k;
+    for (;;) {
+        uint32_t mask = 0;
+        for (int k = 0; k < n; ++k) mask |= 1u << idx[k];
+        if (masks) masks[c] = mask;
+        ++c;
+        int k = n - 1;
+        while (k >= 0 && idx[k] == m - n + k) --k;
+        if (k < 0) break;
+        ++idx[k];
+        for (int r = k + 1; r < n; ++r) idx[r] = idx[r - 1] + 1;
+    }
+    return c == count ? c : -1;
+}
+
+static int cat_group_keys(const float* alpha, int C, float lambda, uint64_t seed, uint64_t step,
+                          uint64_t Q, float* kappa)
+{
+    const uint64_t B = (uint64_t)(C + 3) / 4;
+    int best = 0;
+    for (int c = 0; c < C; ++c) {
+        kappa[c] = key_of(alpha[c], lambda, seed, step, 4 * B * Q + (uint64_t)c);
+        if (kappa[c] > kappa[best]) best = c; /* strict: ties keep the lower index */
+    }
+    return best;
+}
+
+static void cat_softmax(const float* kappa, int C, double tau, double* y)
+{
+    double mx = kappa[0];
+    for (int c = 1; c < C; ++c) mx = kappa[c] > mx ? kappa[c] : mx;
+    double t = 0.0;
+    for (int c = 0; c < C; ++c) {
+        y[c] = exp(((double)kappa[c] - mx) / tau);
+        t += y[c];
+    }
+    for (int c = 0; c < C; ++c) y[c] /= t;
+}
+
+int oracle_cat_fwd(const uint16_t* W, const float* alpha, int64_t ngroups, int n, int m,
+                   float tau, float lambda, uint64_t seed, uint64_t step, uint64_t group_offset,
+                   uint16_t* W_masked, double* S, uint8_t* choice)
+{
+    uint32_t masks[ORACLE_MAX_CAT];
+    if (check_args(ngroups, n, m, tau, lambda)) return -1;
+    const int C = oracle_cat_candidates(n, m, masks);
+    if (C < 1 || C > ORACLE_MAX_CAT) return -1;
+    for (int64_t q = 0; q < ngroups; ++q) {
+        float kappa[ORACLE_MAX_CAT];
+        const int best = cat_group_keys(alpha + q * C, C, lambda, seed, step,
+                                        group_offset + (uint64_t)q, kappa);
+        if (choice) choice[q] = (uint8_t)best;
+        for (int j = 0; j < m; ++j)
+            if (W_masked)
+                W_masked[q * m + j] = ((masks[best] >> j) & 1u) ? W[q * m + j] : (uint16_t)0;
+        if (S) {
+            double y[ORACLE_MAX_CAT];
+            cat_softmax(kappa, C, (double)tau, y);
+            for (int j = 0; j < m; ++j) {
+                double acc = 0.0;
+                for (int c = 0; c < C; ++c)
+                    if ((masks[c] >> j) & 1u) acc += y[c];
+                S[q * m + j] = acc;
+            }
+        }
+    }
+    return 0;
+}
+
+int oracle_cat_bwd(const uint16_t* G, const uint16_t* W, const float* alpha, int64_t ngroups,
+                   int n, int m, float tau, float lambda, uint64_t seed, uint64_t step,
+                   uint64_t group_offset, double* dalpha)
+{
+    uint32_t masks[ORACLE_MAX_CAT];
+    if (check_args(ngroups, n, m, tau, lambda)) return -1;
+    const int C = oracle_cat_candidates(n, m, masks);
+    if (C < 1 || C > ORACLE_MAX_CAT) return -1;
+    for (int64_t q = 0; q < ngroups; ++q) {
+        float kappa[ORACLE_MAX_CAT];
+        double y[ORACLE_MAX_CAT], ybar[ORACLE_MAX_CAT], sbar[8];
+        cat_group_keys(alpha + q * C, C, lambda, seed, step, group_offset + (uint64_t)q, kappa);
+        cat_softmax(kappa, C, (double)tau, y);
+        for (int j = 0; j < m; ++j)
+            sbar[j] = (double)bf16_to_float(G[q * m + j]) * (double)bf16_to_float(W[q * m + j]);
+        double dot = 0.0;
+        for (int c = 0; c < C; ++c) {
+            ybar[c] = 0.0;
+            for (int j = 0; j < m; ++j)
+                if ((masks[c] >> j) & 1u) ybar[c] += sbar[j];
+            dot += y[c] * ybar[c];
+        }
+        for (int c = 0; c < C; ++c)
+            dalpha[q * C + c] = y[c] * (ybar[c] - dot) / (double)tau / (double)lambda;
+    }
+    return 0;
+}

@@ -61,6 +61,16 @@ double oracle_anneal(double v_init, double v_end, double t, double t_anneal);
 int oracle_export(const float* logits, const uint16_t* W, int64_t numel, int n, int m,
                   uint16_t* W_masked, uint16_t* values, uint8_t* idx, uint32_t* meta);
 
+/* Categorical sampler (one logit per candidate mask): candidates, forward
+ * (W_masked, S fp64, chosen candidate) and backward (dL/dalpha fp64). */
+int oracle_cat_candidates(int n, int m, uint32_t* masks);
+int oracle_cat_fwd(const uint16_t* W, const float* alpha, int64_t ngroups, int n, int m,
+                   float tau, float lambda, uint64_t seed, uint64_t step, uint64_t group_offset,
+                   uint16_t* W_masked, double* S, uint8_t* choice);
+int oracle_cat_bwd(const uint16_t* G, const uint16_t* W, const float* alpha, int64_t ngroups,
+                   int n, int m, float tau, float lambda, uint64_t seed, uint64_t step,
+                   uint64_t group_offset, double* dalpha);
+
 /* AdamW step on numel logits from an fp64 gradient (fp64 outputs). */
 int oracle_adamw(const double* grad, int64_t numel, double lr, double beta1, double beta2,
                  double eps, double weight_decay, int64_t t, const float* phi, const float* m,

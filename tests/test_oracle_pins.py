@@ -662,3 +662,94 @@ def test_export_is_the_lambda_to_zero_limit_of_the_sampler(n, m):
         q = np.arange(G)
         nib = (meta[q // 8] >> (4 * (q % 8))) & 0xF
         assert np.array_equal(np.stack([nib & 3, nib >> 2], axis=1), idx)
+
+
+# --------------------------------------------------------------------------- categorical sampler
+@pytest.mark.parametrize("n,m", [(1, 4), (2, 4), (3, 4), (4, 4), (1, 8), (2, 8), (4, 8), (7, 8)])
+def test_cat_candidates_are_the_lexicographic_subsets(n, m):
+    import itertools
+    got = oracle.cat_candidates(n, m)
+    ref = [sum(1 << j for j in comb) for comb in itertools.combinations(range(m), n)]
+    assert got.tolist() == ref
+
+
+@pytest.mark.parametrize("m", [4, 8])
+def test_cat_with_one_kept_entry_is_the_item_sampler(m):
+    """At n = 1 the candidates are the single entries, candidate c of group Q
+    draws the noise of element m Q + c, and Gumbel-Softmax over one logit per
+    entry is the item sampler's top-1 relaxation: both oracles must agree
+    (choice, masked weights exactly; S and the gradient to rounding)."""
+    rng = np.random.default_rng(m)
+    G, off, tau, lam = 3000, 17, 0.4, 0.7
+    bf = lambda x: (x.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    W = bf(rng.normal(0, 1, G * m))
+    Gb = bf(rng.normal(0, 1, G * m))
+    phi = rng.normal(0, 1, G * m).astype(np.float32)
+    Wm_c, S_c, ch = oracle.cat_fwd(W, phi, 1, m, tau, lam, 5, 2, off)
+    Wm_r, S_r, idx = oracle.mask_fwd(W, phi, 1, m, tau, lam, 5, 2, off * m)
+    assert np.array_equal(ch, idx[:, 0]) and np.array_equal(Wm_c, Wm_r)
+    np.testing.assert_allclose(S_c, S_r, rtol=1e-13, atol=1e-15)
+    d_c = oracle.cat_bwd(Gb, W, phi, 1, m, tau, lam, 5, 2, off)
+    d_r = oracle.mask_bwd(Gb, W, phi, 1, m, tau, lam, 5, 2, off * m)
+    np.testing.assert_allclose(d_c, d_r, rtol=1e-10, atol=1e-12 * np.abs(d_r).max())
+
+
+@pytest.mark.parametrize("n,m,lam", [(2, 4, 1.0), (2, 4, 0.5), (2, 8, 1.0), (4, 8, 1.0)])
+def test_cat_choice_follows_softmax(n, m, lam):
+    """Gumbel-max: the chosen candidate is distributed as softmax(alpha / lambda)."""
+    from scipy.stats import chisquare
+    rng = np.random.default_rng(n * 10 + m)
+    C = oracle.cat_candidates(n, m).size
+    a = rng.normal(0, 1, C).astype(np.float32)
+    G = 200000 if C < 30 else 60000
+    alpha = np.tile(a, G)
+    W = np.ones(G * m, dtype=np.uint16)
+    _, _, ch = oracle.cat_fwd(W, alpha, n, m, 1.0, lam, 11, 3, 0, want_soft=False)
+    p = np.exp(a.astype(np.float64) / np.float32(lam))
+    p /= p.sum()
+    counts = np.bincount(ch, minlength=C)
+    ok = p * G >= 5
+    stat = chisquare(counts[ok], p[ok] * G * counts[ok].sum() / (p[ok] * G).sum())
+    assert stat.pvalue > 1e-4
+
+
+def test_cat_invariants_and_gradient():
+    """S sums to n, lies in [0, 1], tends to the hard mask as tau -> 0; a uniform
+    upstream gradient gives zero; the backward matches central differences of
+    <sbar, S> in fp64."""
+    rng = np.random.default_rng(3)
+    bf = lambda x: (x.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    for n, m in ((2, 4), (2, 8), (4, 8)):
+        C = oracle.cat_candidates(n, m).size
+        G = 300
+        alpha = rng.normal(0, 1, G * C).astype(np.float32)
+        W = bf(rng.normal(0, 1, G * m))
+        Wm, S, ch = oracle.cat_fwd(W, alpha, n, m, 0.6, 1.0, 4, 1, 9)
+        np.testing.assert_allclose(S.reshape(G, m).sum(1), n, rtol=1e-12)
+        assert S.min() >= 0 and S.max() <= 1 + 1e-12
+        _, S0, ch0 = oracle.cat_fwd(W, alpha, n, m, 1e-4, 1.0, 4, 1, 9)
+        hard = (Wm != 0).reshape(G, m)
+        np.testing.assert_allclose(S0.reshape(G, m)[::7], hard[::7], atol=1e-6)
+        one = np.full(G * m, 0x3F80, np.uint16)  # bf16 1.0 for W and G: sbar = 1
+        d = oracle.cat_bwd(one, one, alpha, n, m, 0.6, 1.0, 4, 1, 9)
+        assert np.abs(d).max() < 1e-12
+        # central differences of L(alpha) = <sbar, S(alpha)> on a few groups,
+        # divided by the actual change of the (fp32) key of that candidate
+        Gb = bf(rng.normal(0, 1, G * m))
+        B = (C + 3) // 4
+        sbar = ((Gb.astype(np.uint32) << 16).view(np.float32).astype(np.float64) *
+                (W.astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+        d = oracle.cat_bwd(Gb, W, alpha, n, m, 0.6, 1.0, 4, 1, 9)
+        for q in (0, 17, 123):
+            for c in (0, C // 2, C - 1):
+                h = np.float32(2.0 ** -10)
+                ap, am = alpha.copy(), alpha.copy()
+                ap[q * C + c] += h
+                am[q * C + c] -= h
+                Sp = oracle.cat_fwd(W, ap, n, m, 0.6, 1.0, 4, 1, 9)[1]
+                Sm = oracle.cat_fwd(W, am, n, m, 0.6, 1.0, 4, 1, 9)[1]
+                e = 4 * B * (9 + q) + c
+                kp = float(oracle.keys(ap[q * C + c:q * C + c + 1], 1.0, 4, 1, e)[0])
+                km = float(oracle.keys(am[q * C + c:q * C + c + 1], 1.0, 4, 1, e)[0])
+                fd = (sbar @ Sp - sbar @ Sm) / (kp - km)
+                assert abs(fd - d[q * C + c]) <= 1e-4 * np.abs(d).max(), (n, m, q, c, fd)
