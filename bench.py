@@ -311,6 +311,85 @@ def run_export(args) -> int:
     return 0
 
 
+def run_cat(args) -> int:
+    """--mode cat: the categorical sampler (one logit per candidate mask, the
+    parameterization the paper compares with) against the item sampler on the
+    same stack and pattern (--pattern n:m), one forward + one backward each."""
+    import torch
+
+    import paper_2608_23048_amd as roi
+    from paper_2608_23048_amd import workloads as wl
+
+    roi.lib()
+    work = wl.WORKLOADS[args.workload]
+    n, m = (int(x) for x in (args.pattern or f"{work.n}:{work.m}").split(":"))
+    C = roi.cat_num_candidates(n, m)
+    numel = work.numel
+    dev = torch.device("cuda:0")
+    print(f"# cat mode, workload {work.name}: {numel} weights, {n}:{m}, {C} logits per group",
+          file=sys.stderr, flush=True)
+    W, L, G = wl.fill_slab(work, dev)
+    Wm = torch.empty_like(W)
+
+    def timed(fwd, bwd):
+        for t in range(max(args.warmup, 1)):
+            fwd(t), bwd(t)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for t in range(args.steps):
+            ev[t][0].record()
+            fwd(t)
+            ev[t][1].record()
+            bwd(t)
+            ev[t][2].record()
+        torch.cuda.synchronize()
+        el = (time.perf_counter() - t0) * 1e3 / args.steps
+        return (el, sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps,
+                sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps)
+
+    tau = work.tau
+    idx = torch.empty((numel // m, n), dtype=torch.uint8, device=dev)
+    dphi = torch.empty_like(L)
+    roi_ms = timed(lambda t: roi.mask_fwd(W, L, n, m, tau, 1.0, 0, t, 0,
+                                          out={"W_masked": Wm, "sel_idx": idx}),
+                   lambda t: roi.mask_bwd(G, W, L, n, m, tau, 1.0, 0, t, 0, out=dphi))
+    del L, dphi, idx
+    torch.cuda.empty_cache()
+    print(f"# item sampler: {roi_ms[0]:.3f} ms/step (fwd {roi_ms[1]:.3f}, bwd {roi_ms[2]:.3f})",
+          file=sys.stderr, flush=True)
+    ngroups = numel // m
+    A = torch.empty((ngroups, C), dtype=torch.float32, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4_000_000)
+    A.normal_(0.0, 1.0, generator=gen)
+    dA = torch.empty_like(A)
+    ch = torch.empty(ngroups, dtype=torch.uint8, device=dev)
+    cat_ms = timed(lambda t: roi.cat_mask_fwd(W, A, n, m, tau, 1.0, 0, t, 0,
+                                              out={"W_masked": Wm, "choice": ch}),
+                   lambda t: roi.cat_mask_bwd(G, W, A, n, m, tau, 1.0, 0, t, 0, out=dA))
+    print(f"# categorical sampler: {cat_ms[0]:.3f} ms/step (fwd {cat_ms[1]:.3f}, bwd "
+          f"{cat_ms[2]:.3f})", file=sys.stderr, flush=True)
+    cb_f = 2 + 4 * C / m + 2 + 1 / m
+    cb_b = 2 + 2 + 8 * C / m
+    bf, bb = algorithmic_bytes(n, m)
+    out = {"metric": f"masked weights/sec (categorical sampler fwd+bwd), {work.name} {n}:{m}",
+           "value": numel / (cat_ms[0] * 1e-3), "unit": "masked weights/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": cat_ms[0],
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic (as the default mode; categorical logits ~N(0,1))",
+           "config": {"workload": work.name, "masked_weights": numel, "pattern": f"{n}:{m}",
+                      "logits_per_weight": {"categorical": C / m, "item": 1.0}},
+           "categorical": {"fwd_ms": cat_ms[1], "bwd_ms": cat_ms[2],
+                           "bytes_per_weight": {"fwd": cb_f, "bwd": cb_b},
+                           "GBps": {"fwd": cb_f * numel / cat_ms[1] / 1e6,
+                                    "bwd": cb_b * numel / cat_ms[2] / 1e6}},
+           "item": {"ms_per_step": roi_ms[0], "fwd_ms": roi_ms[1], "bwd_ms": roi_ms[2],
+                    "bytes_per_weight": {"fwd": bf, "bwd": bb}}}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -318,10 +397,12 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="qwen2.5-7b-stack-2:4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("st", "adamw", "export"), default="st",
+    ap.add_argument("--pattern", default=None, help="n:m for --mode cat (default: the workload's)")
+    ap.add_argument("--mode", choices=("st", "adamw", "export", "cat"), default="st",
                     help="st: forward + backward (the headline); adamw: forward + backward "
                          "with the AdamW step on the logits fused in; export: the final-mask "
-                         "export after training")
+                         "export after training; cat: the categorical sampler against the item "
+                         "sampler")
     ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
                     help="only run a plain device copy of BYTES (PMC calibration)")
     ap.add_argument("--pmc-summary", nargs=5,
@@ -343,6 +424,8 @@ def main() -> int:
         return run_adamw(args)
     if args.mode == "export":
         return run_export(args)
+    if args.mode == "cat":
+        return run_cat(args)
 
     import torch
 

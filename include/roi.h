@@ -247,6 +247,34 @@ int roi_mask_export(const float* logits, const uint16_t* W, int64_t rows, int64_
                     hipStream_t stream);
 
 /*
+ * The categorical mask sampler: the parameterization the paper compares with
+ * (appendix, "Optimization Efficiency"), one logit per feasible n-hot mask of
+ * a group, Pr(c) = softmax(alpha)_c, sampled with Gumbel-Softmax.  It is a
+ * second workload on the same harness: binom(m, n) logits per group instead
+ * of m (1.5x the weights at 2:4, 3.5x at 2:8, 8.75x at 4:8).
+ *  - candidates: the n-subsets of {0..m-1} in lexicographic order;
+ *  - keys kappa_c = fl(fl(alpha_c / lambda) + g_c), g_c the noise of element
+ *    4 B Q + c with B = ceil(C / 4), Q = group_offset + local group index;
+ *  - hard sample: the candidate of largest key (ties to the lower candidate),
+ *    W_masked = W (.) its mask, choice = its index;
+ *  - soft mask S_j = sum_c softmax(kappa / tau)_c [j in c];
+ *  - backward (straight-through): ybar_c = sum_{j in c} (dL/dW_masked (.) W)_j,
+ *    dL/dalpha = softmax (.) (ybar - <softmax, ybar>) / (tau lambda).
+ * m in {4, 8}.  cat_logits fp32 [rows*cols/m, C] (group-major).  Other
+ * arguments and conventions as for the item sampler.
+ */
+/* binom(m, n), the logits per group, or -1 for an unsupported pattern. */
+int roi_cat_num_candidates(int n, int m);
+int roi_cat_mask_fwd(const uint16_t* W, const float* cat_logits, int64_t rows, int64_t cols,
+                     int n, int m, float tau, float lambda, uint64_t seed, uint64_t step,
+                     uint64_t group_offset, uint16_t* W_masked, float* soft_mask,
+                     uint8_t* choice, hipStream_t stream);
+int roi_cat_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* cat_logits,
+                     int64_t rows, int64_t cols, int n, int m, float tau, float lambda,
+                     uint64_t seed, uint64_t step, uint64_t group_offset, float* grad_cat_logits,
+                     hipStream_t stream);
+
+/*
  * roi_gumbel_noise -- the noise of `count` consecutive elements starting at
  * global index elem_offset (elem_offset % 4 == 0): the raw Philox words
  * and/or g = -L(-L(u)) (Algorithm 1).  Either output may be NULL, not both.

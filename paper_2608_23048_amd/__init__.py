@@ -94,6 +94,14 @@ def lib() -> ctypes.CDLL:
         L.roi_mask_bwd_adamw_grouped.restype = _int
         L.roi_mask_export.argtypes = [_vp, _vp, _i64, _i64, _int, _int, _vp, _vp, _vp, _vp, _vp]
         L.roi_mask_export.restype = _int
+        L.roi_cat_num_candidates.argtypes = [_int, _int]
+        L.roi_cat_num_candidates.restype = _int
+        L.roi_cat_mask_fwd.argtypes = [_vp, _vp, _i64, _i64, _int, _int, _f32, _f32, _u64, _u64,
+                                       _u64, _vp, _vp, _vp, _vp]
+        L.roi_cat_mask_fwd.restype = _int
+        L.roi_cat_mask_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _int, _int, _f32, _f32, _u64,
+                                       _u64, _u64, _vp, _vp]
+        L.roi_cat_mask_bwd.restype = _int
         L.roi_gumbel_noise.argtypes = [_u64, _u64, _u64, _i64, _vp, _vp, _vp]
         L.roi_gumbel_noise.restype = _int
         L.roi_gumbel_from_words.argtypes = [_vp, _i64, _vp, _vp]
@@ -268,6 +276,62 @@ def mask_export(logits, W, n: int, m: int, want_dense: bool = True, want_values:
     _raise_on(lib().roi_mask_export(_ptr(logits), _ptr(W), rows, cols, n, m, _ptr(Wm), _ptr(vals),
                                     _ptr(idx), _ptr(meta), _stream(logits)))
     return Wm, vals, idx, meta
+
+
+def cat_num_candidates(n: int, m: int) -> int:
+    """binom(m, n): logits per group of the categorical sampler (-1 if not built)."""
+    return int(lib().roi_cat_num_candidates(n, m))
+
+
+def _check_cat(W, cat_logits, n, m):
+    import torch
+    _check_tensor(W, torch.bfloat16, "W")
+    _check_tensor(cat_logits, torch.float32, "cat_logits")
+    C = cat_num_candidates(n, m)
+    if C < 1:
+        raise RoiError(ROI_E_UNSUPPORTED, f"no categorical sampler for {n}:{m}")
+    if cat_logits.numel() != (W.numel() // m) * C:
+        raise ValueError(f"cat_logits must hold {C} logits per group of {m} weights")
+    return C
+
+
+def cat_mask_fwd(W, cat_logits, n: int, m: int, tau: float = 1.0, lam: float = 1.0,
+                 seed: int = 0, step: int = 0, group_offset: int = 0, want_soft: bool = False,
+                 want_choice: bool = True, out: dict | None = None):
+    """Categorical sampler forward (one logit per candidate mask, [G, C] fp32):
+    returns (W_masked bf16, soft mask fp32 or None, chosen candidate uint8 [G]
+    or None)."""
+    import torch
+    _check_cat(W, cat_logits, n, m)
+    rows, cols = _shape2d(W)
+    out = out or {}
+    Wm = out.get("W_masked")
+    if Wm is None:
+        Wm = torch.empty_like(W)
+    S = out.get("soft_mask") if want_soft else None
+    if want_soft and S is None:
+        S = torch.empty(W.shape, dtype=torch.float32, device=W.device)
+    ch = out.get("choice") if want_choice else None
+    if want_choice and ch is None:
+        ch = torch.empty(W.numel() // m, dtype=torch.uint8, device=W.device)
+    _raise_on(lib().roi_cat_mask_fwd(_ptr(W), _ptr(cat_logits), rows, cols, n, m, tau, lam, seed,
+                                     step, group_offset, _ptr(Wm), _ptr(S), _ptr(ch),
+                                     _stream(W)))
+    return Wm, S, ch
+
+
+def cat_mask_bwd(grad_W_masked, W, cat_logits, n: int, m: int, tau: float = 1.0,
+                 lam: float = 1.0, seed: int = 0, step: int = 0, group_offset: int = 0, out=None):
+    """Categorical sampler backward: dL/dcat_logits (fp32, shaped like cat_logits)."""
+    import torch
+    _check_cat(W, cat_logits, n, m)
+    _check_tensor(grad_W_masked, torch.bfloat16, "grad_W_masked", like=W)
+    rows, cols = _shape2d(W)
+    d = out if out is not None else torch.empty_like(cat_logits)
+    _raise_on(lib().roi_cat_mask_bwd(_ptr(grad_W_masked), _ptr(W), _ptr(cat_logits), rows, cols,
+                                     n, m, tau, lam, seed, step, group_offset, _ptr(d),
+                                     _stream(W)))
+    return d
 
 
 def _offsets(sizes, offsets):

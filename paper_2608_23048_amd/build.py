@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libroi.so")
 SOURCES = [os.path.join(CSRC, "roi.hip"), os.path.join(CSRC, "wide.hip"),
-           os.path.join(CSRC, "export.hip")]
+           os.path.join(CSRC, "export.hip"), os.path.join(CSRC, "cat.hip")]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -1,0 +1,417 @@
+// cat.hip -- gfx950 kernels of the categorical mask sampler, the
+// parameterization the paper compares with (appendix, "Optimization
+// Efficiency"): one logit alpha_c per feasible n-hot mask c of a group,
+// Pr(c) = softmax(alpha)_c, sampled with Gumbel-Softmax.
+//
+// One lane per group of m in {4, 8} weights; the C = binom(m, n) candidate
+// masks are compile-time bitmasks in lexicographic order of their index sets.
+// Keys kappa_c = alpha_c / lambda + g_c with the noise of element 4 B Q + c
+// (B = ceil(C / 4) Philox blocks per group Q).  The hard sample is the
+// candidate of largest key (ties to the lower candidate), the relaxed mask
+// S_j = sum_c y_c [j in c] with y = softmax(kappa / tau), and the backward is
+// the straight-through derivative through that softmax.  As in the item
+// sampler: the forward without S decides with the hardware-log keys when the
+// top two are further apart than their error margin (else with the exact
+// keys); S uses the exact keys; the backward uses the hardware-log keys.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <utility>
+
+#include "common.hpp"
+#include "host.hpp"
+#include "noise.hpp"
+#include "relax.hpp"
+#include "roi.h"
+
+namespace roi {
+namespace {
+
+constexpr int binom(int m, int n)
+{
+    int r = 1;
+    for (int k = 1; k <= n; ++k) r = r * (m - n + k) / k;
+    return r;
+}
+
+template <int M, int N>
+struct Candidates {
+    static constexpr int C = binom(M, N);
+    uint8_t mask[C];
+};
+
+// The n-subsets of {0..m-1} in lexicographic order, as bitmasks.
+template <int M, int N>
+constexpr Candidates<M, N> make_candidates()
+{
+    Candidates<M, N> t{};
+    int idx[8] = {0, 1, 2, 3, 4, 5, 6, 7};
+    for (int c = 0; c < Candidates<M, N>::C; ++c) {
+        int mask = 0;
+        for (int k = 0; k < N; ++k) mask |= 1 << idx[k];
+        t.mask[c] = (uint8_t)mask;
+        int k = N - 1;
+        while (k >= 0 && idx[k] == M - N + k) --k;
+        if (k < 0) break;
+        ++idx[k];
+        for (int r = k + 1; r < N; ++r) idx[r] = idx[r - 1] + 1;
+    }
+    return t;
+}
+
+template <int M, int N>
+constexpr Candidates<M, N> kCand = make_candidates<M, N>();
+
+// Philox words for a 64-bit block index (the block of a candidate need not
+// share its high word with the rest of the launch).
+__device__ __forceinline__ uint4 philox_block64(uint64_t blk, const NoiseKey& key)
+{
+    return philox4x32_10((uint32_t)blk, (uint32_t)(blk >> 32), key.step_lo, key.step_hi, key.k0,
+                         key.k1);
+}
+
+// The C logits of a group (fp32, contiguous, 4C bytes from a 4C-byte stride).
+template <int C>
+__device__ __forceinline__ void load_cat_logits(const float* p, float (&a)[C])
+{
+    if constexpr (C % 4 == 0) {
+#pragma unroll
+        for (int t = 0; t < C / 4; ++t) {
+            const f32x4 v = stream_load(reinterpret_cast<const f32x4*>(p) + t);
+            a[4 * t] = v.x; a[4 * t + 1] = v.y; a[4 * t + 2] = v.z; a[4 * t + 3] = v.w;
+        }
+    } else if constexpr (C % 2 == 0) {
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+        for (int t = 0; t < C / 2; ++t) {
+            const f32x2 v = stream_load(reinterpret_cast<const f32x2*>(p) + t);
+            a[2 * t] = v.x; a[2 * t + 1] = v.y;
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < C; ++c) a[c] = stream_load(p + c);
+    }
+}
+
+template <int C>
+__device__ __forceinline__ void store_cat(float* p, const float (&a)[C])
+{
+    if constexpr (C % 4 == 0) {
+#pragma unroll
+        for (int t = 0; t < C / 4; ++t) {
+            const f32x4 v = {a[4 * t], a[4 * t + 1], a[4 * t + 2], a[4 * t + 3]};
+            stream_store(v, reinterpret_cast<f32x4*>(p) + t);
+        }
+    } else if constexpr (C % 2 == 0) {
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+        for (int t = 0; t < C / 2; ++t) {
+            const f32x2 v = {a[2 * t], a[2 * t + 1]};
+            stream_store(v, reinterpret_cast<f32x2*>(p) + t);
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < C; ++c) stream_store(a[c], p + c);
+    }
+}
+
+struct CatArgs {
+    const uint16_t* W;
+    const float* alpha;
+    const uint16_t* G; // backward
+    uint16_t* Wm;      // forward
+    float* S;
+    uint8_t* choice;
+    float* dalpha;     // backward
+    int64_t ngroups;
+    uint64_t group0;   // global index of group 0
+    NoiseKey key;      // block_hi unused
+    float lambda;
+    float key_c;       // fl(log2(e) / lambda)
+    float inv_lambda;
+    float inv_tau;
+};
+
+// The exact keys of one group (the words x come from its B Philox blocks).
+template <int C>
+__device__ __forceinline__ void cat_exact_keys(const float (&alpha)[C], const uint32_t (&x)[C],
+                                               float lambda, const float2* tab, float (&k)[C])
+{
+    const bool lam1 = lambda == 1.0f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const float ng = neg_gumbel_from_word(x[c], tab);
+        k[c] = (lam1 ? alpha[c] : alpha[c] / lambda) - ng;
+    }
+}
+
+template <int C>
+__device__ __forceinline__ void cat_words(uint64_t Q, const NoiseKey& key, uint32_t (&x)[C])
+{
+    constexpr int B = (C + 3) / 4;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        const uint4 v = philox_block64(Q * B + b, key);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (4 * b + t < C) x[4 * b + t] = w[t];
+    }
+}
+
+// y = softmax(kappa * scale) in place (scale turns key differences into log2
+// units over tau).
+template <int C>
+__device__ __forceinline__ void cat_softmax(float (&k)[C], float scale)
+{
+    float mx = k[0];
+#pragma unroll
+    for (int c = 1; c < C; ++c) mx = fmaxf(mx, k[c]);
+    float t = 0.0f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        k[c] = __builtin_amdgcn_exp2f((k[c] - mx) * scale);
+        t += k[c];
+    }
+    const float r = __builtin_amdgcn_rcpf(t);
+#pragma unroll
+    for (int c = 0; c < C; ++c) k[c] *= r;
+}
+
+template <int M, int N, bool kSoft>
+__global__ __launch_bounds__(kBlock) void cat_fwd_kernel(CatArgs a)
+{
+    constexpr int C = Candidates<M, N>::C;
+    __shared__ float2 tab[kLogCells];
+    fill_log_table(tab);
+    __syncthreads();
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
+        float alpha[C];
+        uint32_t w[M];
+        load_cat_logits<C>(a.alpha + q * C, alpha);
+        load_bf16<M>(a.W + q * M, w);
+        uint32_t x[C];
+        cat_words<C>(a.group0 + (uint64_t)q, a.key, x);
+        float k[C];
+        int best = 0;
+        bool exact = true;
+        if constexpr (!kSoft) {
+            // hardware-log keys; decided when the top two are further apart
+            // than the error margin of two keys (noise.hpp)
+            // (scanned like the exact argmax: a NaN or infinite key leaves the
+            // gap undefined or the margin infinite, so the exact keys decide)
+#pragma unroll
+            for (int c = 0; c < C; ++c) k[c] = fast_key_log2(alpha[c], a.key_c, x[c]);
+            float top = k[0], second = -INFINITY, big = fabsf(k[0]);
+#pragma unroll
+            for (int c = 1; c < C; ++c) {
+                big = fmaxf(big, fabsf(k[c]));
+                const bool better = k[c] > top;
+                second = better ? top : fmaxf(second, k[c]);
+                best = better ? c : best;
+                top = better ? k[c] : top;
+            }
+            const float margin = __builtin_fmaf(big, 0x1p-20f, kFastPairMargin);
+            exact = C > 1 && !(top - second > margin);
+        }
+        if (exact) {
+            cat_exact_keys<C>(alpha, x, a.lambda, tab, k);
+            float top = k[0];
+            best = 0;
+#pragma unroll
+            for (int c = 1; c < C; ++c) {
+                const bool better = k[c] > top; // strict: ties keep the lower candidate
+                best = better ? c : best;
+                top = better ? k[c] : top;
+            }
+        }
+        {
+            uint32_t mask = 0;
+#pragma unroll
+            for (int c = 0; c < C; ++c) mask = best == c ? kCand<M, N>.mask[c] : mask;
+            uint32_t out[M];
+#pragma unroll
+            for (int j = 0; j < M; ++j) out[j] = ((mask >> j) & 1u) ? w[j] : 0u;
+            if constexpr (M == 4) {
+                const u32x2 v = {out[0] | (out[1] << 16), out[2] | (out[3] << 16)};
+                stream_store(v, reinterpret_cast<u32x2*>(a.Wm + q * M));
+            } else {
+                const u32x4 v = {out[0] | (out[1] << 16), out[2] | (out[3] << 16),
+                                 out[4] | (out[5] << 16), out[6] | (out[7] << 16)};
+                stream_store(v, reinterpret_cast<u32x4*>(a.Wm + q * M));
+            }
+            if (a.choice) stream_store((uint8_t)best, a.choice + q);
+        }
+        if constexpr (kSoft) {
+            cat_softmax<C>(k, kLog2e * a.inv_tau);
+            float S[M];
+#pragma unroll
+            for (int j = 0; j < M; ++j) S[j] = 0.0f;
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+#pragma unroll
+                for (int j = 0; j < M; ++j)
+                    if ((kCand<M, N>.mask[c] >> j) & 1) S[j] += k[c];
+            }
+            if (a.S) store_f32<M>(a.S + q * M, S);
+        }
+    }
+}
+
+template <int M, int N>
+__global__ __launch_bounds__(kBlock) void cat_bwd_kernel(CatArgs a)
+{
+    constexpr int C = Candidates<M, N>::C;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
+        float alpha[C];
+        uint32_t w[M], g[M];
+        load_cat_logits<C>(a.alpha + q * C, alpha);
+        load_bf16<M>(a.W + q * M, w);
+        load_bf16<M>(a.G + q * M, g);
+        uint32_t x[C];
+        cat_words<C>(a.group0 + (uint64_t)q, a.key, x);
+        float y[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) y[c] = fast_key_log2(alpha[c], a.key_c, x[c]);
+        cat_softmax<C>(y, a.inv_tau); // keys are in log2 units already
+        // Straight-through: dL/dS = dL/dW_masked (.) W; ybar_c = sum_{j in c} sbar_j.
+        float sbar[M];
+#pragma unroll
+        for (int j = 0; j < M; ++j) sbar[j] = bf16_bits_to_float(g[j]) * bf16_bits_to_float(w[j]);
+        float ybar[C], dot = 0.0f;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int j = 0; j < M; ++j)
+                if ((kCand<M, N>.mask[c] >> j) & 1) acc += sbar[j];
+            ybar[c] = acc;
+            dot = __builtin_fmaf(y[c], acc, dot);
+        }
+        const float s = a.inv_tau * a.inv_lambda;
+        float d[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) d[c] = y[c] * (ybar[c] - dot) * s;
+        store_cat<C>(a.dalpha + q * C, d);
+    }
+}
+
+template <int M, int... Ns>
+void* cat_fwd_for_n(int n, bool soft, std::integer_sequence<int, Ns...>)
+{
+    void* f = nullptr;
+    ((n == Ns + 1 ? (f = soft ? (void*)cat_fwd_kernel<M, Ns + 1, true>
+                              : (void*)cat_fwd_kernel<M, Ns + 1, false>,
+                     0)
+                  : 0),
+     ...);
+    return f;
+}
+
+template <int M, int... Ns>
+void* cat_bwd_for_n(int n, std::integer_sequence<int, Ns...>)
+{
+    void* f = nullptr;
+    ((n == Ns + 1 ? (f = (void*)cat_bwd_kernel<M, Ns + 1>, 0) : 0), ...);
+    return f;
+}
+
+} // namespace
+} // namespace roi
+
+using namespace roi;
+
+extern "C" int roi_cat_num_candidates(int n, int m)
+{
+    if ((m != 4 && m != 8) || n < 1 || n > m) return -1;
+    return binom(m, n);
+}
+
+namespace roi {
+namespace {
+int cat_run(bool fwd, const uint16_t* W, const float* alpha, const uint16_t* G, int64_t rows,
+            int64_t cols, int n, int m, float tau, float lambda, uint64_t seed, uint64_t step,
+            uint64_t group_offset, uint16_t* W_masked, float* S, uint8_t* choice, float* dalpha,
+            hipStream_t stream)
+{
+    const char* what = fwd ? "roi_cat_mask_fwd" : "roi_cat_mask_bwd";
+    if (rows < 0 || cols < 0) return fail(ROI_E_INVAL, "rows and cols must be >= 0");
+    if (m < 1 || n < 1 || n > m)
+        return fail(ROI_E_INVAL, "pattern n:m = %d:%d needs 1 <= n <= m", n, m);
+    if (m != 4 && m != 8)
+        return fail(ROI_E_UNSUPPORTED, "the categorical sampler is built for m = 4 and 8");
+    if (cols % m != 0) return fail(ROI_E_INVAL, "cols must be a multiple of m");
+    if (rows > 0 && cols > ((int64_t)1 << 62) / rows)
+        return fail(ROI_E_INVAL, "rows * cols must be below 2^62");
+    if (!(tau > 0.0f) || !std::isfinite(tau)) return fail(ROI_E_INVAL, "tau must be finite, > 0");
+    if (!(lambda > 0.0f) || !std::isfinite(lambda))
+        return fail(ROI_E_INVAL, "lambda must be finite and > 0");
+    const int C = binom(m, n);
+    const int64_t ngroups = rows * cols / m;
+    const uint64_t B = (uint64_t)(C + 3) / 4;
+    if (ngroups > 0 && group_offset > (UINT64_MAX / (4 * B)) - (uint64_t)ngroups)
+        return fail(ROI_E_INVAL, "group_offset + groups overflows the noise index space");
+    if (ngroups == 0) return ok();
+    if (!W || !alpha || (fwd ? !W_masked : (!G || !dalpha)))
+        return fail(ROI_E_INVAL, "a required pointer is NULL");
+    const void* ptrs[] = {W, alpha, G, W_masked, S, choice, dalpha};
+    for (const void* p : ptrs)
+        if (p && ((uintptr_t)p & 15u))
+            return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
+    const size_t numel = (size_t)ngroups * (size_t)m, nc = (size_t)ngroups * (size_t)C;
+    std::vector<Range> r;
+    add_range(r, W, numel * 2, false);
+    add_range(r, alpha, nc * 4, false);
+    add_range(r, G, numel * 2, false);
+    add_range(r, W_masked, numel * 2, true);
+    add_range(r, S, numel * 4, true);
+    add_range(r, choice, (size_t)ngroups, true);
+    add_range(r, dalpha, nc * 4, true);
+    if (int st = check_overlaps(r)) return st;
+    void* fn = m == 4 ? (fwd ? cat_fwd_for_n<4>(n, S != nullptr, std::make_integer_sequence<int, 4>{})
+                             : cat_bwd_for_n<4>(n, std::make_integer_sequence<int, 4>{}))
+                      : (fwd ? cat_fwd_for_n<8>(n, S != nullptr, std::make_integer_sequence<int, 8>{})
+                             : cat_bwd_for_n<8>(n, std::make_integer_sequence<int, 8>{}));
+    if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
+    CatArgs a{};
+    a.W = W;
+    a.alpha = alpha;
+    a.G = G;
+    a.Wm = W_masked;
+    a.S = S;
+    a.choice = choice;
+    a.dalpha = dalpha;
+    a.ngroups = ngroups;
+    a.group0 = group_offset;
+    a.key = make_key(seed, step, 0);
+    a.lambda = lambda;
+    a.key_c = (float)(1.4426950408889634 / (double)lambda);
+    a.inv_lambda = (float)(1.0 / (double)lambda);
+    a.inv_tau = (float)(1.0 / (double)tau);
+    void* args[] = {&a};
+    if (hipLaunchKernel(fn, dim3(grid_for(ngroups)), dim3(kBlock), args, 0, stream) != hipSuccess)
+        return launch_status(what);
+    return launch_status(what);
+}
+} // namespace
+} // namespace roi
+
+extern "C" int roi_cat_mask_fwd(const uint16_t* W, const float* cat_logits, int64_t rows,
+                                int64_t cols, int n, int m, float tau, float lambda, uint64_t seed,
+                                uint64_t step, uint64_t group_offset, uint16_t* W_masked,
+                                float* soft_mask, uint8_t* choice, hipStream_t stream)
+{
+    return cat_run(true, W, cat_logits, nullptr, rows, cols, n, m, tau, lambda, seed, step,
+                   group_offset, W_masked, soft_mask, choice, nullptr, stream);
+}
+
+extern "C" int roi_cat_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W,
+                                const float* cat_logits, int64_t rows, int64_t cols, int n, int m,
+                                float tau, float lambda, uint64_t seed, uint64_t step,
+                                uint64_t group_offset, float* grad_cat_logits, hipStream_t stream)
+{
+    return cat_run(false, W, cat_logits, grad_W_masked, rows, cols, n, m, tau, lambda, seed, step,
+                   group_offset, nullptr, nullptr, nullptr, grad_cat_logits, stream);
+}

@@ -21,9 +21,98 @@
 #include <vector>
 
 #include "common.hpp"
+#include "host.hpp"
 #include "noise.hpp"
 #include "relax.hpp"
 #include "roi.h"
+
+// ----------------------------------------------------------------------------- host helpers
+// (declared in host.hpp; shared by the translation units of the library)
+namespace roi {
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return status;
+}
+
+int ok()
+{
+    g_last_error.clear();
+    return ROI_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb)
+{
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// Grid for `items` work items of one thread each: one block per `block` items
+// (a one-shot grid dispatched in address order keeps the set of DRAM pages in
+// use compact; measured on MI355X, a plain copy streams at ~6.3 TB/s this way
+// against ~5 TB/s with a fixed grid looping with a large stride).  A dispatch
+// holds its total work-item count in 32 bits, so grids stop below 2^32
+// threads; kernels keep a stride loop for the items beyond.
+int grid_for(int64_t items, int block)
+{
+    const int64_t max_blocks = (int64_t)(0xFFFFFFFFu / (uint32_t)block);
+    const int64_t need = (items + block - 1) / block;
+    return (int)(need < 1 ? 1 : (need < max_blocks ? need : max_blocks));
+}
+
+
+NoiseKey make_key(uint64_t seed, uint64_t step, uint64_t block)
+{
+    NoiseKey k;
+    k.k0 = (uint32_t)seed;
+    k.k1 = (uint32_t)(seed >> 32);
+    k.step_lo = (uint32_t)step;
+    k.step_hi = (uint32_t)(step >> 32);
+    k.block_hi = (uint32_t)(block >> 32);
+    return k;
+}
+
+int launch_status(const char* what)
+{
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(ROI_E_HIP, "%s: launch failed: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+// Outputs may overlap nothing; inputs may overlap each other.  Sorted by
+// start, a range overlaps an earlier one exactly when it starts before the
+// largest end seen so far (of any range, for an output; of the outputs, for
+// an input).
+int check_overlaps(std::vector<Range>& r)
+{
+    std::sort(r.begin(), r.end(), [](const Range& a, const Range& b) { return a.p < b.p; });
+    uintptr_t end_any = 0, end_out = 0;
+    for (const Range& x : r) {
+        if (x.out ? x.p < end_any : x.p < end_out)
+            return fail(ROI_E_INVAL, "an output overlaps another input or output");
+        end_any = std::max(end_any, x.p + x.n);
+        if (x.out) end_out = std::max(end_out, x.p + x.n);
+    }
+    return ROI_OK;
+}
+
+void add_range(std::vector<Range>& r, const void* p, size_t n, bool out)
+{
+    if (p && n) r.push_back({(uintptr_t)p, n, out});
+}
+
+} // namespace roi
 
 namespace roi {
 namespace {
@@ -359,49 +448,6 @@ __global__ __launch_bounds__(kBlock) void gumbel_words_kernel(const uint32_t* wo
 }
 
 // ----------------------------------------------------------------------------- host side
-thread_local std::string g_last_error;
-
-int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
-int fail(int status, const char* fmt, ...)
-{
-    char buf[512];
-    va_list ap;
-    va_start(ap, fmt);
-    std::vsnprintf(buf, sizeof buf, fmt, ap);
-    va_end(ap);
-    g_last_error = buf;
-    return status;
-}
-
-int ok()
-{
-    g_last_error.clear();
-    return ROI_OK;
-}
-
-bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
-
-bool overlap(const void* a, size_t na, const void* b, size_t nb)
-{
-    if (!a || !b || na == 0 || nb == 0) return false;
-    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
-    return a0 < b0 + nb && b0 < a0 + na;
-}
-
-// Grid for `items` work items of one thread each: one block per `block` items
-// (a one-shot grid dispatched in address order keeps the set of DRAM pages in
-// use compact; measured on MI355X, a plain copy streams at ~6.3 TB/s this way
-// against ~5 TB/s with a fixed grid looping with a large stride).  A dispatch
-// holds its total work-item count in 32 bits, so grids stop below 2^32
-// threads; kernels keep a stride loop for the items beyond.
-int grid_for(int64_t items, int block = kBlock)
-{
-    const int64_t max_blocks = (int64_t)(0xFFFFFFFFu / (uint32_t)block);
-    const int64_t need = (items + block - 1) / block;
-    return (int)(need < 1 ? 1 : (need < max_blocks ? need : max_blocks));
-}
-
-
 struct Shape {
     int64_t numel = 0;
     int64_t ngroups = 0;
@@ -435,17 +481,6 @@ int check_shape(int64_t rows, int64_t cols, int n, int m, float tau, float lambd
     return ROI_OK;
 }
 
-NoiseKey make_key(uint64_t seed, uint64_t step, uint64_t block)
-{
-    NoiseKey k;
-    k.k0 = (uint32_t)seed;
-    k.k1 = (uint32_t)(seed >> 32);
-    k.step_lo = (uint32_t)step;
-    k.step_hi = (uint32_t)(step >> 32);
-    k.block_hi = (uint32_t)(block >> 32);
-    return k;
-}
-
 // Calls launch(first, count, elem0) for consecutive pieces of [0, items) --
 // items of `per_item` elements starting at global element elem_offset -- so
 // that within a piece every Philox block index (element / 4) has the same high
@@ -464,13 +499,6 @@ int for_each_piece(uint64_t elem_offset, int64_t items, int64_t per_item, F&& la
         done += count;
     }
     return ROI_OK;
-}
-
-int launch_status(const char* what)
-{
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return fail(ROI_E_HIP, "%s: launch failed: %s", what, hipGetErrorString(e));
-    return ok();
 }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -533,35 +561,6 @@ using namespace roi;
 
 namespace roi {
 namespace {
-
-// One checked address range of a call: [p, p + n), an input or an output.
-struct Range {
-    uintptr_t p;
-    size_t n;
-    bool out;
-};
-
-// Outputs may overlap nothing; inputs may overlap each other.  Sorted by
-// start, a range overlaps an earlier one exactly when it starts before the
-// largest end seen so far (of any range, for an output; of the outputs, for
-// an input).
-int check_overlaps(std::vector<Range>& r)
-{
-    std::sort(r.begin(), r.end(), [](const Range& a, const Range& b) { return a.p < b.p; });
-    uintptr_t end_any = 0, end_out = 0;
-    for (const Range& x : r) {
-        if (x.out ? x.p < end_any : x.p < end_out)
-            return fail(ROI_E_INVAL, "an output overlaps another input or output");
-        end_any = std::max(end_any, x.p + x.n);
-        if (x.out) end_out = std::max(end_out, x.p + x.n);
-    }
-    return ROI_OK;
-}
-
-void add_range(std::vector<Range>& r, const void* p, size_t n, bool out)
-{
-    if (p && n) r.push_back({(uintptr_t)p, n, out});
-}
 
 // Blocks one piece of `ngroups` groups needs in a launch.
 int64_t blocks_for(int64_t ngroups, int m, bool fwd)

@@ -34,6 +34,7 @@ def test_exports_every_declared_symbol(L):
             "roi_gumbel_from_words", "roi_fast_noise_from_words",
             "roi_mask_fwd_grouped", "roi_mask_fwd_soft_grouped", "roi_mask_bwd_grouped",
             "roi_mask_bwd_adamw", "roi_mask_bwd_adamw_grouped", "roi_mask_export",
+            "roi_cat_num_candidates", "roi_cat_mask_fwd", "roi_cat_mask_bwd",
             "roi_anneal", "roi_status_string", "roi_last_error", "roi_abi_version"} <= set(names)
     for name in names:
         assert hasattr(L, name), name
@@ -283,6 +284,43 @@ def test_export_rejects_before_launch(L, kw, status):
 
 def test_export_empty_is_a_no_op(L):
     assert export(L, rows=0, logits=None, W=None, Wm=None, vals=None, idx=FAKE) == roi.ROI_OK
+
+
+def test_cat_candidates_and_rejections(L):
+    import math as _m
+    for m in (4, 8):
+        for n in range(1, m + 1):
+            assert L.roi_cat_num_candidates(n, m) == _m.comb(m, n)
+    assert L.roi_cat_num_candidates(2, 16) == -1 and L.roi_cat_num_candidates(0, 4) == -1
+
+    def fwd(**kw):
+        a = dict(W=FAKE, al=FAKE + GB, rows=4, cols=8, n=2, m=4, tau=1.0, lam=1.0, off=0,
+                 Wm=FAKE + 2 * GB, S=None, ch=None)
+        a.update(kw)
+        return L.roi_cat_mask_fwd(a["W"], a["al"], a["rows"], a["cols"], a["n"], a["m"],
+                                  a["tau"], a["lam"], 0, 0, a["off"], a["Wm"], a["S"], a["ch"],
+                                  None)
+
+    def bwd(**kw):
+        a = dict(G=FAKE, W=FAKE + GB, al=FAKE + 2 * GB, rows=4, cols=8, n=2, m=4, tau=1.0,
+                 lam=1.0, off=0, d=FAKE + 3 * GB)
+        a.update(kw)
+        return L.roi_cat_mask_bwd(a["G"], a["W"], a["al"], a["rows"], a["cols"], a["n"], a["m"],
+                                  a["tau"], a["lam"], 0, 0, a["off"], a["d"], None)
+
+    for f, kw, st in [
+        (fwd, dict(m=16, n=2, cols=16), roi.ROI_E_UNSUPPORTED),
+        (fwd, dict(n=5), roi.ROI_E_INVAL), (fwd, dict(cols=6), roi.ROI_E_INVAL),
+        (fwd, dict(tau=0.0), roi.ROI_E_INVAL), (fwd, dict(lam=math.nan), roi.ROI_E_INVAL),
+        (fwd, dict(Wm=None), roi.ROI_E_INVAL), (fwd, dict(al=FAKE + GB + 8), roi.ROI_E_INVAL),
+        (fwd, dict(Wm=FAKE + GB + 16), roi.ROI_E_INVAL),        # overlaps the logits
+        (fwd, dict(off=2 ** 64 - 4), roi.ROI_E_INVAL),          # noise index overflow
+        (bwd, dict(d=None), roi.ROI_E_INVAL), (bwd, dict(d=FAKE + 2 * GB + 16), roi.ROI_E_INVAL),
+        (bwd, dict(m=32, n=2, cols=32), roi.ROI_E_UNSUPPORTED), (bwd, dict(rows=-1), roi.ROI_E_INVAL),
+    ]:
+        assert f(**kw) == st, kw
+        assert L.roi_last_error()
+    assert fwd(rows=0, W=None, al=None, Wm=None) == roi.ROI_OK
 
 
 def test_empty_input_is_a_no_op(L):

@@ -537,6 +537,75 @@ def test_export_full_7b_stack(dev):
     torch.cuda.empty_cache()
 
 
+# --------------------------------------------------------------------------- categorical sampler
+CAT = [(37, 36, 2, 4, 1.0, 1.0, 0), (64, 96, 2, 4, 0.3, 0.6, 5), (33, 64, 1, 4, 0.7, 1.0, 3),
+       (33, 64, 3, 4, 1.3, 1.0, 1), (21, 64, 4, 4, 1.0, 1.0, 0), (61, 88, 2, 8, 0.5, 1.0, 7),
+       (61, 88, 4, 8, 1.0, 2.0, 2 ** 33 + 5), (25, 64, 1, 8, 0.4, 1.0, 11),
+       (25, 64, 7, 8, 1.0, 1.0, 0), (19, 96, 3, 8, 0.8, 1.0, 2 ** 40)]
+
+
+@pytest.mark.parametrize("case", CAT, ids=lambda c: "x".join(map(str, c[:4])))
+def test_cat_sampler_against_oracle(dev, case):
+    """The categorical sampler: chosen candidates and masked weights bit-exact
+    (with and without the soft mask), S and dL/dalpha within the float
+    tolerance, against the oracle; large group offsets exercise Philox block
+    indices above 2^32."""
+    import torch
+    rows, cols, n, m, tau, lam, goff = case
+    C = roi.cat_num_candidates(n, m)
+    say(f"cat {rows}x{cols} {n}:{m} C={C} tau={tau} lam={lam} goff={goff}")
+    W, _, G = wl.small_case(rows, cols, rows + 3 * cols + n)
+    gen = torch.Generator(device="cpu").manual_seed(n * 100 + m)
+    A = torch.randn(rows * cols // m, C, generator=gen)
+    W, G, A = W.to(dev), G.to(dev), A.to(dev)
+    Wm, S, ch = roi.cat_mask_fwd(W, A, n, m, tau, lam, 9, 4, goff, want_soft=True)
+    Wm2, _, ch2 = roi.cat_mask_fwd(W, A, n, m, tau, lam, 9, 4, goff)
+    d = roi.cat_mask_bwd(G, W, A, n, m, tau, lam, 9, 4, goff)
+    torch.cuda.synchronize()
+    tau32, lam32 = float(np.float32(tau)), float(np.float32(lam))
+    Wm_o, S_o, ch_o = oracle.cat_fwd(bf16_bits(W), f32(A), n, m, tau32, lam32, 9, 4, goff)
+    d_o = oracle.cat_bwd(bf16_bits(G), bf16_bits(W), f32(A), n, m, tau32, lam32, 9, 4, goff)
+    for a_, b_ in ((ch, ch2), (Wm, Wm2)):
+        assert torch.equal(a_, b_)
+    assert np.array_equal(ch.cpu().numpy(), ch_o), "chosen candidates differ"
+    assert np.array_equal(bf16_bits(Wm).reshape(-1), Wm_o), "masked weights differ"
+    assert_close(f32(S), S_o, "categorical soft mask")
+    assert_close(f32(d), d_o, "dL/dalpha")
+
+
+@pytest.mark.parametrize("n,m", [(2, 4), (4, 8), (2, 8)])
+def test_cat_ties_and_near_ties(dev, n, m):
+    """Logits built from the oracle's noise so that candidate keys tie exactly
+    or nearly: the choice must still be the exact keys' (lowest candidate on a
+    tie), with the fast comparison's fallback exercised."""
+    import torch
+    rows, cols = 32, 64
+    Gn = rows * cols // m
+    C = roi.cat_num_candidates(n, m)
+    B = (C + 3) // 4
+    say(f"cat near ties {n}:{m}")
+    # noise of every candidate: element 4 B Q + c
+    Q = np.arange(Gn, dtype=np.uint64)
+    elems = (4 * B * Q[:, None] + np.arange(C, dtype=np.uint64)[None, :]).reshape(-1)
+    g = np.array([oracle.keys(np.zeros(1, np.float32), 1.0, 3, 6, int(e))[0] for e in elems],
+                 dtype=np.float64).reshape(Gn, C)
+    rng = np.random.default_rng(C)
+    steps = np.array([0.0, 0.0, 1e-7, -3e-7, 2e-6, 1.5e-5, -2.5e-5, 4e-5, 1e-3, 1.0])
+    target = rng.normal(0, 1, (Gn, 1)) + rng.choice(steps, (Gn, C))
+    target[::4] = rng.choice(steps, (Gn, C))[::4]           # around 0: exact ties when step 0
+    A = (target - g).astype(np.float32)
+    A[::4][target[::4] == 0.0] = (-g[::4][target[::4] == 0.0]).astype(np.float32)
+    W = (torch.randn(rows, cols, generator=torch.Generator().manual_seed(1)) + 3).to(torch.bfloat16)
+    W, At = W.to(dev), torch.from_numpy(A).to(dev)
+    Wm, _, ch = roi.cat_mask_fwd(W, At, n, m, 1.0, 1.0, 3, 6, 0)
+    Wm_s, _, ch_s = roi.cat_mask_fwd(W, At, n, m, 1.0, 1.0, 3, 6, 0, want_soft=True)
+    torch.cuda.synchronize()
+    Wm_o, _, ch_o = oracle.cat_fwd(bf16_bits(W), A, n, m, 1.0, 1.0, 3, 6, 0, want_soft=False)
+    assert np.array_equal(ch.cpu().numpy(), ch_o) and np.array_equal(ch_s.cpu().numpy(), ch_o)
+    assert np.array_equal(bf16_bits(Wm).reshape(-1), Wm_o)
+    assert np.array_equal(bf16_bits(Wm_s).reshape(-1), Wm_o)
+
+
 def test_every_output_written_and_deterministic(dev):
     import torch
     W, L, G = wl.small_case(333, 64, 1, device=dev)
