@@ -547,11 +547,11 @@ FwdFn select_fwd(int m, int n, bool s, bool i, bool l)
     return select_wide_fwd(m, n);
 }
 
-BwdFn select_bwd(int m, int n, bool l, bool adam)
+BwdFn select_bwd(int m, int n, bool l, bool adam, bool tau_one)
 {
     if (m == 4) return bwd_for_n<4>(n, l, adam, std::make_integer_sequence<int, 4>{});
     if (m == 8) return bwd_for_n<8>(n, l, adam, std::make_integer_sequence<int, 8>{});
-    return select_wide_bwd(m, n, adam);
+    return select_wide_bwd(m, n, adam, tau_one);
 }
 
 } // namespace
@@ -778,7 +778,7 @@ int mask_bwd_core(const char* what, const BwdDesc* t, int count, int n, int m, f
     }
     if (!any) return ok();
     if (int st = check_overlaps(ranges)) return st;
-    BwdFn fn = select_bwd(m, n, lambda == 1.0f, adam);
+    BwdFn fn = select_bwd(m, n, lambda == 1.0f, adam, tau == 1.0f);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     Launcher<BwdBatch, BwdPiece, BwdFn> L{};
     L.fn = fn;

@@ -64,6 +64,25 @@ __device__ __forceinline__ float max4(const float (&x)[4])
     return fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
 }
 
+template <int L>
+__device__ __forceinline__ float group_min(float v)
+{
+    v = fminf(v, lane_xor<1>(v));
+    if constexpr (L >= 4) v = fminf(v, lane_xor<2>(v));
+    if constexpr (L >= 8) v = fminf(v, lane_xor<4>(v));
+    return v;
+}
+
+__device__ __forceinline__ float min4(const float (&x)[4])
+{
+    return fminf(fminf(x[0], x[1]), fminf(x[2], x[3]));
+}
+
+// Widest key range (in the scaled log2 units of b) for which the exp-domain
+// recursion keeps every mu and omega a normal fp32 number with full precision
+// over 32 steps: exp2(-56) / 32 shrinks by at most 2 per step.
+constexpr float kExpDomainRange = 56.0f;
+
 // Adds, for lane distances D..L-1, how many entries of lane (lane ^ D) beat
 // each of this lane's entries (ties go to the lower index).
 template <int L, int D>
@@ -107,7 +126,12 @@ __device__ __forceinline__ void wide_rank(const float (&k)[4], int part, int (&r
 
 // Relaxation over the group (§3.2 recursion, Algorithm 1), four entries per
 // lane; see relax_forward in relax.hpp for the arithmetic.
-template <int L, int N, bool kKeep>
+// With kTauOne (tau = 1) the update alpha += log(max(omega, FLT_MIN)) is
+// carried out on the exponentials instead, e <- mu * max(omega, FLT_MIN) (the
+// same recursion, without a log, an exp and a maximum per step), whenever every
+// group of the wave spans less than kExpDomainRange; other waves take the
+// log-domain loop.
+template <int L, int N, bool kKeep, bool kTauOne = false>
 __device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], float key_scale,
                                                    float inv_tau, bool want_s, float (&S)[4],
                                                    StepRec<4> (&rec)[N])
@@ -119,6 +143,33 @@ __device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], floa
     for (int e = 0; e < 4; ++e) {
         b[e] = (kappa[e] - kmax) * c;
         S[e] = 0.0f;
+    }
+    if constexpr (kTauOne) {
+        const float span = (kmax - group_min<L>(min4(kappa))) * c;
+        if (__all(span < kExpDomainRange)) { // uniform over the wave
+            float ex[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) ex[e] = __builtin_amdgcn_exp2f(b[e]);
+#pragma unroll
+            for (int k = 0; k < N; ++k) {
+                float others[4], t;
+                sums_but_one<4>(ex, others, t);
+                const float ext = sum_other_lanes<L>(t);
+                const float inv_total = __builtin_amdgcn_rcpf(t + ext);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float mu = ex[e] * inv_total;
+                    const float om = (others[e] + ext) * inv_total;
+                    if (want_s) S[e] += mu;
+                    if (kKeep) {
+                        rec[k].mu[e] = mu;
+                        rec[k].om[e] = om;
+                    }
+                    if (k + 1 < N) ex[e] = mu * fmaxf(om, kFltMin);
+                }
+            }
+            return;
+        }
     }
 #pragma unroll
     for (int k = 0; k < N; ++k) {
@@ -145,8 +196,9 @@ __device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], floa
     }
 }
 
-// Reverse sweep over the group; see relax_backward in relax.hpp.
-template <int L, int N>
+// Reverse sweep over the group; see relax_backward in relax.hpp.  With
+// kTauOne, keep = 1 - mu / tau is omega itself and mu / tau is mu.
+template <int L, int N, bool kTauOne = false>
 __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
                                                     const float (&sbar)[4], float tau,
                                                     float inv_tau, float (&abar)[4])
@@ -178,12 +230,13 @@ __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
             const float inner = __builtin_fmaf(om, sbar[e], -(q[e] + ext));
             float carry = 0.0f;
             if (has_next) {
-                float keep = mu < 0.5f ? __builtin_fmaf(-mu, inv_tau, 1.0f)
-                                       : __builtin_fmaf(om, inv_tau, keep0);
+                float keep = kTauOne ? om
+                                     : (mu < 0.5f ? __builtin_fmaf(-mu, inv_tau, 1.0f)
+                                                  : __builtin_fmaf(om, inv_tau, keep0));
                 keep = (om >= kFltMin) ? keep : 1.0f;
                 carry = abar[e] * keep;
             }
-            abar[e] = __builtin_fmaf(mu * inv_tau, inner, carry);
+            abar[e] = __builtin_fmaf(kTauOne ? mu : mu * inv_tau, inner, carry);
         }
     }
 }
@@ -259,7 +312,7 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
 
 // Backward; with kAdam the AdamW step on the logits is fused in (as in the
 // per-lane kernels).
-template <int M, int N, bool kAdam>
+template <int M, int N, bool kAdam, bool kTauOne = false>
 __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
 {
     constexpr int L = M / 4;
@@ -293,9 +346,10 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
             bf16_bits_to_float(gv.y >> 16) * bf16_bits_to_float(wv.y >> 16)};
         StepRec<4> rec[N];
         float S_unused[4];
-        wide_relax_forward<L, N, true>(kappa, a.inv_tau, a.inv_tau, false, S_unused, rec);
+        wide_relax_forward<L, N, true, kTauOne>(kappa, a.inv_tau, a.inv_tau, false, S_unused,
+                                                rec);
         float abar[4];
-        wide_relax_backward<L, N>(rec, sbar, a.tau, a.inv_tau, abar);
+        wide_relax_backward<L, N, kTauOne>(rec, sbar, a.tau, a.inv_tau, abar);
         // dL/dphi = dL/dkappa / lambda (the product is exact for lambda = 1)
         const float grad[4] = {abar[0] * a.inv_lambda, abar[1] * a.inv_lambda,
                                abar[2] * a.inv_lambda, abar[3] * a.inv_lambda};
@@ -320,10 +374,13 @@ FwdFn wide_fwd_for_n(int n, std::integer_sequence<int, Ns...>)
 }
 
 template <int M, int... Ns>
-BwdFn wide_bwd_for_n(int n, bool adam, std::integer_sequence<int, Ns...>)
+BwdFn wide_bwd_for_n(int n, bool adam, bool tau_one, std::integer_sequence<int, Ns...>)
 {
     BwdFn f = nullptr;
-    ((n == Ns + 1 ? (f = adam ? bwd_wide_kernel<M, Ns + 1, true> : bwd_wide_kernel<M, Ns + 1, false>,
+    ((n == Ns + 1 ? (f = adam ? (tau_one ? bwd_wide_kernel<M, Ns + 1, true, true>
+                                         : bwd_wide_kernel<M, Ns + 1, true, false>)
+                              : (tau_one ? bwd_wide_kernel<M, Ns + 1, false, true>
+                                         : bwd_wide_kernel<M, Ns + 1, false, false>),
                      0)
                   : 0),
      ...);
@@ -339,10 +396,10 @@ FwdFn select_wide_fwd(int m, int n)
     return nullptr;
 }
 
-BwdFn select_wide_bwd(int m, int n, bool adam)
+BwdFn select_wide_bwd(int m, int n, bool adam, bool tau_one)
 {
-    if (m == 16) return wide_bwd_for_n<16>(n, adam, std::make_integer_sequence<int, 16>{});
-    if (m == 32) return wide_bwd_for_n<32>(n, adam, std::make_integer_sequence<int, 32>{});
+    if (m == 16) return wide_bwd_for_n<16>(n, adam, tau_one, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_bwd_for_n<32>(n, adam, tau_one, std::make_integer_sequence<int, 32>{});
     return nullptr;
 }
 
