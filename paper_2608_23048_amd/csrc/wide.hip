@@ -127,12 +127,16 @@ __device__ __forceinline__ void wide_rank(const float (&k)[4], int part, int (&r
 // Relaxation over the group (§3.2 recursion, Algorithm 1), four entries per
 // lane; see relax_forward in relax.hpp for the arithmetic.
 // With kTauOne (tau = 1) the update alpha += log(max(omega, FLT_MIN)) is
-// carried out on the exponentials instead, e <- mu * max(omega, FLT_MIN) (the
-// same recursion, without a log, an exp and a maximum per step), whenever every
-// group of the wave spans less than kExpDomainRange; other waves take the
-// log-domain loop.
+// carried out on the exponentials instead, e <- mu * omega (the same
+// recursion, without a log, an exp and a maximum per step), whenever every
+// group of the wave spans less than kExpDomainRange (2^-56).  Then every e
+// starts at >= 2^-56, the first mu and omega are >= 2^-61, and a step loses at
+// most a factor 2 (max(mu, omega) >= 1/2, so mu * omega >= min(mu, omega) / 2):
+// after 32 steps everything is still >= 2^-92, so the FLT_MIN floor is never
+// reached.  Returns true when the wave took this path (uniform over the wave);
+// other waves take the log-domain loop.
 template <int L, int N, bool kKeep, bool kTauOne = false>
-__device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], float key_scale,
+__device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], float key_scale,
                                                    float inv_tau, bool want_s, float (&S)[4],
                                                    StepRec<4> (&rec)[N])
 {
@@ -165,10 +169,10 @@ __device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], floa
                         rec[k].mu[e] = mu;
                         rec[k].om[e] = om;
                     }
-                    if (k + 1 < N) ex[e] = mu * fmaxf(om, kFltMin);
+                    if (k + 1 < N) ex[e] = mu * om;
                 }
             }
-            return;
+            return true;
         }
     }
 #pragma unroll
@@ -194,11 +198,13 @@ __device__ __forceinline__ void wide_relax_forward(const float (&kappa)[4], floa
                 b[e] = __builtin_fmaf(__builtin_amdgcn_logf(fmaxf(om, kFltMin)), inv_tau, b[e]);
         }
     }
+    return false;
 }
 
 // Reverse sweep over the group; see relax_backward in relax.hpp.  With
-// kTauOne, keep = 1 - mu / tau is omega itself and mu / tau is mu.
-template <int L, int N, bool kTauOne = false>
+// kTauOne, keep = 1 - mu / tau is omega itself and mu / tau is mu; with
+// kNoFloor (the forward never reached the floor) the floor's selects go.
+template <int L, int N, bool kTauOne = false, bool kNoFloor = false>
 __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
                                                     const float (&sbar)[4], float tau,
                                                     float inv_tau, float (&abar)[4])
@@ -216,7 +222,7 @@ __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
             if (has_next) {
                 const float om = rec[k].om[e];
                 const float r = abar[e] * __builtin_amdgcn_rcpf(om);
-                mubar = (om >= kFltMin) ? mubar - r : mubar;
+                mubar = (kNoFloor || om >= kFltMin) ? mubar - r : mubar;
             }
             t[e] = rec[k].mu[e] * mubar;
         }
@@ -233,7 +239,7 @@ __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
                 float keep = kTauOne ? om
                                      : (mu < 0.5f ? __builtin_fmaf(-mu, inv_tau, 1.0f)
                                                   : __builtin_fmaf(om, inv_tau, keep0));
-                keep = (om >= kFltMin) ? keep : 1.0f;
+                keep = (kNoFloor || om >= kFltMin) ? keep : 1.0f;
                 carry = abar[e] * keep;
             }
             abar[e] = __builtin_fmaf(kTauOne ? mu : mu * inv_tau, inner, carry);
@@ -346,10 +352,15 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
             bf16_bits_to_float(gv.y >> 16) * bf16_bits_to_float(wv.y >> 16)};
         StepRec<4> rec[N];
         float S_unused[4];
-        wide_relax_forward<L, N, true, kTauOne>(kappa, a.inv_tau, a.inv_tau, false, S_unused,
-                                                rec);
+        const bool no_floor = wide_relax_forward<L, N, true, kTauOne>(
+            kappa, a.inv_tau, a.inv_tau, false, S_unused, rec);
         float abar[4];
-        wide_relax_backward<L, N, kTauOne>(rec, sbar, a.tau, a.inv_tau, abar);
+        // A second, floor-free copy of the sweep pays for itself at m = 16; at
+        // m = 32 its registers would cost a wave per SIMD.
+        if (kTauOne && L <= 4 && no_floor) // uniform over the wave
+            wide_relax_backward<L, N, kTauOne, L <= 4>(rec, sbar, a.tau, a.inv_tau, abar);
+        else
+            wide_relax_backward<L, N, kTauOne, false>(rec, sbar, a.tau, a.inv_tau, abar);
         // dL/dphi = dL/dkappa / lambda (the product is exact for lambda = 1)
         const float grad[4] = {abar[0] * a.inv_lambda, abar[1] * a.inv_lambda,
                                abar[2] * a.inv_lambda, abar[3] * a.inv_lambda};
