@@ -124,6 +124,54 @@ __device__ __forceinline__ void wide_rank(const float (&k)[4], int part, int (&r
     rank_against_lane<L, 1>(k, part, rank);
 }
 
+// The same ranks from the hardware-log keys (noise.hpp): every comparison of
+// this lane's entries is decided by the sign of d = other - own, and `sep`
+// stays true only if every |d| exceeds the margin of two keys' errors (then
+// no two keys tie and each sign is the exact keys').
+template <int L, int D>
+__device__ __forceinline__ void rank_against_lane_fast(const float (&k)[4], float margin,
+                                                       int (&rank)[4], bool& sep)
+{
+    if constexpr (D < L) {
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = lane_xor<D>(k[e]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+#pragma unroll
+            for (int f = 0; f < 4; ++f) {
+                const float d = o[f] - k[e];
+                sep &= fabsf(d) > margin;
+                rank[e] += d > 0.0f ? 1 : 0;
+            }
+        }
+        rank_against_lane_fast<L, D + 1>(k, margin, rank, sep);
+    }
+}
+
+template <int L>
+__device__ __forceinline__ bool wide_rank_fast(const float (&k)[4], int (&rank)[4])
+{
+    float big = fmaxf(fmaxf(fabsf(k[0]), fabsf(k[1])), fmaxf(fabsf(k[2]), fabsf(k[3])));
+    big = group_max<L>(big);
+    const float margin = __builtin_fmaf(big, 0x1p-20f, kFastPairMargin);
+    bool sep = true;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) rank[e] = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int j = i + 1; j < 4; ++j) {
+            const float d = k[i] - k[j];
+            sep &= fabsf(d) > margin;
+            rank[j] += d > 0.0f ? 1 : 0;
+            rank[i] += d > 0.0f ? 0 : 1;
+        }
+    }
+    rank_against_lane_fast<L, 1>(k, margin, rank, sep);
+    return sep;
+}
+
 // Relaxation over the group (§3.2 recursion, Algorithm 1), four entries per
 // lane; see relax_forward in relax.hpp for the arithmetic.
 // With kTauOne (tau = 1) the update alpha += log(max(omega, FLT_MIN)) is
@@ -281,9 +329,24 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
         const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
         const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
         float kappa[4];
-        wide_keys(phi, pc.block0 + (uint32_t)slot, key, a.lambda, tab, kappa);
         int rank[4];
-        wide_rank<L>(kappa, part, rank);
+        const bool relax = pc.S || a.soft; // uniform over the launch
+        bool decided = false;
+        if (!relax) {
+            // Comparisons only: the hardware-log keys decide when every pair of
+            // every group in the wave is further apart than the margin (else
+            // the whole wave takes the exact keys: the ranks are cross-lane).
+            const uint4 x = philox_block(pc.block0 + (uint32_t)slot, key);
+            const float kf[4] = {fast_key_log2(phi[0], a.key_c, x.x),
+                                 fast_key_log2(phi[1], a.key_c, x.y),
+                                 fast_key_log2(phi[2], a.key_c, x.z),
+                                 fast_key_log2(phi[3], a.key_c, x.w)};
+            decided = __all(wide_rank_fast<L>(kf, rank));
+        }
+        if (!decided) {
+            wide_keys(phi, pc.block0 + (uint32_t)slot, key, a.lambda, tab, kappa);
+            wide_rank<L>(kappa, part, rank);
+        }
         if (!a.soft) {
             const uint32_t m01 = (rank[0] < N ? 0x0000FFFFu : 0u) | (rank[1] < N ? 0xFFFF0000u : 0u);
             const uint32_t m23 = (rank[2] < N ? 0x0000FFFFu : 0u) | (rank[3] < N ? 0xFFFF0000u : 0u);
