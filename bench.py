@@ -84,9 +84,14 @@ def pmc_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes
         return vals
 
     def pick(vals, key):
+        # mean over the full-size dispatches of the kernel (within a factor 2 of
+        # the largest), so that smaller launches of the same kernel do not count
         hits = [v for k, v in vals.items() if key in k]
         flat = [x for v in hits for x in v]
-        return sum(flat) / len(flat) if flat else None
+        if not flat:
+            return None
+        big = [x for x in flat if x >= 0.5 * max(flat)]
+        return sum(big) / len(big)
 
     cf = per_kernel(copy_fetch_csv, "FETCH_SIZE")
     cw = per_kernel(copy_write_csv, "WRITE_SIZE")
@@ -390,6 +395,28 @@ def run_cat(args) -> int:
     return 0
 
 
+def grouped_timing(grouped_step, steps, work):
+    """Times `steps` steps through the grouped calls (after one warm-up)."""
+    import torch
+    grouped_step(1000)
+    gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    g0 = time.perf_counter()
+    for t in range(steps):
+        grouped_step(t, gev[t])
+    torch.cuda.synchronize()
+    g_elapsed = time.perf_counter() - g0
+    g_fwd = sum(e[0].elapsed_time(e[1]) for e in gev) / len(gev)
+    g_bwd = sum(e[1].elapsed_time(e[2]) for e in gev) / len(gev)
+    per_launch = 16  # pieces per grid (common.hpp kMaxPieces)
+    grouped = {"ms_per_step": g_elapsed * 1e3 / steps, "fwd_ms": g_fwd, "bwd_ms": g_bwd,
+               "descriptors": len(work.tensors),
+               "launches_per_step": 2 * -(-len(work.tensors) // per_launch)}
+    print(f"# grouped calls over {len(work.tensors)} tensors: {grouped['ms_per_step']:.3f} "
+          f"ms/step, fwd {g_fwd:.3f} ms, bwd {g_bwd:.3f} ms", file=sys.stderr, flush=True)
+    return grouped
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -397,6 +424,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="qwen2.5-7b-stack-2:4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-grouped", action="store_true",
+                    help="skip the secondary timing through the grouped calls")
     ap.add_argument("--pattern", default=None, help="n:m for --mode cat (default: the workload's)")
     ap.add_argument("--mode", choices=("st", "adamw", "export", "cat"), default="st",
                     help="st: forward + backward (the headline); adamw: forward + backward "
@@ -522,22 +551,9 @@ def main() -> int:
         if ev is not None:
             ev[2].record()
 
-    grouped_step(1000)
-    gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    g0 = time.perf_counter()
-    for t in range(args.steps):
-        grouped_step(t, gev[t])
-    torch.cuda.synchronize()
-    g_elapsed = time.perf_counter() - g0
-    g_fwd = sum(e[0].elapsed_time(e[1]) for e in gev) / len(gev)
-    g_bwd = sum(e[1].elapsed_time(e[2]) for e in gev) / len(gev)
-    per_launch = 16  # pieces per grid (common.hpp kMaxPieces)
-    grouped = {"ms_per_step": g_elapsed * 1e3 / args.steps, "fwd_ms": g_fwd, "bwd_ms": g_bwd,
-               "descriptors": len(work.tensors),
-               "launches_per_step": 2 * -(-len(work.tensors) // per_launch)}
-    print(f"# grouped calls over {len(work.tensors)} tensors: {grouped['ms_per_step']:.3f} "
-          f"ms/step, fwd {g_fwd:.3f} ms, bwd {g_bwd:.3f} ms", file=sys.stderr, flush=True)
+    grouped = None
+    if not args.no_grouped:
+        grouped = grouped_timing(grouped_step, args.steps, work)
 
     cpu = None
     if not args.no_cpu_baseline:
