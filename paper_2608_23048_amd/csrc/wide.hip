@@ -4,7 +4,7 @@
 // and one 8-byte bf16 load per lane), a group spread over L = m / 4 adjacent
 // lanes of one wave.  Group-wide maxima and "sum over the other lanes" use
 // cross-lane butterflies: DPP quad permutations for lane distances 1..3 and
-// ds_swizzle for distance 4.  Every group is whole inside a wave and either
+// the DPP half-row mirror for distances 4..7.  Every group is whole inside a wave and either
 // all its lanes are active or none is, so the butterflies never read a lane
 // outside the group.  Same arithmetic as the per-lane kernels for m = 4 and 8:
 // the noise of noise.hpp, ranks with ties to the lower index, and the
@@ -20,14 +20,17 @@
 namespace roi {
 namespace {
 
-// Value held by lane (lane ^ D) of the same group (D < 8).
+// Value held by lane (lane ^ D) of the same group (D < 8), with DPP only:
+// quad permutations for D < 4; for D >= 4, the half-row mirror (lane i of an
+// 8-lane half to lane 7 - i, i.e. xor 7) followed by the quad permutation of
+// D ^ 7.
 template <int D>
 __device__ __forceinline__ float lane_xor(float v)
 {
     static_assert(D > 0 && D < 8, "lane distance");
     int x = __float_as_int(v);
-    if constexpr ((D & 4) != 0) x = __builtin_amdgcn_ds_swizzle(x, 0x101F); // xor 4 within 32 lanes
-    constexpr int lo = D & 3;
+    if constexpr ((D & 4) != 0) x = __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, true);
+    constexpr int lo = ((D & 4) != 0 ? (D ^ 7) : D) & 3;
     if constexpr (lo == 1) x = __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, true); // [1,0,3,2]
     if constexpr (lo == 2) x = __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, true); // [2,3,0,1]
     if constexpr (lo == 3) x = __builtin_amdgcn_update_dpp(0, x, 0x1B, 0xF, 0xF, true); // [3,2,1,0]
