@@ -115,6 +115,34 @@ __device__ __forceinline__ void store_cat(float* p, const float (&a)[C])
     }
 }
 
+// Threads per block: the tile of a block's logits (block * C floats) is staged
+// through LDS and must fit in 64 KB.
+constexpr int cat_block(int C) { return C > 64 ? 128 : 256; }
+// Groups with at least 8 logits (32 bytes) are staged: read per lane from
+// global memory, their 32-280-byte strides would touch up to 8x more cache
+// lines per load instruction than a contiguous 16-byte-per-lane stream.
+constexpr bool cat_staged(int C) { return C >= 8; }
+
+// Coalesced copies between global memory and a block's LDS tile, in 8-byte
+// chunks (every staged C is even, so a group's logits start 8-byte aligned).
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+
+template <int B>
+__device__ __forceinline__ void tile_in(const float* g, float* lds, int count)
+{
+    const f32x2v* src = reinterpret_cast<const f32x2v*>(g);
+    f32x2v* dst = reinterpret_cast<f32x2v*>(lds);
+    for (int i = threadIdx.x; i < count / 2; i += B) dst[i] = stream_load(src + i);
+}
+
+template <int B>
+__device__ __forceinline__ void tile_out(const float* lds, float* g, int count)
+{
+    const f32x2v* src = reinterpret_cast<const f32x2v*>(lds);
+    f32x2v* dst = reinterpret_cast<f32x2v*>(g);
+    for (int i = threadIdx.x; i < count / 2; i += B) stream_store(src[i], dst + i);
+}
+
 struct CatArgs {
     const uint16_t* W;
     const float* alpha;
@@ -179,17 +207,32 @@ __device__ __forceinline__ void cat_softmax(float (&k)[C], float scale)
 }
 
 template <int M, int N, bool kSoft>
-__global__ __launch_bounds__(kBlock) void cat_fwd_kernel(CatArgs a)
+__global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_fwd_kernel(CatArgs a)
 {
     constexpr int C = Candidates<M, N>::C;
+    constexpr int B = cat_block(C);
+    constexpr bool kStage = cat_staged(C);
     __shared__ float2 tab[kLogCells];
+    __shared__ float tile[kStage ? B * C : 2];
     fill_log_table(tab);
     __syncthreads();
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
+    // The loop bound is uniform over the block (the tile copies are cooperative).
+    for (int64_t base = (int64_t)blockIdx.x * B; base < a.ngroups; base += (int64_t)gridDim.x * B) {
+        const int here = (int)(a.ngroups - base < B ? a.ngroups - base : B);
+        const int64_t q = base + threadIdx.x;
         float alpha[C];
+        if constexpr (kStage) {
+            tile_in<B>(a.alpha + base * C, tile, here * C);
+            __syncthreads();
+            if ((int)threadIdx.x < here) {
+#pragma unroll
+                for (int c = 0; c < C; ++c) alpha[c] = tile[threadIdx.x * C + c];
+            }
+            __syncthreads(); // the tile is refilled next iteration
+        }
+        if ((int)threadIdx.x >= here) continue;
+        if constexpr (!kStage) load_cat_logits<C>(a.alpha + q * C, alpha);
         uint32_t w[M];
-        load_cat_logits<C>(a.alpha + q * C, alpha);
         load_bf16<M>(a.W + q * M, w);
         uint32_t x[C];
         cat_words<C>(a.group0 + (uint64_t)q, a.key, x);
@@ -260,14 +303,32 @@ __global__ __launch_bounds__(kBlock) void cat_fwd_kernel(CatArgs a)
 }
 
 template <int M, int N>
-__global__ __launch_bounds__(kBlock) void cat_bwd_kernel(CatArgs a)
+__global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_bwd_kernel(CatArgs a)
 {
     constexpr int C = Candidates<M, N>::C;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < a.ngroups; q += stride) {
+    constexpr int B = cat_block(C);
+    constexpr bool kStage = cat_staged(C);
+    __shared__ float tile[kStage ? B * C : 2];
+    // The loop bound is uniform over the block (the tile copies are cooperative).
+    for (int64_t base = (int64_t)blockIdx.x * B; base < a.ngroups; base += (int64_t)gridDim.x * B) {
+        const int here = (int)(a.ngroups - base < B ? a.ngroups - base : B);
+        const int64_t q = base + threadIdx.x;
+        const bool live = (int)threadIdx.x < here;
         float alpha[C];
+        if constexpr (kStage) {
+            tile_in<B>(a.alpha + base * C, tile, here * C);
+            __syncthreads();
+            if (live) {
+#pragma unroll
+                for (int c = 0; c < C; ++c) alpha[c] = tile[threadIdx.x * C + c];
+            }
+            __syncthreads(); // the gradients go into the same tile
+        } else if (live) {
+            load_cat_logits<C>(a.alpha + q * C, alpha);
+        }
+        float d[C];
+        if (live) {
         uint32_t w[M], g[M];
-        load_cat_logits<C>(a.alpha + q * C, alpha);
         load_bf16<M>(a.W + q * M, w);
         load_bf16<M>(a.G + q * M, g);
         uint32_t x[C];
@@ -291,10 +352,20 @@ __global__ __launch_bounds__(kBlock) void cat_bwd_kernel(CatArgs a)
             dot = __builtin_fmaf(y[c], acc, dot);
         }
         const float s = a.inv_tau * a.inv_lambda;
-        float d[C];
 #pragma unroll
         for (int c = 0; c < C; ++c) d[c] = y[c] * (ybar[c] - dot) * s;
-        store_cat<C>(a.dalpha + q * C, d);
+        }
+        if constexpr (kStage) {
+            if (live) {
+#pragma unroll
+                for (int c = 0; c < C; ++c) tile[threadIdx.x * C + c] = d[c];
+            }
+            __syncthreads();
+            tile_out<B>(tile, a.dalpha + base * C, here * C);
+            __syncthreads(); // before the next tile overwrites it
+        } else if (live) {
+            store_cat<C>(a.dalpha + q * C, d);
+        }
     }
 }
 
@@ -391,7 +462,9 @@ int cat_run(bool fwd, const uint16_t* W, const float* alpha, const uint16_t* G, 
     a.inv_lambda = (float)(1.0 / (double)lambda);
     a.inv_tau = (float)(1.0 / (double)tau);
     void* args[] = {&a};
-    if (hipLaunchKernel(fn, dim3(grid_for(ngroups)), dim3(kBlock), args, 0, stream) != hipSuccess)
+    const int block = cat_block(C);
+    if (hipLaunchKernel(fn, dim3(grid_for(ngroups, block)), dim3(block), args, 0, stream) !=
+        hipSuccess)
         return launch_status(what);
     return launch_status(what);
 }
