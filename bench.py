@@ -28,16 +28,20 @@ HBM_PEAK_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "roi_mask_qwen7b_stack_2of4_traffic.json")
 
 
+# The sources the benchmark's two kernels (fwd_lane_kernel, bwd_lane_kernel
+# for m = 4 and 8) are compiled from.
+KERNEL_SOURCES = ("roi.hip", "common.hpp", "noise.hpp", "relax.hpp", "host.hpp")
+
+
 def kernel_source_hash() -> str:
-    """Hash of the HIP sources: measured traffic is reported only for the
-    kernels it was measured on."""
+    """Hash of the sources of the measured kernels: measured traffic is
+    reported only while they are unchanged."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_23048_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".hpp", ".h")):
-            h.update(name.encode())
-            h.update(open(os.path.join(csrc, name), "rb").read())
+    for name in KERNEL_SOURCES:
+        h.update(name.encode())
+        h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()[:16]
 
 
