@@ -1,0 +1,66 @@
+"""bench.py's host-side contract (no GPU needed): more than one GPU is refused
+with a message, the traffic record matches its kernels' sources, and the
+counter summary keeps only full-size dispatches."""
+from __future__ import annotations
+
+import csv
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_traffic_record_matches_the_kernel_sources():
+    rec = json.load(open(bench.TRAFFIC_FILE))
+    assert rec["kernel_source_hash"] == bench.kernel_source_hash()
+    for k in ("fwd_lane_kernel", "bwd_lane_kernel"):
+        assert abs(rec["kernels"][k]["traffic_over_algorithmic"] - 1.0) < 1e-3
+
+
+def _counters(path, rows):
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for r in rows:
+            w.writerow(r)
+
+
+def test_pmc_summary_keeps_full_size_dispatches(tmp_path, monkeypatch):
+    """Two full-size dispatches and a small one of the same kernel: the small
+    one does not dilute the per-launch figure; the copy calibration scales
+    FETCH_SIZE by 2 when it reads half the bytes."""
+    numel, n, m = 1 << 20, 2, 4
+    bf, bb = bench.algorithmic_bytes(n, m)
+    f_full, w_full = bf * numel / 2 / 1024 * 0.75, bf * numel / 1024 * 0.25
+    rows_f = [{"Kernel_Name": "fwd_lane_kernel<4,2>", "Counter_Name": "FETCH_SIZE",
+               "Counter_Value": v} for v in (f_full, f_full, f_full / 50)]
+    rows_w = [{"Kernel_Name": "fwd_lane_kernel<4,2>", "Counter_Name": "WRITE_SIZE",
+               "Counter_Value": v} for v in (w_full, w_full, w_full / 50)]
+    copy = 1 << 30
+    _counters(tmp_path / "f.csv", rows_f)
+    _counters(tmp_path / "w.csv", rows_w)
+    _counters(tmp_path / "cf.csv", [{"Kernel_Name": "__amd_rocclr_copyBuffer",
+                                     "Counter_Name": "FETCH_SIZE", "Counter_Value": copy / 2048}])
+    _counters(tmp_path / "cw.csv", [{"Kernel_Name": "__amd_rocclr_copyBuffer",
+                                     "Counter_Name": "WRITE_SIZE", "Counter_Value": copy / 1024}])
+    out = tmp_path / "traffic.json"
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(out))
+    assert bench.pmc_summary(tmp_path / "f.csv", tmp_path / "w.csv", tmp_path / "cf.csv",
+                             tmp_path / "cw.csv", copy, numel, n, m) == 0
+    rec = json.load(open(out))
+    assert rec["fetch_scale"] == pytest.approx(2.0) and rec["write_scale"] == pytest.approx(1.0)
+    assert rec["kernels"]["fwd_lane_kernel"]["traffic_over_algorithmic"] == pytest.approx(1.0)
