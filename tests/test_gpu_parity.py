@@ -537,6 +537,35 @@ def test_export_full_7b_stack(dev):
     torch.cuda.empty_cache()
 
 
+SPARSE_MM = [(16, 64, 16), (64, 256, 32), (48, 640, 48), (128, 3584, 32)]
+
+
+@pytest.mark.parametrize("case", SPARSE_MM, ids=lambda c: "x".join(map(str, c)))
+def test_export_feeds_sparse_mfma(dev, case):
+    """The 2:4 export read as written by gfx950's sparse matrix core
+    (v_smfmac_f32_16x16x64_bf16): W_sparse X^T from the compressed values and
+    metadata equals the oracle's masked dense weights times X^T exactly
+    (small-integer values, so every fp32 sum is exact)."""
+    import torch
+    from tests import sparse_mfma
+    rows, cols, tokens = case
+    say(f"export -> sparse MFMA: W {rows}x{cols}, X {tokens}x{cols}")
+    rng = np.random.default_rng(rows * cols + tokens)
+    Wi = rng.integers(-8, 9, size=(rows, cols)).astype(np.float32)
+    Xi = rng.integers(-8, 9, size=(tokens, cols)).astype(np.float32)
+    W = torch.from_numpy(Wi).to(dev).to(torch.bfloat16)
+    X = torch.from_numpy(Xi).to(dev).to(torch.bfloat16)
+    L = torch.from_numpy(rng.standard_normal((rows, cols)).astype(np.float32)).to(dev)
+    _, vals, _, meta = roi.mask_export(L, W, 2, 4, want_dense=False, want_idx=False,
+                                       want_meta=True)
+    Y = sparse_mfma.matmul_2of4(vals, meta, X, rows, cols)
+    torch.cuda.synchronize()
+    Wm_o, _, _, _ = oracle.export(f32(L), bf16_bits(W), 2, 4)
+    Wd = (Wm_o.astype(np.uint32) << 16).view(np.float32).reshape(rows, cols).astype(np.float64)
+    ref = Wd @ Xi.astype(np.float64).T
+    assert np.array_equal(Y.cpu().numpy().astype(np.float64), ref)
+
+
 # --------------------------------------------------------------------------- categorical sampler
 CAT = [(37, 36, 2, 4, 1.0, 1.0, 0), (64, 96, 2, 4, 0.3, 0.6, 5), (33, 64, 1, 4, 0.7, 1.0, 3),
        (33, 64, 3, 4, 1.3, 1.0, 1), (21, 64, 4, 4, 1.0, 1.0, 0), (61, 88, 2, 8, 0.5, 1.0, 7),
