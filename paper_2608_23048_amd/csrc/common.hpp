@@ -41,6 +41,7 @@ struct FwdBatch {
     float lambda;
     float key_c; // fl(log2(e) / lambda): the scale of the hardware-log keys
     float inv_tau;
+    float exp_span; // key-span limit of the exp-domain relaxation (relax.hpp)
     int soft; // 1: W_masked = W (.) S (pure soft forward), 0: W (.) hard mask
 };
 
@@ -76,6 +77,7 @@ struct BwdBatch {
     float inv_lambda;
     float tau;
     float inv_tau;
+    float exp_span; // key-span limit of the exp-domain relaxation (relax.hpp)
     AdamStep adam;
 };
 

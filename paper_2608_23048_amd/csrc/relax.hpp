@@ -101,37 +101,51 @@ struct StepRec {
     float om[M]; // 1 - mu^(k), evaluated as the sum of the other entries over the total
 };
 
+// Keys scaled for the relaxation: b_j = kappa_j * key_scale, the softmax
+// argument alpha / tau in log2 units; bmax = max b.  Returns the span
+// (max - min) of b.  key_scale is log2(e) / tau for keys in natural units and
+// 1 / tau for keys already in log2 units (any common offset cancels).  The
+// keys are not shifted by their maximum here: each softmax subtracts the
+// largest b of its own step, so the entries that compete at a step are
+// compared without the rounding of a shift by an entry already selected
+// (which would cost about ulp(span) in every exponent).
+template <int M>
+__device__ __forceinline__ float scaled_keys(const float (&kappa)[M], float key_scale, float (&b)[M],
+                                             float& bmax)
+{
+    float kmax = kappa[0], kmin = kappa[0];
+#pragma unroll
+    for (int j = 1; j < M; ++j) {
+        kmax = fmaxf(kmax, kappa[j]);
+        kmin = fminf(kmin, kappa[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < M; ++j) b[j] = kappa[j] * key_scale;
+    bmax = kmax * key_scale; // = max b (rounding is monotone)
+    return (kmax - kmin) * key_scale;
+}
+
 // Relaxation (§3.2 recursion, Algorithm 1) in fp32:
 //   alpha^(1) = kappa; mu^(k) = softmax(alpha^(k) / tau);
 //   alpha^(k+1) = alpha^(k) + log(1 - mu^(k));  S = sum_k mu^(k).
-// Internally b = (alpha - max kappa) * log2(e) / tau, so the softmax is
+// Internally b = alpha * log2(e) / tau (scaled_keys), so the softmax is
 // exp2(b - max b) and the update is b += log2(1 - mu) / tau: the same values
-// with one multiply fewer per element and step.  Subtracting the group's
-// largest key first keeps the competing entries near 0, where fp32 is
-// densest.  1 - mu_j is evaluated as (sum of the other exponentials) / total,
-// which never cancels, and log(1 - mu) is floored at log(FLT_MIN).
-// key_scale turns key differences into b: log2(e) / tau for keys in natural
-// units, 1 / tau for keys already in log2 units (any common offset cancels).
+// with one multiply fewer per element and step.  1 - mu_j is evaluated as
+// (sum of the other exponentials) / total, which never cancels, and
+// log(1 - mu) is floored at log(FLT_MIN).
 template <int M, int N, bool kWantS, bool kKeep>
-__device__ __forceinline__ void relax_forward(const float (&kappa)[M], float key_scale,
-                                              float inv_tau, float (&S)[M], StepRec<M> (&rec)[N])
+__device__ __forceinline__ void relax_forward(float (&b)[M], float bmax0, float inv_tau,
+                                              float (&S)[M], StepRec<M> (&rec)[N])
 {
-    float kmax = kappa[0];
 #pragma unroll
-    for (int j = 1; j < M; ++j) kmax = fmaxf(kmax, kappa[j]);
-    const float c = key_scale;
-    float b[M];
-#pragma unroll
-    for (int j = 0; j < M; ++j) {
-        b[j] = (kappa[j] - kmax) * c;
+    for (int j = 0; j < M; ++j)
         if (kWantS) S[j] = 0.0f;
-    }
 #pragma unroll
     for (int k = 0; k < N; ++k) {
         float e[M];
-        if (k == 0) { // the largest b is exactly 0
+        if (k == 0) { // the largest b is known
 #pragma unroll
-            for (int j = 0; j < M; ++j) e[j] = __builtin_amdgcn_exp2f(b[j]);
+            for (int j = 0; j < M; ++j) e[j] = __builtin_amdgcn_exp2f(b[j] - bmax0);
         } else {
             float bmax = b[0];
 #pragma unroll
@@ -157,33 +171,106 @@ __device__ __forceinline__ void relax_forward(const float (&kappa)[M], float key
     }
 }
 
-// Reverse sweep of relax_forward: given sbar = dL/dS, returns dL/dkappa.
-// Chain rule through the recursion, with a = dL/dalpha^(k+1) (0 above the
-// last step) and omega = 1 - mu^(k):
-//   mubar_j = sbar_j - a_j / omega_j            (no a_j / omega_j where the floor was hit)
-//   dL/dalpha^(k)_j = a_j + (mu_j / tau) (mubar_j - sum_l mu_l mubar_l).
-// With 1 - mu_j = omega_j and omega_j mubar_j = omega_j sbar_j - a_j this is
-//   dL/dalpha^(k)_j = a_j keep_j + (mu_j / tau) (omega_j sbar_j - sum_{l != j} mu_l mubar_l),
-//   keep_j = 1 - mu_j / tau = (omega_j + tau - 1) / tau   (1 where the floor was hit),
-// the same form for every j, with no difference of two large numbers when
-// mu_j is close to 1 (the sum over l != j is built from prefix and suffix
-// sums).
-template <int M, int N>
-__device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const float (&sbar)[M],
-                                               float tau, float inv_tau, float (&abar)[M])
+// The same recursion on the exponentials.  With e proportional to
+// exp(alpha / tau), the update alpha += log(1 - mu) is e <- e * (1 - mu)^q,
+// q = 1 / tau; rescaled by the total this is e <- mu * omega^q: no maximum,
+// shift or floor per element and step, and for tau = 1 (kQ = 1) or 1/2
+// (kQ = 2) no log or exp either (a product of q + 1 factors).  Other
+// temperatures (kQ = 0) take omega^q = exp2(q log2 omega).
+//
+// When it agrees with relax_forward: call an entry "dominant" at a step where
+// its mu >= 1/2 (at most one entry per step).  An entry never dominant so far
+// has omega > 1/2, so each step multiplies its weight by at least 2^-q while
+// the total of the products never exceeds 1: after k steps its mu is at least
+// 2^-(span + log2 M + k q).  Before the last step at most N - 1 <= M - 1
+// entries have been dominant, so one such entry always exists, and the
+// dominant entry's omega (the sum of the others) is at least as large.  Hence,
+// for M <= 8, span + (N - 1) q <= kExpSpanLimit keeps every such mu and omega
+// above 2^-91: normal numbers far from underflow, and far above the FLT_MIN
+// floor of log(1 - mu), which is therefore never reached.  An entry that has
+// been dominant and falls below 2^-126 moves the total by less than 2^-35 of
+// itself, so the exp-domain and log-domain recursions agree to rounding.
+// Unlike the log-domain loop, this form keeps the first step's shift by the
+// largest key for good: each exponent b_j - bmax carries a rounding of about
+// 2^-24 |b_j - bmax| (with that of key_scale), a relative error of about
+// 4e-8 span in e_j.  span <= kExpSpanAccuracy keeps it near 1e-6.
+constexpr float kExpSpanLimit = 88.0f;
+constexpr float kExpSpanAccuracy = 32.0f;
+
+template <int kQ>
+__device__ __forceinline__ float pow_q(float om, float q)
 {
-    const float keep0 = (tau - 1.0f) * inv_tau;
+    if constexpr (kQ == 1) return om;
+    else if constexpr (kQ == 2) return om * om;
+    else return __builtin_amdgcn_exp2f(__builtin_amdgcn_logf(om) * q);
+}
+
+template <int M, int N, bool kWantS, bool kKeep, int kQ>
+__device__ __forceinline__ void relax_forward_exp(const float (&b)[M], float bmax, float q,
+                                                  float (&S)[M], StepRec<M> (&rec)[N])
+{
+    static_assert(kQ >= 0 && kQ <= 2, "exp-domain recursion: kQ");
+    float e[M];
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+        e[j] = __builtin_amdgcn_exp2f(b[j] - bmax);
+        if (kWantS) S[j] = 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        float others[M], total;
+        sums_but_one<M>(e, others, total);
+        const float inv_total = __builtin_amdgcn_rcpf(total);
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+            const float mu = e[j] * inv_total;
+            const float om = others[j] * inv_total;
+            if (kWantS) S[j] += mu;
+            if (kKeep) {
+                rec[k].mu[j] = mu;
+                rec[k].om[j] = om;
+            }
+            if (k + 1 < N) e[j] = mu * pow_q<kQ>(om, q);
+        }
+    }
+}
+
+// Reverse sweep of relax_forward / relax_forward_exp: given sbar = dL/dS,
+// returns dL/dkappa (in the units of the keys times 1/tau's scale, as the
+// caller's b).  Chain rule through the recursion, with a = dL/dalpha^(k+1)
+// (0 above the last step), omega = 1 - mu^(k),
+//   mubar_j = sbar_j - a_j / omega_j,
+//   dL/dalpha^(k)_j = a_j + (mu_j / tau) (mubar_j - sum_l mu_l mubar_l).
+// Since omega_j mubar_j = omega_j sbar_j - a_j, with
+// X_j = omega_j sbar_j - sum_{l != j} mu_l mubar_l this is
+//   dL/dalpha^(k)_j = a_j + (mu_j / tau) (X_j - a_j),
+// one form for every j, and the sum over l != j comes from prefix and suffix
+// sums (nothing cancels when mu_j is near 1).  The rounding of X_j - a_j is
+// relative to |a_j|, which is small exactly for an entry whose mu is near 1:
+// that entry is selected at this step, so its later weights, and with them
+// a_j, are negligible.
+// With kFloor, an entry whose 1 - mu fell below FLT_MIN at an updating step
+// had its log floored, so no derivative flows through it: mubar_j = sbar_j and
+// dL/dalpha^(k)_j = a_j + (mu_j / tau) X_j.  Without kFloor the caller has
+// ruled the floor out (the exp-domain form's span bound).
+template <int M, int N, bool kTauIsOne, bool kFloor>
+__device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const float (&sbar)[M],
+                                               float inv_tau, float (&abar)[M])
+{
 #pragma unroll
     for (int k = N - 1; k >= 0; --k) {
         const bool has_next = (k + 1 < N);
-        float t[M];
+        float t[M], a_in[M];
 #pragma unroll
         for (int j = 0; j < M; ++j) {
             float mubar = sbar[j];
+            a_in[j] = 0.0f;
             if (has_next) {
                 const float om = rec[k].om[j];
-                const float r = abar[j] * __builtin_amdgcn_rcpf(om);
-                mubar = (om >= kFltMin) ? mubar - r : mubar;
+                const bool live = !kFloor || om >= kFltMin;
+                const float rinv = live ? __builtin_amdgcn_rcpf(om) : 0.0f;
+                mubar = __builtin_fmaf(-abar[j], rinv, sbar[j]);
+                a_in[j] = live ? abar[j] : 0.0f;
             }
             t[j] = rec[k].mu[j] * mubar;
         }
@@ -191,20 +278,9 @@ __device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const
         sums_but_one<M>(t, q, unused);
 #pragma unroll
         for (int j = 0; j < M; ++j) {
-            const float om = rec[k].om[j];
-            const float inner = __builtin_fmaf(om, sbar[j], -q[j]);
-            const float m_t = rec[k].mu[j] * inv_tau;
-            float carry = 0.0f;
-            if (has_next) {
-                // keep = 1 - mu/tau, from mu while mu < 1/2 and from omega above (where
-                // 1 - mu would cancel); 1 where the floor was hit
-                const float mu = rec[k].mu[j];
-                float keep = mu < 0.5f ? __builtin_fmaf(-mu, inv_tau, 1.0f)
-                                       : __builtin_fmaf(om, inv_tau, keep0);
-                keep = (om >= kFltMin) ? keep : 1.0f;
-                carry = abar[j] * keep;
-            }
-            abar[j] = __builtin_fmaf(m_t, inner, carry);
+            const float x = __builtin_fmaf(rec[k].om[j], sbar[j], -q[j]);
+            const float m_t = kTauIsOne ? rec[k].mu[j] : rec[k].mu[j] * inv_tau;
+            abar[j] = has_next ? __builtin_fmaf(m_t, x - a_in[j], abar[j]) : m_t * x;
         }
     }
 }

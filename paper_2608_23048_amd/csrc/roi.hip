@@ -254,7 +254,13 @@ __device__ __forceinline__ void fast_keys(const float (&phi)[M], const uint32_t 
 // groups base + u * kLaneBlock + l, u < U, so every load and store instruction
 // of a wave is one contiguous span, and all of a lane's loads are issued
 // before its first group is computed (more bytes in flight per wave).
-template <int M, int N, bool kRelax, bool kWantIdx, bool kLambdaOne>
+//
+// The relaxation takes the exp-domain recursion in groups whose key spans
+// allow it, else the log-domain one (relax.hpp); kQ is 1 or 2 for tau = 1 or
+// 1/2 (powers by multiplication), else 0.  The choice is made per group, from
+// the group's own keys, so a group's outputs never depend on which groups
+// share its wave (any split of a tensor into calls gives the same bits).
+template <int M, int N, bool kRelax, bool kWantIdx, bool kLambdaOne, int kQ>
 __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
 {
     __shared__ float2 tab[kLogCells];
@@ -317,9 +323,13 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
                 if (kWantIdx) store_idx<M, N>(pc.idx + q * N, rank);
             }
             if (kRelax) {
-                float S[M];
+                float S[M], b[M], bmax;
                 StepRec<M> unused[N]; // not written when records are not kept
-                relax_forward<M, N, true, false>(kappa, kLog2e * a.inv_tau, a.inv_tau, S, unused);
+                const float span = scaled_keys<M>(kappa, kLog2e * a.inv_tau, b, bmax);
+                if (span <= a.exp_span)
+                    relax_forward_exp<M, N, true, false, kQ>(b, bmax, a.inv_tau, S, unused);
+                else
+                    relax_forward<M, N, true, false>(b, bmax, a.inv_tau, S, unused);
                 if (pc.S) {
                     f32x4* s4 = reinterpret_cast<f32x4*>(pc.S + q * M);
 #pragma unroll
@@ -343,8 +353,12 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
 // Backward; with kAdam the AdamW step on the logits is fused in: the moments
 // are read with the group's other inputs, and the updated logits and moments
 // are written instead of (or besides, when pc.dphi is set) the gradient.
-template <int M, int N, bool kLambdaOne, bool kAdam>
-__global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
+// kQ as in fwd_lane_kernel.  At m = 8 and n <= 4 the plain backward is held
+// to 128 VGPRs, so that four waves share a SIMD (at larger n the records, and
+// with the optimizer step the moments, need more).
+template <int M, int N, bool kLambdaOne, bool kAdam, int kQ>
+__global__ __launch_bounds__(kLaneBlock)
+__attribute__((amdgpu_waves_per_eu(M == 8 && N <= 4 && !kAdam ? 4 : 1))) void bwd_lane_kernel(BwdBatch a)
 {
     const BwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
@@ -384,11 +398,20 @@ __global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
 #pragma unroll
             for (int j = 0; j < M; ++j)
                 sbar[j] = bf16_bits_to_float(g[u][j]) * bf16_bits_to_float(w[u][j]);
+            // Relaxation forward keeping its records, then the reverse sweep:
+            // the exp-domain recursion where the group's key span allows it
+            // (the floor of log(1 - mu) is then out of reach), else the
+            // log-domain one with the floor's case in the sweep (relax.hpp).
             StepRec<M> rec[N];
-            float S_unused[M];
-            relax_forward<M, N, false, true>(kappa, a.inv_tau, a.inv_tau, S_unused, rec);
-            float abar[M];
-            relax_backward<M, N>(rec, sbar, a.tau, a.inv_tau, abar);
+            float S_unused[M], b[M], abar[M], bmax;
+            const float span = scaled_keys<M>(kappa, a.inv_tau, b, bmax);
+            if (span <= a.exp_span) {
+                relax_forward_exp<M, N, false, true, kQ>(b, bmax, a.inv_tau, S_unused, rec);
+                relax_backward<M, N, kQ == 1, false>(rec, sbar, a.inv_tau, abar);
+            } else {
+                relax_forward<M, N, false, true>(b, bmax, a.inv_tau, S_unused, rec);
+                relax_backward<M, N, false, true>(rec, sbar, a.inv_tau, abar);
+            }
             float grad[M]; // dL/dphi = dL/dkappa / lambda
 #pragma unroll
             for (int j = 0; j < M; ++j) grad[j] = kLambdaOne ? abar[j] : abar[j] * a.inv_lambda;
@@ -505,11 +528,40 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // ---- dispatch tables over (m, n) and the boolean variants
 
+// How the exp-domain recursion raises omega to 1 / tau: 1 or 2 when 1 / tau
+// is that integer (by multiplication), else 0 (exp2 and log2).
+int tau_mode(float tau) { return tau == 1.0f ? 1 : (tau == 0.5f ? 2 : 0); }
+
+// Largest key span (units of b, relax.hpp) for which a group may take the
+// exp-domain recursion: kExpSpanAccuracy, and kExpSpanLimit - (n - 1) q with
+// q = 1 / tau (without an update step, n = 1, only the first applies).  For
+// q > 2.25 the bound admits only key spans below 10 (natural units; 32 /
+// (q log2 e)), a few times the spread of the keys themselves, so many waves
+// would mix groups of both kinds and run both recursions; there the
+// exp-domain form is off (-1 admits no group).  The limit depends only on
+// (n, tau).
+float exp_span_limit(int n, float tau)
+{
+    const double q = 1.0 / (double)tau;
+    if (q > 2.25) return -1.0f;
+    const double repr = n <= 1 ? INFINITY : (double)kExpSpanLimit - (n - 1) * q;
+    return (float)std::min((double)kExpSpanAccuracy, repr);
+}
+
+template <int M, int N, bool S, bool I, bool L>
+FwdFn pick_fwd_q(int q)
+{
+    if constexpr (!S) return fwd_lane_kernel<M, N, S, I, L, 0>; // no relaxation
+    else
+        return q == 1 ? fwd_lane_kernel<M, N, S, I, L, 1>
+                      : (q == 2 ? fwd_lane_kernel<M, N, S, I, L, 2> : fwd_lane_kernel<M, N, S, I, L, 0>);
+}
+
 template <int M, int N>
-FwdFn pick_fwd(bool want_s, bool want_idx, bool lam1)
+FwdFn pick_fwd(bool want_s, bool want_idx, bool lam1, int q)
 {
 #define ROI_FWD(S, I, L) \
-    if (want_s == S && want_idx == I && lam1 == L) return fwd_lane_kernel<M, N, S, I, L>;
+    if (want_s == S && want_idx == I && lam1 == L) return pick_fwd_q<M, N, S, I, L>(q);
     ROI_FWD(false, false, false) ROI_FWD(false, false, true) ROI_FWD(false, true, false)
     ROI_FWD(false, true, true) ROI_FWD(true, false, false) ROI_FWD(true, false, true)
     ROI_FWD(true, true, false) ROI_FWD(true, true, true)
@@ -517,41 +569,50 @@ FwdFn pick_fwd(bool want_s, bool want_idx, bool lam1)
     return nullptr;
 }
 
-template <int M, int N>
-BwdFn pick_bwd(bool lam1, bool adam)
+template <int M, int N, bool L, bool A>
+BwdFn pick_bwd_q(int q)
 {
-    if (adam) return lam1 ? bwd_lane_kernel<M, N, true, true> : bwd_lane_kernel<M, N, false, true>;
-    return lam1 ? bwd_lane_kernel<M, N, true, false> : bwd_lane_kernel<M, N, false, false>;
+    return q == 1 ? bwd_lane_kernel<M, N, L, A, 1>
+                  : (q == 2 ? bwd_lane_kernel<M, N, L, A, 2> : bwd_lane_kernel<M, N, L, A, 0>);
+}
+
+template <int M, int N>
+BwdFn pick_bwd(bool lam1, bool adam, int q)
+{
+    if (adam) return lam1 ? pick_bwd_q<M, N, true, true>(q) : pick_bwd_q<M, N, false, true>(q);
+    return lam1 ? pick_bwd_q<M, N, true, false>(q) : pick_bwd_q<M, N, false, false>(q);
 }
 
 template <int M, int... Ns>
-FwdFn fwd_for_n(int n, bool s, bool i, bool l, std::integer_sequence<int, Ns...>)
+FwdFn fwd_for_n(int n, bool s, bool i, bool l, int q, std::integer_sequence<int, Ns...>)
 {
     FwdFn f = nullptr;
-    ((n == Ns + 1 ? (f = pick_fwd<M, Ns + 1>(s, i, l), 0) : 0), ...);
+    ((n == Ns + 1 ? (f = pick_fwd<M, Ns + 1>(s, i, l, q), 0) : 0), ...);
     return f;
 }
 
 template <int M, int... Ns>
-BwdFn bwd_for_n(int n, bool l, bool adam, std::integer_sequence<int, Ns...>)
+BwdFn bwd_for_n(int n, bool l, bool adam, int q, std::integer_sequence<int, Ns...>)
 {
     BwdFn f = nullptr;
-    ((n == Ns + 1 ? (f = pick_bwd<M, Ns + 1>(l, adam), 0) : 0), ...);
+    ((n == Ns + 1 ? (f = pick_bwd<M, Ns + 1>(l, adam, q), 0) : 0), ...);
     return f;
 }
 
-FwdFn select_fwd(int m, int n, bool s, bool i, bool l)
+FwdFn select_fwd(int m, int n, bool s, bool i, bool l, float tau)
 {
-    if (m == 4) return fwd_for_n<4>(n, s, i, l, std::make_integer_sequence<int, 4>{});
-    if (m == 8) return fwd_for_n<8>(n, s, i, l, std::make_integer_sequence<int, 8>{});
+    const int q = tau_mode(tau);
+    if (m == 4) return fwd_for_n<4>(n, s, i, l, q, std::make_integer_sequence<int, 4>{});
+    if (m == 8) return fwd_for_n<8>(n, s, i, l, q, std::make_integer_sequence<int, 8>{});
     return select_wide_fwd(m, n);
 }
 
-BwdFn select_bwd(int m, int n, bool l, bool adam, bool tau_one)
+BwdFn select_bwd(int m, int n, bool l, bool adam, float tau)
 {
-    if (m == 4) return bwd_for_n<4>(n, l, adam, std::make_integer_sequence<int, 4>{});
-    if (m == 8) return bwd_for_n<8>(n, l, adam, std::make_integer_sequence<int, 8>{});
-    return select_wide_bwd(m, n, adam, tau_one);
+    const int q = tau_mode(tau);
+    if (m == 4) return bwd_for_n<4>(n, l, adam, q, std::make_integer_sequence<int, 4>{});
+    if (m == 8) return bwd_for_n<8>(n, l, adam, q, std::make_integer_sequence<int, 8>{});
+    return select_wide_bwd(m, n, adam, tau == 1.0f);
 }
 
 } // namespace
@@ -665,7 +726,7 @@ int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count
     }
     if (with_s < 0) return ok(); // nothing to do
     if (int st = check_overlaps(ranges)) return st;
-    FwdFn fn = select_fwd(m, n, soft || with_s == 1, with_idx == 1, lambda == 1.0f);
+    FwdFn fn = select_fwd(m, n, soft || with_s == 1, with_idx == 1, lambda == 1.0f, tau);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     Launcher<FwdBatch, FwdPiece, FwdFn> L{};
     L.fn = fn;
@@ -678,6 +739,7 @@ int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count
     L.batch.lambda = lambda;
     L.batch.key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
     L.batch.inv_tau = (float)(1.0 / (double)tau);
+    L.batch.exp_span = exp_span_limit(n, tau);
     L.batch.soft = soft ? 1 : 0;
     for (int i = 0; i < count; ++i) {
         const int64_t ngroups = t[i].rows * t[i].cols / m;
@@ -778,7 +840,7 @@ int mask_bwd_core(const char* what, const BwdDesc* t, int count, int n, int m, f
     }
     if (!any) return ok();
     if (int st = check_overlaps(ranges)) return st;
-    BwdFn fn = select_bwd(m, n, lambda == 1.0f, adam, tau == 1.0f);
+    BwdFn fn = select_bwd(m, n, lambda == 1.0f, adam, tau);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     Launcher<BwdBatch, BwdPiece, BwdFn> L{};
     L.fn = fn;
@@ -792,6 +854,7 @@ int mask_bwd_core(const char* what, const BwdDesc* t, int count, int n, int m, f
     L.batch.inv_lambda = (float)(1.0 / (double)lambda);
     L.batch.tau = tau;
     L.batch.inv_tau = (float)(1.0 / (double)tau);
+    L.batch.exp_span = exp_span_limit(n, tau);
     L.batch.adam = astep;
     for (int i = 0; i < count; ++i) {
         const int64_t ngroups = t[i].rows * t[i].cols / m;

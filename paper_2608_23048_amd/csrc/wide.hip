@@ -83,8 +83,10 @@ __device__ __forceinline__ float min4(const float (&x)[4])
 
 // Widest key range (in the scaled log2 units of b) for which the exp-domain
 // recursion keeps every mu and omega a normal fp32 number with full precision
-// over 32 steps: exp2(-56) / 32 shrinks by at most 2 per step.
-constexpr float kExpDomainRange = 56.0f;
+// over 32 steps (exp2(-56) / 32 shrinks by at most 2 per step), and the
+// rounding its first shift by the largest key leaves in every exponent near
+// 1e-6 relative (relax.hpp, kExpSpanAccuracy).
+constexpr float kExpDomainRange = kExpSpanAccuracy < 56.0f ? kExpSpanAccuracy : 56.0f;
 
 // Adds, for lane distances D..L-1, how many entries of lane (lane ^ D) beat
 // each of this lane's entries (ties go to the lower index).
@@ -179,32 +181,36 @@ __device__ __forceinline__ bool wide_rank_fast(const float (&k)[4], int (&rank)[
 // lane; see relax_forward in relax.hpp for the arithmetic.
 // With kTauOne (tau = 1) the update alpha += log(max(omega, FLT_MIN)) is
 // carried out on the exponentials instead, e <- mu * omega (the same
-// recursion, without a log, an exp and a maximum per step), whenever every
-// group of the wave spans less than kExpDomainRange (2^-56).  Then every e
-// starts at >= 2^-56, the first mu and omega are >= 2^-61, and a step loses at
-// most a factor 2 (max(mu, omega) >= 1/2, so mu * omega >= min(mu, omega) / 2):
-// after 32 steps everything is still >= 2^-92, so the FLT_MIN floor is never
-// reached.  Returns true when the wave took this path (uniform over the wave);
-// other waves take the log-domain loop.
+// recursion, without a log, an exp and a maximum per step), whenever the
+// group spans less than kExpDomainRange (at most 2^-56).  Then every e starts
+// at >= 2^-56, the first mu and omega are >= 2^-61, and a step loses at most a
+// factor 2 (max(mu, omega) >= 1/2, so mu * omega >= min(mu, omega) / 2): after
+// 32 steps everything is still >= 2^-92, so the FLT_MIN floor is never
+// reached.  The choice is the group's own (all its lanes agree), so its
+// outputs do not depend on which groups share its wave; other groups take the
+// log-domain loop.  Returns true when this group took the exp-domain path.
 template <int L, int N, bool kKeep, bool kTauOne = false>
 __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], float key_scale,
                                                    float inv_tau, bool want_s, float (&S)[4],
                                                    StepRec<4> (&rec)[N])
 {
+    // b = kappa * key_scale unshifted, each step subtracting its own largest b
+    // (see scaled_keys in relax.hpp)
     const float kmax = group_max<L>(max4(kappa));
     const float c = key_scale;
+    const float bmax0 = kmax * c;
     float b[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        b[e] = (kappa[e] - kmax) * c;
+        b[e] = kappa[e] * c;
         S[e] = 0.0f;
     }
     if constexpr (kTauOne) {
         const float span = (kmax - group_min<L>(min4(kappa))) * c;
-        if (__all(span < kExpDomainRange)) { // uniform over the wave
+        if (span < kExpDomainRange) { // the same on all lanes of the group
             float ex[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) ex[e] = __builtin_amdgcn_exp2f(b[e]);
+            for (int e = 0; e < 4; ++e) ex[e] = __builtin_amdgcn_exp2f(b[e] - bmax0);
 #pragma unroll
             for (int k = 0; k < N; ++k) {
                 float others[4], t;
@@ -229,7 +235,7 @@ __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], floa
 #pragma unroll
     for (int k = 0; k < N; ++k) {
         float ex[4];
-        const float bmax = k == 0 ? 0.0f : group_max<L>(max4(b));
+        const float bmax = k == 0 ? bmax0 : group_max<L>(max4(b));
 #pragma unroll
         for (int e = 0; e < 4; ++e) ex[e] = __builtin_amdgcn_exp2f(b[e] - bmax);
         float others[4], t;
@@ -423,7 +429,9 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
         float abar[4];
         // A second, floor-free copy of the sweep pays for itself at m = 16; at
         // m = 32 its registers would cost a wave per SIMD.
-        if (kTauOne && L <= 4 && no_floor) // uniform over the wave
+        // (the two sweeps give the same bits wherever the floor was not reached,
+        // so this choice may be the wave's)
+        if (kTauOne && L <= 4 && __all(no_floor))
             wide_relax_backward<L, N, kTauOne, L <= 4>(rec, sbar, a.tau, a.inv_tau, abar);
         else
             wide_relax_backward<L, N, kTauOne, false>(rec, sbar, a.tau, a.inv_tau, abar);

@@ -32,12 +32,14 @@ def dev():
 
 
 def run_case(dev, rows, cols, n, m, tau, lam, seed, step, off, case_seed, w_std=wl.W_STD,
-             grad_std=wl.GRAD_STD, logit_std=wl.LOGIT_STD, scale_aware=False):
+             grad_std=wl.GRAD_STD, logit_std=wl.LOGIT_STD, scale_aware=False, logits=None):
     import torch
     say(f"case rows={rows} cols={cols} {n}:{m} tau={tau} lam={lam} seed={seed} step={step} "
         f"off={off} case_seed={case_seed}")
     W, L, G = wl.small_case(rows, cols, case_seed, device=dev, w_std=w_std, logit_std=logit_std,
                             grad_std=grad_std)
+    if logits is not None:
+        L = torch.from_numpy(np.ascontiguousarray(logits, dtype=np.float32)).to(dev)
     Wm, S, idx = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True)
     d = roi.mask_bwd(G, W, L, n, m, tau, lam, seed, step, off)
     torch.cuda.synchronize()
@@ -158,6 +160,57 @@ def test_small_unit_scale(dev, case):
              w_std=1.0, grad_std=1.0, logit_std=2.0, scale_aware=True)
 
 
+def relaxation_form_logits(rows, cols, m, tau, lam, seed):
+    """Logits laid out wave by wave (64 groups): calm groups (small key spans:
+    the exp-domain recursion), groups with one key 100 tau / lambda above the
+    rest (1 - mu of that key falls below FLT_MIN, so log(1 - mu) is floored),
+    groups with two such keys, wide-spread groups, and waves mixing calm and
+    dominant groups, which must all take the log-domain recursion together."""
+    rng = np.random.default_rng(seed)
+    groups = rows * cols // m
+    L = rng.normal(0.0, 1.0, size=(groups, m))
+    kind = (np.arange(groups) // 64) % 6
+    mixed = (kind == 4) & (np.arange(groups) % 2 == 1)
+    calm = (kind == 0) | ((kind == 4) & ~mixed)
+    L[calm] *= 0.3
+    big = 100.0 * tau * lam
+    top = rng.integers(0, m, size=groups)
+    second = (top + 1 + rng.integers(0, m - 1, size=groups)) % m
+    spike = (kind == 1) | (kind == 2) | mixed | (kind == 5)
+    L[spike, top[spike]] += big
+    two = kind == 2
+    L[two, second[two]] += 0.5 * big
+    wide = kind == 3
+    L[wide] *= 4.0
+    return L.reshape(rows, cols).astype(np.float32)
+
+
+RELAX_FORMS = [
+    # rows, cols, n, m, tau, lam: 392 groups = 6 full waves of each kind + a tail
+    (49, 32, 2, 4, 1.0, 1.0),
+    (49, 32, 2, 4, 0.5, 1.0),
+    (49, 32, 2, 4, 0.3, 1.0),
+    (49, 32, 1, 4, 1.0, 1.0),
+    (49, 32, 3, 4, 0.5, 0.7),
+    (49, 64, 4, 8, 0.5, 1.0),
+    (49, 64, 2, 8, 1.0, 2.0),
+    (49, 64, 6, 8, 0.25, 1.0),
+    (49, 128, 8, 16, 1.0, 1.0),
+    (49, 256, 16, 32, 1.0, 1.0),
+]
+
+
+@pytest.mark.parametrize("case", RELAX_FORMS, ids=lambda c: "x".join(map(str, c[:5])))
+def test_relaxation_forms_and_floor(dev, case):
+    """Waves that take the exp-domain recursion, waves that must fall back to
+    the log-domain one, and groups that reach the FLT_MIN floor of log(1 - mu)
+    (so the backward's floor case runs), in one launch, against the oracle."""
+    rows, cols, n, m, tau, lam = case
+    logits = relaxation_form_logits(rows, cols, m, tau, lam, seed=rows * cols + n)
+    run_case(dev, rows, cols, n, m, tau, lam, 3, 1, 0, case_seed=cols + n, w_std=1.0,
+             grad_std=1.0, scale_aware=True, logits=logits)
+
+
 def test_single_layer_896(dev):
     """One 896x896 linear layer, 2:4, tau = 1, seed 0, step 0: every output."""
     run_case(dev, 896, 896, 2, 4, 1.0, 1.0, 0, 0, 0, case_seed=0)
@@ -250,33 +303,40 @@ def test_near_ties_bit_exact(dev, case):
 
 
 # --------------------------------------------------------------------------- layout properties
-def test_split_calls_equal_one_slab_call(dev):
+@pytest.mark.parametrize("tau", [1.0, 0.5, 0.4])
+def test_split_calls_equal_one_slab_call(dev, tau):
     """Per-tensor calls with cumulative elem_offset give exactly the outputs of
-    one call over the back-to-back slab."""
+    one call over the back-to-back slab.  Tensor boundaries fall inside waves
+    at every m, and the logits mix spreads so that groups of one wave disagree
+    on which form of the relaxation their key spans allow: a group's bits must
+    not depend on the groups that share its wave."""
     import torch
-    shapes = [(128, 96), (32, 96), (32, 96), (128, 96), (200, 96), (96, 224)]
+    shapes = [(128, 96), (33, 96), (32, 96), (128, 96), (200, 96), (96, 224), (7, 96)]
     offs = np.cumsum([0] + [r * c for r, c in shapes])
     total = int(offs[-1])
     gen = torch.Generator(device="cpu")
     gen.manual_seed(3)
     W = (torch.randn(total, generator=gen) * 0.02).to(torch.bfloat16).to(dev)
-    L = torch.randn(total, generator=gen).to(dev)
+    spread = torch.where(torch.rand(total // 4, generator=gen) < 0.3, 6.0, 1.0)
+    L = (torch.randn(total, generator=gen) * spread.repeat_interleave(4)).to(dev)
     G = (torch.randn(total, generator=gen) * 1e-3).to(torch.bfloat16).to(dev)
     for n, m in ((2, 4), (4, 8), (8, 16), (16, 32)):
-        say(f"split vs slab {n}:{m}")
-        Wm, S, idx = roi.mask_fwd(W, L, n, m, 0.5, 1.0, 9, 2, 0, want_soft=True)
-        d = roi.mask_bwd(G, W, L, n, m, 0.5, 1.0, 9, 2, 0)
+        say(f"split vs slab {n}:{m} tau={tau}")
+        Wm, S, idx = roi.mask_fwd(W, L, n, m, tau, 1.0, 9, 2, 0, want_soft=True)
+        d = roi.mask_bwd(G, W, L, n, m, tau, 1.0, 9, 2, 0)
         for (r, c), o in zip(shapes, offs[:-1]):
             o = int(o)
             sl = slice(o, o + r * c)
             w_t, l_t, g_t = (W[sl].view(r, c), L[sl].view(r, c), G[sl].view(r, c))
-            Wm_t, S_t, idx_t = roi.mask_fwd(w_t, l_t, n, m, 0.5, 1.0, 9, 2, o, want_soft=True)
-            d_t = roi.mask_bwd(g_t, w_t, l_t, n, m, 0.5, 1.0, 9, 2, o)
+            Wm_t, S_t, idx_t = roi.mask_fwd(w_t, l_t, n, m, tau, 1.0, 9, 2, o, want_soft=True)
+            d_t = roi.mask_bwd(g_t, w_t, l_t, n, m, tau, 1.0, 9, 2, o)
             torch.cuda.synchronize()
             assert torch.equal(Wm_t.reshape(-1).view(torch.int16), Wm[sl].view(torch.int16))
-            assert torch.equal(S_t.reshape(-1).view(torch.int32), S[sl].view(torch.int32))
+            assert torch.equal(S_t.reshape(-1).view(torch.int32), S[sl].view(torch.int32)), \
+                f"soft mask differs, tensor at {o}"
             assert torch.equal(idx_t, idx[o // m:(o + r * c) // m])
-            assert torch.equal(d_t.reshape(-1).view(torch.int32), d[sl].view(torch.int32))
+            assert torch.equal(d_t.reshape(-1).view(torch.int32), d[sl].view(torch.int32)), \
+                f"grad_logits differs, tensor at {o}"
 
 
 def grouped_inputs(dev, m, count=20, seed=5):
