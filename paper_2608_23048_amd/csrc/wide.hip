@@ -129,51 +129,88 @@ __device__ __forceinline__ void wide_rank(const float (&k)[4], int part, int (&r
     rank_against_lane<L, 1>(k, part, rank);
 }
 
-// The same ranks from the hardware-log keys (noise.hpp): every comparison of
-// this lane's entries is decided by the sign of d = other - own, and `sep`
-// stays true only if every |d| exceeds the margin of two keys' errors (then
-// no two keys tie and each sign is the exact keys').
-template <int L, int D>
-__device__ __forceinline__ void rank_against_lane_fast(const float (&k)[4], float margin,
-                                                       int (&rank)[4], bool& sep)
+// Hard top-n from the hardware-log keys by a bitonic sort of the group
+// (descending), entry i = 4 part + e of the group at lane `part`, slot e.
+// Each key travels with its index.  A stage (kk, j) pairs entry i with
+// i ^ j; the pair is ordered descending when (i & kk) == 0 and ascending
+// otherwise, the lower entry of a descending pair keeping the larger key.
+// j = 1, 2 pair slots of one lane; j >= 4 pairs lane part with lane
+// part ^ (j / 4), each lane keeping one side of its four pairs.  The
+// network is log2(m) (log2(m) + 1) / 2 stages of 4 entries per lane, against
+// m comparisons per entry for counting ranks.
+template <int KK, int J>
+__device__ __forceinline__ void bitonic_stage(float (&k)[4], int (&ix)[4], int part)
 {
-    if constexpr (D < L) {
-        float o[4];
+    if constexpr (J < 4) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = lane_xor<D>(k[e]);
+        for (int lo = 0; lo < 4; ++lo) {
+            if ((lo & J) != 0) continue;
+            const int hi = lo | J;
+            // direction of the pair: (i & KK) with i = 4 part + lo
+            const bool desc = KK < 4 ? ((lo & KK) == 0) : ((part & (KK >> 2)) == 0);
+            const bool sw = (k[hi] > k[lo]) == desc;
+            const float kl = k[lo], kh = k[hi];
+            const int il = ix[lo], ih = ix[hi];
+            k[lo] = sw ? kh : kl;
+            k[hi] = sw ? kl : kh;
+            ix[lo] = sw ? ih : il;
+            ix[hi] = sw ? il : ih;
+        }
+    } else {
+        constexpr int D = J / 4; // lane distance
+        const bool lower = (part & D) == 0;
+        const bool desc = (part & (KK >> 2)) == 0;
+        const bool keep_max = lower == desc;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-#pragma unroll
-            for (int f = 0; f < 4; ++f) {
-                const float d = o[f] - k[e];
-                sep &= fabsf(d) > margin;
-                rank[e] += d > 0.0f ? 1 : 0;
-            }
+            const float o = lane_xor<D>(k[e]);
+            const int oi = __float_as_int(lane_xor<D>(__int_as_float(ix[e])));
+            const bool take = (o > k[e]) == keep_max;
+            k[e] = take ? o : k[e];
+            ix[e] = take ? oi : ix[e];
         }
-        rank_against_lane_fast<L, D + 1>(k, margin, rank, sep);
     }
 }
 
-template <int L>
-__device__ __forceinline__ bool wide_rank_fast(const float (&k)[4], int (&rank)[4])
+template <int M, int KK, int J>
+__device__ __forceinline__ void bitonic_from(float (&k)[4], int (&ix)[4], int part)
 {
-    float big = fmaxf(fmaxf(fabsf(k[0]), fabsf(k[1])), fmaxf(fabsf(k[2]), fabsf(k[3])));
+    bitonic_stage<KK, J>(k, ix, part);
+    if constexpr (J > 1)
+        bitonic_from<M, KK, J / 2>(k, ix, part);
+    else if constexpr (KK < M)
+        bitonic_from<M, KK * 2, KK>(k, ix, part);
+}
+
+// Sorts the group's hardware-log keys and returns whether every two keys of
+// the group are further apart than the margin of their errors (noise.hpp):
+// then the order is the exact keys' order and no two tie, and checking the
+// m - 1 pairs adjacent in the sorted order covers every pair.  On return
+// keep[e] tells whether this lane's entry e is among the n largest, and
+// sidx[e] is the index (within the group) of the entry at sorted position
+// 4 part + e.
+template <int L, int N>
+__device__ __forceinline__ bool wide_top_fast(const float (&kf)[4], int part, bool (&keep)[4],
+                                              int (&sidx)[4])
+{
+    constexpr int M = 4 * L;
+    float big = fmaxf(fmaxf(fabsf(kf[0]), fabsf(kf[1])), fmaxf(fabsf(kf[2]), fabsf(kf[3])));
     big = group_max<L>(big);
     const float margin = __builtin_fmaf(big, 0x1p-20f, kFastPairMargin);
-    bool sep = true;
+    float k[4] = {kf[0], kf[1], kf[2], kf[3]};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) rank[e] = 0;
+    for (int e = 0; e < 4; ++e) sidx[e] = 4 * part + e;
+    bitonic_from<M, 2, 1>(k, sidx, part);
+    // adjacent sorted pairs: three in the lane, and the lane's last with the
+    // next lane's first (the group's last lane has no successor)
+    bool sep = (k[0] - k[1] > margin) & (k[1] - k[2] > margin) & (k[2] - k[3] > margin);
+    const int lane = (int)(threadIdx.x & 63);
+    const float next = __shfl(k[0], part + 1 < L ? lane + 1 : lane);
+    sep &= (part + 1 == L) || (k[3] - next > margin);
+    // the n-th largest key, held by lane (n - 1) / 4 of the group
+    const float kth = __shfl(k[(N - 1) % 4], lane - part + (N - 1) / 4);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-        for (int j = i + 1; j < 4; ++j) {
-            const float d = k[i] - k[j];
-            sep &= fabsf(d) > margin;
-            rank[j] += d > 0.0f ? 1 : 0;
-            rank[i] += d > 0.0f ? 0 : 1;
-        }
-    }
-    rank_against_lane_fast<L, 1>(k, margin, rank, sep);
+    for (int e = 0; e < 4; ++e) keep[e] = kf[e] >= kth;
     return sep;
 }
 
@@ -341,6 +378,8 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
         int rank[4];
         const bool relax = pc.S || a.soft; // uniform over the launch
         bool decided = false;
+        bool keep[4];
+        int sidx[4];
         if (!relax) {
             // Comparisons only: the hardware-log keys decide when every pair of
             // every group in the wave is further apart than the margin (else
@@ -350,22 +389,41 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
                                  fast_key_log2(phi[1], a.key_c, x.y),
                                  fast_key_log2(phi[2], a.key_c, x.z),
                                  fast_key_log2(phi[3], a.key_c, x.w)};
-            decided = __all(wide_rank_fast<L>(kf, rank));
+            decided = __all(wide_top_fast<L, N>(kf, part, keep, sidx));
         }
         if (!decided) {
             wide_keys(phi, pc.block0 + (uint32_t)slot, key, a.lambda, tab, kappa);
             wide_rank<L>(kappa, part, rank);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) keep[e] = rank[e] < N;
         }
         if (!a.soft) {
-            const uint32_t m01 = (rank[0] < N ? 0x0000FFFFu : 0u) | (rank[1] < N ? 0xFFFF0000u : 0u);
-            const uint32_t m23 = (rank[2] < N ? 0x0000FFFFu : 0u) | (rank[3] < N ? 0xFFFF0000u : 0u);
+            const uint32_t m01 = (keep[0] ? 0x0000FFFFu : 0u) | (keep[1] ? 0xFFFF0000u : 0u);
+            const uint32_t m23 = (keep[2] ? 0x0000FFFFu : 0u) | (keep[3] ? 0xFFFF0000u : 0u);
             const u32x2 out = {wv.x & m01, wv.y & m23};
             stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
         }
         if (pc.idx) {
+            if (decided) {
+                // this lane holds sorted positions 4 part .. 4 part + 3
+                uint8_t* dst = pc.idx + group * N + 4 * part;
+                if (4 * part + 4 <= N) {
+                    const uint32_t w = (uint32_t)sidx[0] | ((uint32_t)sidx[1] << 8) |
+                                       ((uint32_t)sidx[2] << 16) | ((uint32_t)sidx[3] << 24);
+                    if constexpr (N % 4 == 0)
+                        stream_store(w, reinterpret_cast<uint32_t*>(dst));
+                    else
+                        for (int e = 0; e < 4; ++e) dst[e] = (uint8_t)(w >> (8 * e));
+                } else {
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                if (rank[e] < N) pc.idx[group * N + rank[e]] = (uint8_t)(part * 4 + e);
+                    for (int e = 0; e < 4; ++e)
+                        if (4 * part + e < N) dst[e] = (uint8_t)sidx[e];
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (rank[e] < N) pc.idx[group * N + rank[e]] = (uint8_t)(part * 4 + e);
+            }
         }
         if (pc.S || a.soft) {
             float S[4];
