@@ -184,8 +184,8 @@ __device__ __forceinline__ void relax_forward(float (&b)[M], float bmax0, float 
 // the total of the products never exceeds 1: after k steps its mu is at least
 // 2^-(span + log2 M + k q).  Before the last step at most N - 1 <= M - 1
 // entries have been dominant, so one such entry always exists, and the
-// dominant entry's omega (the sum of the others) is at least as large.  Hence,
-// for M <= 8, span + (N - 1) q <= kExpSpanLimit keeps every such mu and omega
+// dominant entry's omega (the sum of the others) is at least as large.  Hence
+// span + log2 M + (N - 1) q <= kExpNormalBound keeps every such mu and omega
 // above 2^-91: normal numbers far from underflow, and far above the FLT_MIN
 // floor of log(1 - mu), which is therefore never reached.  An entry that has
 // been dominant and falls below 2^-126 moves the total by less than 2^-35 of
@@ -194,7 +194,7 @@ __device__ __forceinline__ void relax_forward(float (&b)[M], float bmax0, float 
 // largest key for good: each exponent b_j - bmax carries a rounding of about
 // 2^-24 |b_j - bmax| (with that of key_scale), a relative error of about
 // 4e-8 span in e_j.  span <= kExpSpanAccuracy keeps it near 1e-6.
-constexpr float kExpSpanLimit = 88.0f;
+constexpr float kExpNormalBound = 91.0f;
 constexpr float kExpSpanAccuracy = 32.0f;
 
 template <int kQ>

@@ -533,18 +533,20 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int tau_mode(float tau) { return tau == 1.0f ? 1 : (tau == 0.5f ? 2 : 0); }
 
 // Largest key span (units of b, relax.hpp) for which a group may take the
-// exp-domain recursion: kExpSpanAccuracy, and kExpSpanLimit - (n - 1) q with
-// q = 1 / tau (without an update step, n = 1, only the first applies).  For
+// exp-domain recursion: kExpSpanAccuracy, and kExpNormalBound - log2 m -
+// (n - 1) q with q = 1 / tau (without an update step, n = 1, only the first
+// applies).  For
 // q > 2.25 the bound admits only key spans below 10 (natural units; 32 /
 // (q log2 e)), a few times the spread of the keys themselves, so many waves
 // would mix groups of both kinds and run both recursions; there the
 // exp-domain form is off (-1 admits no group).  The limit depends only on
 // (n, tau).
-float exp_span_limit(int n, float tau)
+float exp_span_limit(int n, int m, float tau)
 {
     const double q = 1.0 / (double)tau;
     if (q > 2.25) return -1.0f;
-    const double repr = n <= 1 ? INFINITY : (double)kExpSpanLimit - (n - 1) * q;
+    const double repr =
+        n <= 1 ? INFINITY : (double)kExpNormalBound - std::log2((double)m) - (n - 1) * q;
     return (float)std::min((double)kExpSpanAccuracy, repr);
 }
 
@@ -604,7 +606,7 @@ FwdFn select_fwd(int m, int n, bool s, bool i, bool l, float tau)
     const int q = tau_mode(tau);
     if (m == 4) return fwd_for_n<4>(n, s, i, l, q, std::make_integer_sequence<int, 4>{});
     if (m == 8) return fwd_for_n<8>(n, s, i, l, q, std::make_integer_sequence<int, 8>{});
-    return select_wide_fwd(m, n);
+    return select_wide_fwd(m, n, q);
 }
 
 BwdFn select_bwd(int m, int n, bool l, bool adam, float tau)
@@ -612,7 +614,7 @@ BwdFn select_bwd(int m, int n, bool l, bool adam, float tau)
     const int q = tau_mode(tau);
     if (m == 4) return bwd_for_n<4>(n, l, adam, q, std::make_integer_sequence<int, 4>{});
     if (m == 8) return bwd_for_n<8>(n, l, adam, q, std::make_integer_sequence<int, 8>{});
-    return select_wide_bwd(m, n, adam, tau == 1.0f);
+    return select_wide_bwd(m, n, adam, q);
 }
 
 } // namespace
@@ -739,7 +741,7 @@ int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count
     L.batch.lambda = lambda;
     L.batch.key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
     L.batch.inv_tau = (float)(1.0 / (double)tau);
-    L.batch.exp_span = exp_span_limit(n, tau);
+    L.batch.exp_span = exp_span_limit(n, m, tau);
     L.batch.soft = soft ? 1 : 0;
     for (int i = 0; i < count; ++i) {
         const int64_t ngroups = t[i].rows * t[i].cols / m;
@@ -854,7 +856,7 @@ int mask_bwd_core(const char* what, const BwdDesc* t, int count, int n, int m, f
     L.batch.inv_lambda = (float)(1.0 / (double)lambda);
     L.batch.tau = tau;
     L.batch.inv_tau = (float)(1.0 / (double)tau);
-    L.batch.exp_span = exp_span_limit(n, tau);
+    L.batch.exp_span = exp_span_limit(n, m, tau);
     L.batch.adam = astep;
     for (int i = 0; i < count; ++i) {
         const int64_t ngroups = t[i].rows * t[i].cols / m;

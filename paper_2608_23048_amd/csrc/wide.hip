@@ -81,13 +81,6 @@ __device__ __forceinline__ float min4(const float (&x)[4])
     return fminf(fminf(x[0], x[1]), fminf(x[2], x[3]));
 }
 
-// Widest key range (in the scaled log2 units of b) for which the exp-domain
-// recursion keeps every mu and omega a normal fp32 number with full precision
-// over 32 steps (exp2(-56) / 32 shrinks by at most 2 per step), and the
-// rounding its first shift by the largest key leaves in every exponent near
-// 1e-6 relative (relax.hpp, kExpSpanAccuracy).
-constexpr float kExpDomainRange = kExpSpanAccuracy < 56.0f ? kExpSpanAccuracy : 56.0f;
-
 // Adds, for lane distances D..L-1, how many entries of lane (lane ^ D) beat
 // each of this lane's entries (ties go to the lower index).
 template <int L, int D>
@@ -215,21 +208,16 @@ __device__ __forceinline__ bool wide_top_fast(const float (&kf)[4], int part, bo
 }
 
 // Relaxation over the group (§3.2 recursion, Algorithm 1), four entries per
-// lane; see relax_forward in relax.hpp for the arithmetic.
-// With kTauOne (tau = 1) the update alpha += log(max(omega, FLT_MIN)) is
-// carried out on the exponentials instead, e <- mu * omega (the same
-// recursion, without a log, an exp and a maximum per step), whenever the
-// group spans less than kExpDomainRange (at most 2^-56).  Then every e starts
-// at >= 2^-56, the first mu and omega are >= 2^-61, and a step loses at most a
-// factor 2 (max(mu, omega) >= 1/2, so mu * omega >= min(mu, omega) / 2): after
-// 32 steps everything is still >= 2^-92, so the FLT_MIN floor is never
-// reached.  The choice is the group's own (all its lanes agree), so its
-// outputs do not depend on which groups share its wave; other groups take the
-// log-domain loop.  Returns true when this group took the exp-domain path.
-template <int L, int N, bool kKeep, bool kTauOne = false>
+// lane: the exp-domain recursion of relax_forward_exp when the group's key
+// span is at most exp_span (the host's bound, relax.hpp), else the log-domain
+// loop of relax_forward, with sums over the group's other lanes.  The choice
+// is the group's own (all its lanes agree), so its outputs do not depend on
+// which groups share its wave.  Returns true when this group took the
+// exp-domain path (its omegas then never reach the floor).
+template <int L, int N, bool kKeep, int kQ>
 __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], float key_scale,
-                                                   float inv_tau, bool want_s, float (&S)[4],
-                                                   StepRec<4> (&rec)[N])
+                                                   float inv_tau, float exp_span, bool want_s,
+                                                   float (&S)[4], StepRec<4> (&rec)[N])
 {
     // b = kappa * key_scale unshifted, each step subtracting its own largest b
     // (see scaled_keys in relax.hpp)
@@ -242,32 +230,30 @@ __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], floa
         b[e] = kappa[e] * c;
         S[e] = 0.0f;
     }
-    if constexpr (kTauOne) {
-        const float span = (kmax - group_min<L>(min4(kappa))) * c;
-        if (span < kExpDomainRange) { // the same on all lanes of the group
-            float ex[4];
+    const float span = (kmax - group_min<L>(min4(kappa))) * c;
+    if (span <= exp_span) { // the same on all lanes of the group
+        float ex[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) ex[e] = __builtin_amdgcn_exp2f(b[e] - bmax0);
+        for (int e = 0; e < 4; ++e) ex[e] = __builtin_amdgcn_exp2f(b[e] - bmax0);
 #pragma unroll
-            for (int k = 0; k < N; ++k) {
-                float others[4], t;
-                sums_but_one<4>(ex, others, t);
-                const float ext = sum_other_lanes<L>(t);
-                const float inv_total = __builtin_amdgcn_rcpf(t + ext);
+        for (int k = 0; k < N; ++k) {
+            float others[4], t;
+            sums_but_one<4>(ex, others, t);
+            const float ext = sum_other_lanes<L>(t);
+            const float inv_total = __builtin_amdgcn_rcpf(t + ext);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float mu = ex[e] * inv_total;
-                    const float om = (others[e] + ext) * inv_total;
-                    if (want_s) S[e] += mu;
-                    if (kKeep) {
-                        rec[k].mu[e] = mu;
-                        rec[k].om[e] = om;
-                    }
-                    if (k + 1 < N) ex[e] = mu * om;
+            for (int e = 0; e < 4; ++e) {
+                const float mu = ex[e] * inv_total;
+                const float om = (others[e] + ext) * inv_total;
+                if (want_s) S[e] += mu;
+                if (kKeep) {
+                    rec[k].mu[e] = mu;
+                    rec[k].om[e] = om;
                 }
+                if (k + 1 < N) ex[e] = mu * pow_q<kQ>(om, inv_tau);
             }
-            return true;
         }
+        return true;
     }
 #pragma unroll
     for (int k = 0; k < N; ++k) {
@@ -295,28 +281,28 @@ __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], floa
     return false;
 }
 
-// Reverse sweep over the group; see relax_backward in relax.hpp.  With
-// kTauOne, keep = 1 - mu / tau is omega itself and mu / tau is mu; with
-// kNoFloor (the forward never reached the floor) the floor's selects go.
-template <int L, int N, bool kTauOne = false, bool kNoFloor = false>
+// Reverse sweep over the group: relax_backward of relax.hpp (one form for
+// every entry; with kFloor, floored logs pass no derivative), with the sum over
+// the other entries taken across the group's lanes.
+template <int L, int N, bool kTauIsOne, bool kFloor>
 __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
-                                                    const float (&sbar)[4], float tau,
-                                                    float inv_tau, float (&abar)[4])
+                                                    const float (&sbar)[4], float inv_tau,
+                                                    float (&abar)[4])
 {
-    const float keep0 = (tau - 1.0f) * inv_tau;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) abar[e] = 0.0f;
 #pragma unroll
     for (int k = N - 1; k >= 0; --k) {
         const bool has_next = (k + 1 < N);
-        float t[4];
+        float t[4], a_in[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             float mubar = sbar[e];
+            a_in[e] = 0.0f;
             if (has_next) {
                 const float om = rec[k].om[e];
-                const float r = abar[e] * __builtin_amdgcn_rcpf(om);
-                mubar = (kNoFloor || om >= kFltMin) ? mubar - r : mubar;
+                const bool live = !kFloor || om >= kFltMin;
+                const float rinv = live ? __builtin_amdgcn_rcpf(om) : 0.0f;
+                mubar = __builtin_fmaf(-abar[e], rinv, sbar[e]);
+                a_in[e] = live ? abar[e] : 0.0f;
             }
             t[e] = rec[k].mu[e] * mubar;
         }
@@ -325,18 +311,9 @@ __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
         const float ext = sum_other_lanes<L>(tl);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float om = rec[k].om[e];
-            const float mu = rec[k].mu[e];
-            const float inner = __builtin_fmaf(om, sbar[e], -(q[e] + ext));
-            float carry = 0.0f;
-            if (has_next) {
-                float keep = kTauOne ? om
-                                     : (mu < 0.5f ? __builtin_fmaf(-mu, inv_tau, 1.0f)
-                                                  : __builtin_fmaf(om, inv_tau, keep0));
-                keep = (kNoFloor || om >= kFltMin) ? keep : 1.0f;
-                carry = abar[e] * keep;
-            }
-            abar[e] = __builtin_fmaf(kTauOne ? mu : mu * inv_tau, inner, carry);
+            const float x = __builtin_fmaf(rec[k].om[e], sbar[e], -(q[e] + ext));
+            const float m_t = kTauIsOne ? rec[k].mu[e] : rec[k].mu[e] * inv_tau;
+            abar[e] = has_next ? __builtin_fmaf(m_t, x - a_in[e], abar[e]) : m_t * x;
         }
     }
 }
@@ -355,7 +332,8 @@ __device__ __forceinline__ void wide_keys(const float (&phi)[4], uint32_t block,
     }
 }
 
-template <int M, int N>
+// kQ: how the exp-domain recursion raises omega to 1 / tau (relax.hpp pow_q).
+template <int M, int N, int kQ>
 __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
 {
     constexpr int L = M / 4;
@@ -428,8 +406,8 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
         if (pc.S || a.soft) {
             float S[4];
             StepRec<4> unused[N]; // not written when records are not kept
-            wide_relax_forward<L, N, false>(kappa, kLog2e * a.inv_tau, a.inv_tau, true, S,
-                                            unused);
+            wide_relax_forward<L, N, false, kQ>(kappa, kLog2e * a.inv_tau, a.inv_tau, a.exp_span,
+                                                true, S, unused);
             if (pc.S) {
                 const f32x4 sv = {S[0], S[1], S[2], S[3]};
                 stream_store(sv, reinterpret_cast<f32x4*>(pc.S + slot * 4));
@@ -448,7 +426,7 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
 
 // Backward; with kAdam the AdamW step on the logits is fused in (as in the
 // per-lane kernels).
-template <int M, int N, bool kAdam, bool kTauOne = false>
+template <int M, int N, bool kAdam, int kQ>
 __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
 {
     constexpr int L = M / 4;
@@ -482,17 +460,17 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
             bf16_bits_to_float(gv.y >> 16) * bf16_bits_to_float(wv.y >> 16)};
         StepRec<4> rec[N];
         float S_unused[4];
-        const bool no_floor = wide_relax_forward<L, N, true, kTauOne>(
-            kappa, a.inv_tau, a.inv_tau, false, S_unused, rec);
+        const bool exp_domain = wide_relax_forward<L, N, true, kQ>(
+            kappa, a.inv_tau, a.inv_tau, a.exp_span, false, S_unused, rec);
         float abar[4];
-        // A second, floor-free copy of the sweep pays for itself at m = 16; at
-        // m = 32 its registers would cost a wave per SIMD.
-        // (the two sweeps give the same bits wherever the floor was not reached,
-        // so this choice may be the wave's)
-        if (kTauOne && L <= 4 && __all(no_floor))
-            wide_relax_backward<L, N, kTauOne, L <= 4>(rec, sbar, a.tau, a.inv_tau, abar);
+        // Where every group of the wave took the exp-domain recursion, no
+        // floor was reached and the sweep drops its selects (the two forms give
+        // the same bits there, so this choice may be the wave's).  At m = 32
+        // a second copy of the sweep would cost a wave per SIMD in registers.
+        if (L <= 4 && __all(exp_domain))
+            wide_relax_backward<L, N, kQ == 1, false>(rec, sbar, a.inv_tau, abar);
         else
-            wide_relax_backward<L, N, kTauOne, false>(rec, sbar, a.tau, a.inv_tau, abar);
+            wide_relax_backward<L, N, kQ == 1, true>(rec, sbar, a.inv_tau, abar);
         // dL/dphi = dL/dkappa / lambda (the product is exact for lambda = 1)
         const float grad[4] = {abar[0] * a.inv_lambda, abar[1] * a.inv_lambda,
                                abar[2] * a.inv_lambda, abar[3] * a.inv_lambda};
@@ -508,23 +486,33 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
     }
 }
 
+template <int M, int N>
+FwdFn wide_fwd_q(int q)
+{
+    return q == 1 ? fwd_wide_kernel<M, N, 1>
+                  : (q == 2 ? fwd_wide_kernel<M, N, 2> : fwd_wide_kernel<M, N, 0>);
+}
+
+template <int M, int N, bool A>
+BwdFn wide_bwd_q(int q)
+{
+    return q == 1 ? bwd_wide_kernel<M, N, A, 1>
+                  : (q == 2 ? bwd_wide_kernel<M, N, A, 2> : bwd_wide_kernel<M, N, A, 0>);
+}
+
 template <int M, int... Ns>
-FwdFn wide_fwd_for_n(int n, std::integer_sequence<int, Ns...>)
+FwdFn wide_fwd_for_n(int n, int q, std::integer_sequence<int, Ns...>)
 {
     FwdFn f = nullptr;
-    ((n == Ns + 1 ? (f = fwd_wide_kernel<M, Ns + 1>, 0) : 0), ...);
+    ((n == Ns + 1 ? (f = wide_fwd_q<M, Ns + 1>(q), 0) : 0), ...);
     return f;
 }
 
 template <int M, int... Ns>
-BwdFn wide_bwd_for_n(int n, bool adam, bool tau_one, std::integer_sequence<int, Ns...>)
+BwdFn wide_bwd_for_n(int n, bool adam, int q, std::integer_sequence<int, Ns...>)
 {
     BwdFn f = nullptr;
-    ((n == Ns + 1 ? (f = adam ? (tau_one ? bwd_wide_kernel<M, Ns + 1, true, true>
-                                         : bwd_wide_kernel<M, Ns + 1, true, false>)
-                              : (tau_one ? bwd_wide_kernel<M, Ns + 1, false, true>
-                                         : bwd_wide_kernel<M, Ns + 1, false, false>),
-                     0)
+    ((n == Ns + 1 ? (f = adam ? wide_bwd_q<M, Ns + 1, true>(q) : wide_bwd_q<M, Ns + 1, false>(q), 0)
                   : 0),
      ...);
     return f;
@@ -532,17 +520,17 @@ BwdFn wide_bwd_for_n(int n, bool adam, bool tau_one, std::integer_sequence<int, 
 
 } // namespace
 
-FwdFn select_wide_fwd(int m, int n)
+FwdFn select_wide_fwd(int m, int n, int q)
 {
-    if (m == 16) return wide_fwd_for_n<16>(n, std::make_integer_sequence<int, 16>{});
-    if (m == 32) return wide_fwd_for_n<32>(n, std::make_integer_sequence<int, 32>{});
+    if (m == 16) return wide_fwd_for_n<16>(n, q, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_fwd_for_n<32>(n, q, std::make_integer_sequence<int, 32>{});
     return nullptr;
 }
 
-BwdFn select_wide_bwd(int m, int n, bool adam, bool tau_one)
+BwdFn select_wide_bwd(int m, int n, bool adam, int q)
 {
-    if (m == 16) return wide_bwd_for_n<16>(n, adam, tau_one, std::make_integer_sequence<int, 16>{});
-    if (m == 32) return wide_bwd_for_n<32>(n, adam, tau_one, std::make_integer_sequence<int, 32>{});
+    if (m == 16) return wide_bwd_for_n<16>(n, adam, q, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_bwd_for_n<32>(n, adam, q, std::make_integer_sequence<int, 32>{});
     return nullptr;
 }
 
