@@ -134,13 +134,14 @@ def algorithmic_bytes(n: int, m: int) -> tuple[float, float]:
 
 def cpu_baseline(W, L, G, work, n, m, tau):
     """The CPU oracle, as it is, on a bounded sample of the same workload: the
-    q, k, v and o projections of layer 0, one forward + backward."""
+    q, k, v, o and gate projections of layer 0 (about 10 s of one core), one
+    forward + backward."""
     import numpy as np
     import torch
 
     import oracle
 
-    sample = [t for t in work.tensors[:4]]
+    sample = [t for t in work.tensors[:5]]
     end = sample[-1].offset + sample[-1].numel
     bits = lambda t: t[:end].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     Wb, Gb, Lf = bits(W), bits(G), L[:end].cpu().numpy()
