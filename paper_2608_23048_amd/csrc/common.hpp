@@ -196,7 +196,7 @@ ExportFn select_export(int m, int n);
 
 // Kernels for m = 16 and 32 (wide.hip): four consecutive elements per lane,
 // a group spread over m / 4 adjacent lanes.
-FwdFn select_wide_fwd(int m, int n, int q);            // q: tau_mode (roi.hip)
+FwdFn select_wide_fwd(int m, int n, bool relax, int q); // q: tau_mode (roi.hip)
 BwdFn select_wide_bwd(int m, int n, bool adam, int q);
 
 } // namespace roi

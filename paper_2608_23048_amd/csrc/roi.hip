@@ -606,7 +606,7 @@ FwdFn select_fwd(int m, int n, bool s, bool i, bool l, float tau)
     const int q = tau_mode(tau);
     if (m == 4) return fwd_for_n<4>(n, s, i, l, q, std::make_integer_sequence<int, 4>{});
     if (m == 8) return fwd_for_n<8>(n, s, i, l, q, std::make_integer_sequence<int, 8>{});
-    return select_wide_fwd(m, n, q);
+    return select_wide_fwd(m, n, s, q);
 }
 
 BwdFn select_bwd(int m, int n, bool l, bool adam, float tau)

@@ -81,57 +81,25 @@ __device__ __forceinline__ float min4(const float (&x)[4])
     return fminf(fminf(x[0], x[1]), fminf(x[2], x[3]));
 }
 
-// Adds, for lane distances D..L-1, how many entries of lane (lane ^ D) beat
-// each of this lane's entries (ties go to the lower index).
-template <int L, int D>
-__device__ __forceinline__ void rank_against_lane(const float (&k)[4], int part, int (&rank)[4])
+// Hard top-n by a bitonic sort of the group (descending), entry i = 4 part + e
+// of the group at lane `part`, slot e.  Each key travels with its index.  An
+// entry beats another when its key is larger, or (kTies) equal with a lower
+// index: the order of the ranks, ties to the lower index.  Without kTies the
+// keys must be distinct for the result to mean anything (the caller checks).
+// A stage (kk, j) pairs entry i with i ^ j; the pair is ordered descending
+// when (i & kk) == 0 and ascending otherwise, the lower entry of a
+// descending pair keeping the entry that beats.  j = 1, 2 pair slots of one
+// lane; j >= 4 pairs lane part with lane part ^ (j / 4), each lane keeping
+// one side of its four pairs.  The network is log2(m) (log2(m) + 1) / 2
+// stages of 4 entries per lane, against m comparisons per entry for counting
+// ranks, and keeps few values live.
+template <bool kTies>
+__device__ __forceinline__ bool beats(float ka, int ia, float kb, int ib)
 {
-    if constexpr (D < L) {
-        float o[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = lane_xor<D>(k[e]);
-        const bool lower = (part ^ D) < part; // that lane's entries have lower indices
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-#pragma unroll
-            for (int f = 0; f < 4; ++f) {
-                const bool beats = lower ? (o[f] >= k[e]) : (o[f] > k[e]);
-                rank[e] += beats ? 1 : 0;
-            }
-        }
-        rank_against_lane<L, D + 1>(k, part, rank);
-    }
+    return kTies ? (ka > kb || (ka == kb && ia < ib)) : ka > kb;
 }
 
-// Keys of the group beaten-by counts: rank[e] = number of entries of the group
-// that beat this lane's entry e (kappa_i > kappa_j, or equal and i < j).
-template <int L>
-__device__ __forceinline__ void wide_rank(const float (&k)[4], int part, int (&rank)[4])
-{
-#pragma unroll
-    for (int e = 0; e < 4; ++e) rank[e] = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-        for (int j = i + 1; j < 4; ++j) {
-            const bool i_wins = k[i] >= k[j];
-            rank[j] += i_wins ? 1 : 0;
-            rank[i] += i_wins ? 0 : 1;
-        }
-    }
-    rank_against_lane<L, 1>(k, part, rank);
-}
-
-// Hard top-n from the hardware-log keys by a bitonic sort of the group
-// (descending), entry i = 4 part + e of the group at lane `part`, slot e.
-// Each key travels with its index.  A stage (kk, j) pairs entry i with
-// i ^ j; the pair is ordered descending when (i & kk) == 0 and ascending
-// otherwise, the lower entry of a descending pair keeping the larger key.
-// j = 1, 2 pair slots of one lane; j >= 4 pairs lane part with lane
-// part ^ (j / 4), each lane keeping one side of its four pairs.  The
-// network is log2(m) (log2(m) + 1) / 2 stages of 4 entries per lane, against
-// m comparisons per entry for counting ranks.
-template <int KK, int J>
+template <int KK, int J, bool kTies>
 __device__ __forceinline__ void bitonic_stage(float (&k)[4], int (&ix)[4], int part)
 {
     if constexpr (J < 4) {
@@ -141,7 +109,7 @@ __device__ __forceinline__ void bitonic_stage(float (&k)[4], int (&ix)[4], int p
             const int hi = lo | J;
             // direction of the pair: (i & KK) with i = 4 part + lo
             const bool desc = KK < 4 ? ((lo & KK) == 0) : ((part & (KK >> 2)) == 0);
-            const bool sw = (k[hi] > k[lo]) == desc;
+            const bool sw = beats<kTies>(k[hi], ix[hi], k[lo], ix[lo]) == desc;
             const float kl = k[lo], kh = k[hi];
             const int il = ix[lo], ih = ix[hi];
             k[lo] = sw ? kh : kl;
@@ -158,52 +126,57 @@ __device__ __forceinline__ void bitonic_stage(float (&k)[4], int (&ix)[4], int p
         for (int e = 0; e < 4; ++e) {
             const float o = lane_xor<D>(k[e]);
             const int oi = __float_as_int(lane_xor<D>(__int_as_float(ix[e])));
-            const bool take = (o > k[e]) == keep_max;
+            const bool take = beats<kTies>(o, oi, k[e], ix[e]) == keep_max;
             k[e] = take ? o : k[e];
             ix[e] = take ? oi : ix[e];
         }
     }
 }
 
-template <int M, int KK, int J>
+template <int M, int KK, int J, bool kTies>
 __device__ __forceinline__ void bitonic_from(float (&k)[4], int (&ix)[4], int part)
 {
-    bitonic_stage<KK, J>(k, ix, part);
+    bitonic_stage<KK, J, kTies>(k, ix, part);
     if constexpr (J > 1)
-        bitonic_from<M, KK, J / 2>(k, ix, part);
+        bitonic_from<M, KK, J / 2, kTies>(k, ix, part);
     else if constexpr (KK < M)
-        bitonic_from<M, KK * 2, KK>(k, ix, part);
+        bitonic_from<M, KK * 2, KK, kTies>(k, ix, part);
 }
 
-// Sorts the group's hardware-log keys and returns whether every two keys of
+// Sorts the group's keys (four per lane, kf) and sets keep[e] (is this lane's
+// entry e among the n that beat the others) and sidx[e] (the index within the
+// group of the entry at sorted position 4 part + e, i.e. of rank 4 part + e).
+// For the hardware-log keys (kTies false) it returns whether every two keys of
 // the group are further apart than the margin of their errors (noise.hpp):
 // then the order is the exact keys' order and no two tie, and checking the
-// m - 1 pairs adjacent in the sorted order covers every pair.  On return
-// keep[e] tells whether this lane's entry e is among the n largest, and
-// sidx[e] is the index (within the group) of the entry at sorted position
-// 4 part + e.
-template <int L, int N>
-__device__ __forceinline__ bool wide_top_fast(const float (&kf)[4], int part, bool (&keep)[4],
-                                              int (&sidx)[4])
+// m - 1 pairs adjacent in the sorted order covers every pair.  For exact keys
+// (kTies) ties go to the lower index and the return value is true.
+template <int L, int N, bool kTies>
+__device__ __forceinline__ bool wide_top(const float (&kf)[4], int part, bool (&keep)[4],
+                                         int (&sidx)[4])
 {
     constexpr int M = 4 * L;
-    float big = fmaxf(fmaxf(fabsf(kf[0]), fabsf(kf[1])), fmaxf(fabsf(kf[2]), fabsf(kf[3])));
-    big = group_max<L>(big);
-    const float margin = __builtin_fmaf(big, 0x1p-20f, kFastPairMargin);
     float k[4] = {kf[0], kf[1], kf[2], kf[3]};
 #pragma unroll
     for (int e = 0; e < 4; ++e) sidx[e] = 4 * part + e;
-    bitonic_from<M, 2, 1>(k, sidx, part);
+    bitonic_from<M, 2, 1, kTies>(k, sidx, part);
+    const int lane = (int)(threadIdx.x & 63);
+    // the entry of rank n - 1, held by lane (n - 1) / 4 of the group
+    const int src = lane - part + (N - 1) / 4;
+    const float kth = __shfl(k[(N - 1) % 4], src);
+    const int ith = __shfl(sidx[(N - 1) % 4], src);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        keep[e] = kTies ? !beats<true>(kth, ith, kf[e], 4 * part + e) : kf[e] >= kth;
+    if constexpr (kTies) return true;
+    float big = fmaxf(fmaxf(fabsf(kf[0]), fabsf(kf[1])), fmaxf(fabsf(kf[2]), fabsf(kf[3])));
+    big = group_max<L>(big);
+    const float margin = __builtin_fmaf(big, 0x1p-20f, kFastPairMargin);
     // adjacent sorted pairs: three in the lane, and the lane's last with the
     // next lane's first (the group's last lane has no successor)
     bool sep = (k[0] - k[1] > margin) & (k[1] - k[2] > margin) & (k[2] - k[3] > margin);
-    const int lane = (int)(threadIdx.x & 63);
     const float next = __shfl(k[0], part + 1 < L ? lane + 1 : lane);
     sep &= (part + 1 == L) || (k[3] - next > margin);
-    // the n-th largest key, held by lane (n - 1) / 4 of the group
-    const float kth = __shfl(k[(N - 1) % 4], lane - part + (N - 1) / 4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) keep[e] = kf[e] >= kth;
     return sep;
 }
 
@@ -332,8 +305,12 @@ __device__ __forceinline__ void wide_keys(const float (&phi)[4], uint32_t block,
     }
 }
 
+// Forward.  Without kRelax (the straight-through forward with neither the
+// soft mask nor the soft output) the ranks come from the hardware-log keys,
+// and a wave with any group closer than their margin recomputes the exact
+// keys; with kRelax the exact keys are needed for the relaxation anyway.
 // kQ: how the exp-domain recursion raises omega to 1 / tau (relax.hpp pow_q).
-template <int M, int N, int kQ>
+template <int M, int N, bool kRelax, int kQ>
 __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
 {
     constexpr int L = M / 4;
@@ -353,57 +330,45 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
         const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
         const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
         float kappa[4];
-        int rank[4];
-        const bool relax = pc.S || a.soft; // uniform over the launch
-        bool decided = false;
         bool keep[4];
         int sidx[4];
-        if (!relax) {
-            // Comparisons only: the hardware-log keys decide when every pair of
-            // every group in the wave is further apart than the margin (else
-            // the whole wave takes the exact keys: the ranks are cross-lane).
+        bool decided = false;
+        if constexpr (!kRelax) {
             const uint4 x = philox_block(pc.block0 + (uint32_t)slot, key);
             const float kf[4] = {fast_key_log2(phi[0], a.key_c, x.x),
                                  fast_key_log2(phi[1], a.key_c, x.y),
                                  fast_key_log2(phi[2], a.key_c, x.z),
                                  fast_key_log2(phi[3], a.key_c, x.w)};
-            decided = __all(wide_top_fast<L, N>(kf, part, keep, sidx));
+            decided = __all(wide_top<L, N, false>(kf, part, keep, sidx));
         }
         if (!decided) {
             wide_keys(phi, pc.block0 + (uint32_t)slot, key, a.lambda, tab, kappa);
-            wide_rank<L>(kappa, part, rank);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) keep[e] = rank[e] < N;
+            wide_top<L, N, true>(kappa, part, keep, sidx);
         }
-        if (!a.soft) {
+        const bool soft = kRelax && a.soft;
+        if (!soft) {
             const uint32_t m01 = (keep[0] ? 0x0000FFFFu : 0u) | (keep[1] ? 0xFFFF0000u : 0u);
             const uint32_t m23 = (keep[2] ? 0x0000FFFFu : 0u) | (keep[3] ? 0xFFFF0000u : 0u);
             const u32x2 out = {wv.x & m01, wv.y & m23};
             stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
         }
         if (pc.idx) {
-            if (decided) {
-                // this lane holds sorted positions 4 part .. 4 part + 3
-                uint8_t* dst = pc.idx + group * N + 4 * part;
-                if (4 * part + 4 <= N) {
-                    const uint32_t w = (uint32_t)sidx[0] | ((uint32_t)sidx[1] << 8) |
-                                       ((uint32_t)sidx[2] << 16) | ((uint32_t)sidx[3] << 24);
-                    if constexpr (N % 4 == 0)
-                        stream_store(w, reinterpret_cast<uint32_t*>(dst));
-                    else
-                        for (int e = 0; e < 4; ++e) dst[e] = (uint8_t)(w >> (8 * e));
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (4 * part + e < N) dst[e] = (uint8_t)sidx[e];
-                }
+            // this lane holds ranks 4 part .. 4 part + 3
+            uint8_t* dst = pc.idx + group * N + 4 * part;
+            if (4 * part + 4 <= N) {
+                const uint32_t w = (uint32_t)sidx[0] | ((uint32_t)sidx[1] << 8) |
+                                   ((uint32_t)sidx[2] << 16) | ((uint32_t)sidx[3] << 24);
+                if constexpr (N % 4 == 0)
+                    stream_store(w, reinterpret_cast<uint32_t*>(dst));
+                else
+                    for (int e = 0; e < 4; ++e) dst[e] = (uint8_t)(w >> (8 * e));
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    if (rank[e] < N) pc.idx[group * N + rank[e]] = (uint8_t)(part * 4 + e);
+                    if (4 * part + e < N) dst[e] = (uint8_t)sidx[e];
             }
         }
-        if (pc.S || a.soft) {
+        if constexpr (kRelax) {
             float S[4];
             StepRec<4> unused[N]; // not written when records are not kept
             wide_relax_forward<L, N, false, kQ>(kappa, kLog2e * a.inv_tau, a.inv_tau, a.exp_span,
@@ -412,7 +377,7 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
                 const f32x4 sv = {S[0], S[1], S[2], S[3]};
                 stream_store(sv, reinterpret_cast<f32x4*>(pc.S + slot * 4));
             }
-            if (a.soft) { // pure soft forward: W (.) S, rounded to bf16
+            if (soft) { // pure soft forward: W (.) S, rounded to bf16
                 const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
                 const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
                 const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
@@ -487,10 +452,11 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
 }
 
 template <int M, int N>
-FwdFn wide_fwd_q(int q)
+FwdFn wide_fwd_q(bool relax, int q)
 {
-    return q == 1 ? fwd_wide_kernel<M, N, 1>
-                  : (q == 2 ? fwd_wide_kernel<M, N, 2> : fwd_wide_kernel<M, N, 0>);
+    if (!relax) return fwd_wide_kernel<M, N, false, 0>; // no relaxation
+    return q == 1 ? fwd_wide_kernel<M, N, true, 1>
+                  : (q == 2 ? fwd_wide_kernel<M, N, true, 2> : fwd_wide_kernel<M, N, true, 0>);
 }
 
 template <int M, int N, bool A>
@@ -501,10 +467,10 @@ BwdFn wide_bwd_q(int q)
 }
 
 template <int M, int... Ns>
-FwdFn wide_fwd_for_n(int n, int q, std::integer_sequence<int, Ns...>)
+FwdFn wide_fwd_for_n(int n, bool relax, int q, std::integer_sequence<int, Ns...>)
 {
     FwdFn f = nullptr;
-    ((n == Ns + 1 ? (f = wide_fwd_q<M, Ns + 1>(q), 0) : 0), ...);
+    ((n == Ns + 1 ? (f = wide_fwd_q<M, Ns + 1>(relax, q), 0) : 0), ...);
     return f;
 }
 
@@ -520,10 +486,10 @@ BwdFn wide_bwd_for_n(int n, bool adam, int q, std::integer_sequence<int, Ns...>)
 
 } // namespace
 
-FwdFn select_wide_fwd(int m, int n, int q)
+FwdFn select_wide_fwd(int m, int n, bool relax, int q)
 {
-    if (m == 16) return wide_fwd_for_n<16>(n, q, std::make_integer_sequence<int, 16>{});
-    if (m == 32) return wide_fwd_for_n<32>(n, q, std::make_integer_sequence<int, 32>{});
+    if (m == 16) return wide_fwd_for_n<16>(n, relax, q, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_fwd_for_n<32>(n, relax, q, std::make_integer_sequence<int, 32>{});
     return nullptr;
 }
 
