@@ -19,7 +19,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libroi.so")
-SOURCES = [os.path.join(CSRC, "roi.hip"), os.path.join(CSRC, "wide.hip"),
+SOURCES = [os.path.join(CSRC, "roi.hip"), os.path.join(CSRC, "wide_fwd.hip"),
+           os.path.join(CSRC, "wide_bwd.hip"),
            os.path.join(CSRC, "export.hip"), os.path.join(CSRC, "cat.hip")]
 ARCH = "gfx950"
 

@@ -1,0 +1,121 @@
+// wide_fwd.hip -- the forward kernel for groups of m = 16 and 32 weights
+// (helpers and layout in wide.hpp).
+#include <hip/hip_runtime.h>
+
+#include <utility>
+
+#include "wide.hpp"
+
+namespace roi {
+namespace {
+
+// Forward.  Without kRelax (the straight-through forward with neither the
+// soft mask nor the soft output) the ranks come from the hardware-log keys,
+// and a wave with any group closer than their margin recomputes the exact
+// keys; with kRelax the exact keys are needed for the relaxation anyway.
+// kQ: how the exp-domain recursion raises omega to 1 / tau (relax.hpp pow_q).
+template <int M, int N, bool kRelax, int kQ>
+__global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
+{
+    constexpr int L = M / 4;
+    __shared__ float2 tab[kLogCells];
+    fill_log_table(tab);
+    __syncthreads();
+    const FwdPiece& pc = a.p[find_piece(a)];
+    NoiseKey key = a.key_base;
+    key.block_hi = pc.block_hi;
+    const int64_t nslots = pc.ngroups * L;
+    const int64_t stride = (int64_t)pc.nblocks * kBlock;
+    for (int64_t slot = (int64_t)(blockIdx.x - pc.first_block) * kBlock + threadIdx.x;
+         slot < nslots; slot += stride) {
+        const int part = (int)(slot % L);
+        const int64_t group = slot / L;
+        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
+        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
+        const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
+        float kappa[4];
+        bool keep[4];
+        int sidx[4];
+        bool decided = false;
+        if constexpr (!kRelax) {
+            const uint4 x = philox_block(pc.block0 + (uint32_t)slot, key);
+            const float kf[4] = {fast_key_log2(phi[0], a.key_c, x.x),
+                                 fast_key_log2(phi[1], a.key_c, x.y),
+                                 fast_key_log2(phi[2], a.key_c, x.z),
+                                 fast_key_log2(phi[3], a.key_c, x.w)};
+            decided = __all(wide_top<L, N, false>(kf, part, keep, sidx));
+        }
+        if (!decided) {
+            wide_keys(phi, pc.block0 + (uint32_t)slot, key, a.lambda, tab, kappa);
+            wide_top<L, N, true>(kappa, part, keep, sidx);
+        }
+        const bool soft = kRelax && a.soft;
+        if (!soft) {
+            const uint32_t m01 = (keep[0] ? 0x0000FFFFu : 0u) | (keep[1] ? 0xFFFF0000u : 0u);
+            const uint32_t m23 = (keep[2] ? 0x0000FFFFu : 0u) | (keep[3] ? 0xFFFF0000u : 0u);
+            const u32x2 out = {wv.x & m01, wv.y & m23};
+            stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
+        }
+        if (pc.idx) {
+            // this lane holds ranks 4 part .. 4 part + 3
+            uint8_t* dst = pc.idx + group * N + 4 * part;
+            if (4 * part + 4 <= N) {
+                const uint32_t w = (uint32_t)sidx[0] | ((uint32_t)sidx[1] << 8) |
+                                   ((uint32_t)sidx[2] << 16) | ((uint32_t)sidx[3] << 24);
+                if constexpr (N % 4 == 0)
+                    stream_store(w, reinterpret_cast<uint32_t*>(dst));
+                else
+                    for (int e = 0; e < 4; ++e) dst[e] = (uint8_t)(w >> (8 * e));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * part + e < N) dst[e] = (uint8_t)sidx[e];
+            }
+        }
+        if constexpr (kRelax) {
+            float S[4];
+            StepRec<4> unused[N]; // not written when records are not kept
+            wide_relax_forward<L, N, false, kQ>(kappa, kLog2e * a.inv_tau, a.inv_tau, a.exp_span,
+                                                true, S, unused);
+            if (pc.S) {
+                const f32x4 sv = {S[0], S[1], S[2], S[3]};
+                stream_store(sv, reinterpret_cast<f32x4*>(pc.S + slot * 4));
+            }
+            if (soft) { // pure soft forward: W (.) S, rounded to bf16
+                const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
+                const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
+                const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
+                const uint32_t h3 = float_to_bf16_rne(bf16_bits_to_float(wv.y >> 16) * S[3]);
+                const u32x2 out = {h0 | (h1 << 16), h2 | (h3 << 16)};
+                stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
+            }
+        }
+    }
+}
+
+template <int M, int N>
+FwdFn wide_fwd_q(bool relax, int q)
+{
+    if (!relax) return fwd_wide_kernel<M, N, false, 0>; // no relaxation
+    return q == 1 ? fwd_wide_kernel<M, N, true, 1>
+                  : (q == 2 ? fwd_wide_kernel<M, N, true, 2> : fwd_wide_kernel<M, N, true, 0>);
+}
+
+template <int M, int... Ns>
+FwdFn wide_fwd_for_n(int n, bool relax, int q, std::integer_sequence<int, Ns...>)
+{
+    FwdFn f = nullptr;
+    ((n == Ns + 1 ? (f = wide_fwd_q<M, Ns + 1>(relax, q), 0) : 0), ...);
+    return f;
+}
+
+} // namespace
+
+FwdFn select_wide_fwd(int m, int n, bool relax, int q)
+{
+    if (m == 16) return wide_fwd_for_n<16>(n, relax, q, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_fwd_for_n<32>(n, relax, q, std::make_integer_sequence<int, 32>{});
+    return nullptr;
+}
+
+} // namespace roi
