@@ -818,7 +818,10 @@ def test_full_qwen15b_stack_wide(dev, name, n, m):
 SOFT = [(37, 36, 2, 4, 1.0, 1.0, 3, 1, 0), (64, 96, 2, 4, 0.1, 1.0, 5, 9, 8),
         (33, 64, 3, 4, 1.3, 0.6, 2, 3, 12), (61, 88, 4, 8, 0.5, 1.0, 8, 5, 8),
         (37, 48, 8, 16, 1.0, 1.0, 2, 0, 0), (33, 96, 16, 32, 1.0, 1.0, 4, 2, 0),
-        (13, 64, 5, 32, 0.3, 0.8, 5, 3, 64)]
+        (13, 64, 5, 32, 0.3, 0.8, 5, 3, 64),
+        # the exp-domain relaxation with powers by multiplication (tau = 1/2) and
+        # by exp2 / log2 (tau = 0.7) in the wide kernels
+        (37, 48, 8, 16, 0.5, 1.0, 6, 2, 16), (33, 96, 16, 32, 0.7, 1.3, 7, 4, 0)]
 
 
 @pytest.mark.parametrize("case", SOFT, ids=lambda c: "x".join(map(str, c[:4])))
