@@ -236,8 +236,9 @@ __device__ __forceinline__ void relax_forward_exp(const float (&b)[M], float bma
 }
 
 // Reverse sweep of relax_forward / relax_forward_exp: given sbar = dL/dS,
-// returns dL/dkappa (in the units of the keys times 1/tau's scale, as the
-// caller's b).  Chain rule through the recursion, with a = dL/dalpha^(k+1)
+// returns dL/dkappa for kappa in natural units (the records are unit-free, so
+// the units the caller's keys had when forming b do not matter; the 1/tau is
+// that of softmax(alpha / tau)).  Chain rule through the recursion, with a = dL/dalpha^(k+1)
 // (0 above the last step), omega = 1 - mu^(k),
 //   mubar_j = sbar_j - a_j / omega_j,
 //   dL/dalpha^(k)_j = a_j + (mu_j / tau) (mubar_j - sum_l mu_l mubar_l).
