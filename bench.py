@@ -33,15 +33,41 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "roi_mask_qwen7b_stack_2of4_traffi
 KERNEL_SOURCES = ("roi.hip", "common.hpp", "noise.hpp", "relax.hpp", "host.hpp")
 
 
+def code_only(text: str) -> str:
+    """C/C++ source without its comments, whitespace collapsed (string and
+    character literals kept as they are)."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash() -> str:
-    """Hash of the sources of the measured kernels: measured traffic is
-    reported only while they are unchanged."""
+    """Hash of the code of the measured kernels' sources (comments and
+    whitespace aside): measured traffic is reported only while it is
+    unchanged."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_23048_amd", "csrc")
     for name in KERNEL_SOURCES:
         h.update(name.encode())
-        h.update(open(os.path.join(csrc, name), "rb").read())
+        h.update(code_only(open(os.path.join(csrc, name)).read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -1,6 +1,6 @@
 """bench.py's host-side contract (no GPU needed): more than one GPU is refused
-with a message, the traffic record matches its kernels' sources, and the
-counter summary keeps only full-size dispatches."""
+with a message, the traffic record matches its kernels' code (comments
+aside), and the counter summary keeps only full-size dispatches."""
 from __future__ import annotations
 
 import csv
@@ -29,6 +29,16 @@ def test_traffic_record_matches_the_kernel_sources():
     assert rec["kernel_source_hash"] == bench.kernel_source_hash()
     for k in ("fwd_lane_kernel", "bwd_lane_kernel"):
         assert abs(rec["kernels"][k]["traffic_over_algorithmic"] - 1.0) < 1e-3
+
+
+def test_source_hash_ignores_comments_only():
+    """The record stays valid across comment and layout edits of the kernel
+    sources, and no longer matches once their code changes."""
+    src = 'int f(int a) { // add one\n  return a + 1; /* done */ }\nconst char* s = "x//y";'
+    assert bench.code_only(src) == bench.code_only(
+        "/* header */\nint f(int a)\n{\n    return a + 1;\n}\nconst char* s = \"x//y\";  // end")
+    assert bench.code_only(src) != bench.code_only(src.replace("a + 1", "a + 2"))
+    assert bench.code_only(src) != bench.code_only(src.replace('"x//y"', '"x/y"'))
 
 
 def _counters(path, rows):
