@@ -216,10 +216,11 @@ __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], floa
             sums_but_one<4>(ex, others, t);
             const float ext = sum_other_lanes<L>(t);
             const float inv_total = __builtin_amdgcn_rcpf(t + ext);
+            const float ext_w = ext * inv_total; // the other lanes' weight
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const float mu = ex[e] * inv_total;
-                const float om = (others[e] + ext) * inv_total;
+                const float om = __builtin_fmaf(others[e], inv_total, ext_w);
                 if (want_s) S[e] += mu;
                 if (kKeep) {
                     rec[k].mu[e] = mu;
@@ -240,10 +241,11 @@ __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], floa
         sums_but_one<4>(ex, others, t);
         const float ext = sum_other_lanes<L>(t);
         const float inv_total = __builtin_amdgcn_rcpf(t + ext);
+        const float ext_w = ext * inv_total; // the other lanes' weight
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const float mu = ex[e] * inv_total;
-            const float om = (others[e] + ext) * inv_total;
+            const float om = __builtin_fmaf(others[e], inv_total, ext_w);
             if (want_s) S[e] += mu;
             if (kKeep) {
                 rec[k].mu[e] = mu;
