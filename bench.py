@@ -439,7 +439,7 @@ def grouped_timing(grouped_step, steps, work):
     g_elapsed = time.perf_counter() - g0
     g_fwd = sum(e[0].elapsed_time(e[1]) for e in gev) / len(gev)
     g_bwd = sum(e[1].elapsed_time(e[2]) for e in gev) / len(gev)
-    per_launch = 16  # pieces per grid (common.hpp kMaxPieces)
+    per_launch = 32  # pieces per grid (common.hpp kMaxPieces)
     grouped = {"ms_per_step": g_elapsed * 1e3 / steps, "fwd_ms": g_fwd, "bwd_ms": g_bwd,
                "descriptors": len(work.tensors),
                "launches_per_step": 2 * -(-len(work.tensors) // per_launch)}

@@ -133,7 +133,7 @@ int roi_mask_bwd(const uint16_t* grad_W_masked, const uint16_t* W, const float* 
  * linear layer of a model), with the shared pattern, temperatures, seed and
  * step.  Tensor i is processed exactly as the single-tensor call with its own
  * pointers, rows, cols and elem_offset would process it (same outputs, bit
- * for bit); the library launches the work of up to 16 tensor pieces per grid
+ * for bit); the library launches the work of up to 32 tensor pieces per grid
  * instead of one grid per tensor.  The descriptor array is host memory, read
  * during the call only; the pointers in it follow the conventions above.
  * Tensors with rows * cols == 0 are skipped (their pointers may be NULL).

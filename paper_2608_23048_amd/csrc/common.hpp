@@ -20,7 +20,8 @@ constexpr int kBlock = 256;
 // one tensor whose Philox block indices share their high 32 bits.  Piece i
 // owns the launch's blocks [first_block, first_block + nblocks); its blocks
 // stride over the piece when it has more groups than blocks cover.
-constexpr int kMaxPieces = 16;
+constexpr int kMaxPieces = 32;
+static_assert((kMaxPieces & (kMaxPieces - 1)) == 0, "binary search over the pieces");
 
 struct FwdPiece {
     const uint16_t* W;
@@ -34,7 +35,11 @@ struct FwdPiece {
     uint32_t first_block, nblocks;
 };
 
+// starts[i]: the first block of piece i (= p[i].first_block), and 0xFFFFFFFF
+// for the unused entries, contiguous so that a block finds its piece from two
+// wide scalar loads.
 struct FwdBatch {
+    uint32_t starts[kMaxPieces];
     FwdPiece p[kMaxPieces];
     int count;
     NoiseKey key_base; // key_base.block_hi is replaced by the piece's
@@ -70,6 +75,7 @@ struct AdamStep {
 };
 
 struct BwdBatch {
+    uint32_t starts[kMaxPieces]; // as in FwdBatch
     BwdPiece p[kMaxPieces];
     int count;
     NoiseKey key_base; // key_base.block_hi is replaced by the piece's
@@ -80,6 +86,9 @@ struct BwdBatch {
     float exp_span; // key-span limit of the exp-domain relaxation (relax.hpp)
     AdamStep adam;
 };
+
+// A batch travels as the kernel's argument block, which is at most 4 KiB.
+static_assert(sizeof(FwdBatch) <= 4096 && sizeof(BwdBatch) <= 4096, "kernel arguments");
 
 // The fused AdamW update of one logit from its gradient g (fp32, fast
 // reciprocal and square root: the result is held to the float tolerance).
@@ -92,14 +101,20 @@ __device__ __forceinline__ void adamw_update(const AdamStep& a, float g, float& 
     phi = __builtin_fmaf(-a.step_size * m, __builtin_amdgcn_rcpf(den), phi * a.decay);
 }
 
-// The piece that owns this block (the table is in the kernel arguments; the
-// scan is uniform over the block).
+// The piece that owns this block: the last piece that starts at or before it,
+// by binary search over the starts (unused entries are 0xFFFFFFFF).  Every
+// wave of every block runs this on the CU's shared scalar unit, and a launch
+// has millions of blocks of a few microseconds each, so it is kept to a few
+// scalar instructions: none for a single piece, five steps otherwise.
 template <typename Batch>
 __device__ __forceinline__ int find_piece(const Batch& a)
 {
+    if (a.count == 1) return 0;
     const uint32_t b = blockIdx.x;
     int i = 0;
-    while (i + 1 < a.count && b >= a.p[i + 1].first_block) ++i;
+#pragma unroll
+    for (int step = kMaxPieces / 2; step >= 1; step /= 2)
+        if (b >= a.starts[i + step]) i += step;
     return i;
 }
 

@@ -667,8 +667,11 @@ struct Launcher {
         const int64_t nb = std::min(blocks_for(pc.ngroups, m, fwd), max_blocks());
         if (batch.count == kMaxPieces || blocks + nb > max_blocks())
             if (int st = flush()) return st;
+        if (batch.count == 0)
+            for (uint32_t& s : batch.starts) s = 0xFFFFFFFFu;
         pc.first_block = (uint32_t)blocks;
         pc.nblocks = (uint32_t)nb;
+        batch.starts[batch.count] = pc.first_block;
         batch.p[batch.count++] = pc;
         blocks += nb;
         return ROI_OK;

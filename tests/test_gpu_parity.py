@@ -339,7 +339,7 @@ def test_split_calls_equal_one_slab_call(dev, tau):
                 f"grad_logits differs, tensor at {o}"
 
 
-def grouped_inputs(dev, m, count=20, seed=5):
+def grouped_inputs(dev, m, count=40, seed=5):
     """`count` separately allocated tensors of mixed shapes (cols % 32 == 0),
     one of them empty, with stack offsets except one piece placed just below
     a multiple of 2^34 elements, so that its noise crosses the boundary."""
@@ -511,7 +511,7 @@ def test_bwd_adamw_three_steps(dev):
 def test_bwd_adamw_grouped_equals_single(dev):
     import torch
     say("bwd+adamw grouped vs single")
-    tensors, offs = grouped_inputs(dev, 4, count=18, seed=21)
+    tensors, offs = grouped_inputs(dev, 4, count=36, seed=21)
     opt = roi.adamw_params(1e-3, t=4)
     states = []
     for W, L, G in tensors:
