@@ -263,14 +263,23 @@ __device__ __forceinline__ void fast_keys(const float (&phi)[M], const uint32_t 
 template <int M, int N, bool kRelax, bool kWantIdx, bool kLambdaOne, int kQ>
 __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
 {
-    __shared__ float2 tab[kLogCells];
-    __shared__ Top4Entry top4[64];
-    fill_log_table(tab);
-    if constexpr (M == 4) {
-        if (threadIdx.x >= kLogCells && threadIdx.x < kLogCells + 64)
-            top4[threadIdx.x - kLogCells] = kTop4Table<N>.e[threadIdx.x - kLogCells];
+    // LDS copies of the tables: the top-2-of-4 table (read by every group at
+    // m = 4) and the log cells (read by the exact keys).  Without either use on
+    // the common path (m = 8 without the relaxation: exact keys only for
+    // groups with near ties) the cells are read from global memory, where
+    // they stay cached, and a block starts streaming without a barrier.
+    constexpr bool kLds = M == 4 || kRelax;
+    __shared__ float2 tab_lds[kLds ? kLogCells : 1];
+    __shared__ Top4Entry top4[M == 4 ? 64 : 1];
+    const float2* tab = kLds ? tab_lds : kLogCellTable.cell;
+    if constexpr (kLds) {
+        fill_log_table(tab_lds);
+        if constexpr (M == 4) {
+            if (threadIdx.x >= kLogCells && threadIdx.x < kLogCells + 64)
+                top4[threadIdx.x - kLogCells] = kTop4Table<N>.e[threadIdx.x - kLogCells];
+        }
+        __syncthreads();
     }
-    __syncthreads();
     const FwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;

@@ -18,9 +18,15 @@ template <int M, int N, bool kRelax, int kQ>
 __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
 {
     constexpr int L = M / 4;
-    __shared__ float2 tab[kLogCells];
-    fill_log_table(tab);
-    __syncthreads();
+    // The exact keys read the log cells: from LDS when every group needs them
+    // (kRelax), else (only groups of waves with near ties) from global memory,
+    // where they stay cached, so that a block starts without a barrier.
+    __shared__ float2 tab_lds[kRelax ? kLogCells : 1];
+    const float2* tab = kRelax ? tab_lds : kLogCellTable.cell;
+    if constexpr (kRelax) {
+        fill_log_table(tab_lds);
+        __syncthreads();
+    }
     const FwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
