@@ -814,6 +814,89 @@ def test_full_qwen15b_stack_wide(dev, name, n, m):
     full_workload_check(dev, name, n, m, 1.0, 0, 20000)
 
 
+def check_sampled(dev, W, L, G, Wm, idx, d, n, m, tau, step, picks):
+    """Sampled groups of a one-call slab against the oracle (indices and masked
+    weights bit for bit, gradient within the tolerance)."""
+    import torch
+    pt = torch.from_numpy(picks).to(dev)
+    take = lambda t: t.view(-1, m).index_select(0, pt)
+    Wg, Lg = take(W), take(L)
+    tau32 = float(np.float32(tau))
+    ge = picks.astype(np.uint64) * np.uint64(m)
+    if Wm is not None:
+        Wm_o, _, idx_o = oracle.mask_fwd_groups(bf16_bits(Wg), f32(Lg), ge, n, m, tau32, 1.0, 0,
+                                                step, want_soft=False)
+        assert np.array_equal(idx.index_select(0, pt).cpu().numpy(), idx_o), "indices differ"
+        assert np.array_equal(bf16_bits(take(Wm)), Wm_o), "masked weights differ"
+    if d is not None:
+        d_o = oracle.mask_bwd_groups(bf16_bits(take(G)), bf16_bits(Wg), f32(Lg), ge, n, m, tau32,
+                                     1.0, 0, step)
+        return assert_close(f32(take(d)), d_o, "grad_logits")
+    return 0.0
+
+
+def test_launch_beyond_2e32_work_items(dev):
+    """A slab of 2^34 + 2^28 weights in one call.  Its first piece (2^34
+    elements, up to the Philox block index's high-word change) needs 2^32
+    work-items in the backward at m = 4 (one group per lane) and in both wide
+    kernels at m = 16 (four elements per lane), one block more than a dispatch
+    can hold: the grid is capped and its last 256 work-items run in the
+    kernels' stride loops.  The second piece goes to a launch of its own.
+    Sampled groups (random, around the 2^34 boundary, and those reached by
+    the stride loops) against the oracle; every group keeps exactly n."""
+    import torch
+    E = (1 << 34) + (1 << 28)
+    cols = 4096
+    rows = E // cols
+    say(f"beyond 2^32 work-items: allocating {E} weights")
+    W = torch.empty(E, dtype=torch.bfloat16, device=dev)
+    L = torch.empty(E, dtype=torch.float32, device=dev)
+    gen = torch.Generator(device=dev).manual_seed(77)
+    for c0 in range(0, E, 1 << 30):
+        c1 = min(E, c0 + (1 << 30))
+        L[c0:c1].normal_(0.0, 1.0, generator=gen)
+        W[c0:c1] = (L[c0:c1] * 0.02).to(torch.bfloat16)  # any bf16 values of weight scale
+    L.normal_(0.0, 1.0, generator=gen)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(99)
+    for n, m, tau, step in ((2, 4, 0.7, 3), (8, 16, 1.0, 5)):
+        ng = E // m
+        first = (1 << 34) // m  # groups of the first piece
+        # work-items of the largest grid of 256-thread blocks; the backward at
+        # m = 4 has one group per work-item, the wide kernels m / 4 per group
+        capped = (0xFFFFFFFF // 256) * 256
+        in_grid = capped if m == 4 else capped // (m // 4)  # groups before the stride loop
+        picks = np.unique(np.concatenate([
+            rng.integers(0, ng, 4000), np.arange(first - 300, first + 300),
+            np.arange(in_grid - 8, min(first, in_grid + 300)), [0, ng - 1]]))
+        say(f"  {n}:{m}: forward")
+        Wm, _, idx = roi.mask_fwd(W.view(rows, cols), L.view(rows, cols), n, m, tau, 1.0, 0, step,
+                                  0, want_soft=False)
+        torch.cuda.synchronize()
+        chunk = 1 << 26
+        for g0 in range(0, ng, chunk):
+            g1 = min(ng, g0 + chunk)
+            hard = torch.zeros((g1 - g0, m), dtype=torch.bool, device=dev)
+            hard.scatter_(1, idx[g0:g1].long(), True)
+            assert bool((hard.sum(1) == n).all()), "a group does not keep exactly n entries"
+            del hard
+        check_sampled(dev, W, L, None, Wm.view(-1), idx, None, n, m, tau, step, picks)
+        del idx
+        say(f"  {n}:{m}: backward")
+        G = Wm.view(-1)  # the masked weights serve as an upstream gradient of bf16 values
+        d = roi.mask_bwd(G.view(rows, cols), W.view(rows, cols), L.view(rows, cols), n, m, tau,
+                         1.0, 0, step, 0)
+        torch.cuda.synchronize()
+        for g0 in range(0, E, 1 << 30):
+            assert bool(torch.isfinite(d.view(-1)[g0:g0 + (1 << 30)]).all())
+        r = check_sampled(dev, W, L, G, None, None, d.view(-1), n, m, tau, step, picks)
+        say(f"  ok: {picks.size} sampled groups, grad err/bound {r:.3f}")
+        del Wm, G, d
+        torch.cuda.empty_cache()
+    del W, L
+    torch.cuda.empty_cache()
+
+
 # --------------------------------------------------------------------------- pure soft forward
 SOFT = [(37, 36, 2, 4, 1.0, 1.0, 3, 1, 0), (64, 96, 2, 4, 0.1, 1.0, 5, 9, 8),
         (33, 64, 3, 4, 1.3, 0.6, 2, 3, 12), (61, 88, 4, 8, 0.5, 1.0, 8, 5, 8),
