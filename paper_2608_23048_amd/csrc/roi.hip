@@ -263,14 +263,18 @@ __device__ __forceinline__ void fast_keys(const float (&phi)[M], const uint32_t 
 template <int M, int N, bool kRelax, bool kWantIdx, bool kLambdaOne, int kQ>
 __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
 {
-    // LDS copies of the tables: the top-2-of-4 table (read by every group at
-    // m = 4) and the log cells (read by the exact keys).  Without either use on
-    // the common path (m = 8 without the relaxation: exact keys only for
-    // groups with near ties) the cells are read from global memory, where
-    // they stay cached, and a block starts streaming without a barrier.
-    constexpr bool kLds = M == 4 || kRelax;
+    // Tables.  With the relaxation every group reads the log cells (exact
+    // keys), so the block copies them, and at m = 4 the top-2-of-4 table, into
+    // LDS.  Without it the cells serve only groups with near ties and are read
+    // from global memory, where they stay cached; and at m = 4 lane e of each
+    // wave holds entry e of the 64-entry top-2 table in registers, a group
+    // reading entry `code` from lane `code` (ds_bpermute, with every lane of
+    // the wave active).  A block then starts streaming without filling LDS or
+    // waiting at a barrier.
+    constexpr bool kLds = kRelax;
+    constexpr bool kLaneTable = M == 4 && !kRelax;
     __shared__ float2 tab_lds[kLds ? kLogCells : 1];
-    __shared__ Top4Entry top4[M == 4 ? 64 : 1];
+    __shared__ Top4Entry top4[M == 4 && kLds ? 64 : 1];
     const float2* tab = kLds ? tab_lds : kLogCellTable.cell;
     if constexpr (kLds) {
         fill_log_table(tab_lds);
@@ -280,6 +284,8 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
         }
         __syncthreads();
     }
+    Top4Entry lane_entry{};
+    if constexpr (kLaneTable) lane_entry = kTop4Table<N>.e[threadIdx.x & 63];
     const FwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
@@ -296,12 +302,18 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
             if (q < ng) {
                 load_logits<M>(pc.phi + q * M, phi[u]);
                 load_bf16<M>(pc.W + q * M, w[u]);
+            } else if constexpr (kLaneTable) { // a group past the end still looks up
+#pragma unroll
+                for (int j = 0; j < M; ++j) {
+                    phi[u][j] = 0.0f;
+                    w[u][j] = 0u;
+                }
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q >= ng) continue;
+            if (!kLaneTable && q >= ng) continue;
             uint32_t x[M];
             group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
             float kappa[M];
@@ -317,7 +329,22 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
                     exact_keys<M, kLambdaOne>(phi[u], x, a.lambda, tab, kappa);
             }
             const bool soft = kRelax && a.soft;
-            if constexpr (M == 4) {
+            if constexpr (kLaneTable) {
+                const int addr = (int)(top4_code(kappa) << 2); // byte address of lane `code`
+                const uint32_t m01 =
+                    (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)lane_entry.m01);
+                const uint32_t m23 =
+                    (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)lane_entry.m23);
+                const uint32_t order =
+                    kWantIdx ? (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)lane_entry.order)
+                             : 0u;
+                if (q < ng) {
+                    const u32x2 v = {(w[u][0] | (w[u][1] << 16)) & m01,
+                                     (w[u][2] | (w[u][3] << 16)) & m23};
+                    stream_store(v, reinterpret_cast<u32x2*>(pc.Wm + q * M));
+                    if (kWantIdx) store_order<N>(pc.idx + q * N, order);
+                }
+            } else if constexpr (M == 4) {
                 const Top4Entry t4 = top4[top4_code(kappa)];
                 if (!soft) {
                     const u32x2 v = {(w[u][0] | (w[u][1] << 16)) & t4.m01,
