@@ -212,10 +212,16 @@ __global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_fwd_kernel
     constexpr int C = Candidates<M, N>::C;
     constexpr int B = cat_block(C);
     constexpr bool kStage = cat_staged(C);
-    __shared__ float2 tab[kLogCells];
+    // The log cells in LDS only when every group takes the exact keys (kSoft);
+    // otherwise they serve groups whose top two keys are close and are read
+    // from global memory, where they stay cached.
+    __shared__ float2 tab_lds[kSoft ? kLogCells : 1];
     __shared__ float tile[kStage ? B * C : 2];
-    fill_log_table(tab);
-    __syncthreads();
+    const float2* tab = kSoft ? tab_lds : kLogCellTable.cell;
+    if constexpr (kSoft) {
+        fill_log_table(tab_lds);
+        __syncthreads();
+    }
     // The loop bound is uniform over the block (the tile copies are cooperative).
     for (int64_t base = (int64_t)blockIdx.x * B; base < a.ngroups; base += (int64_t)gridDim.x * B) {
         const int here = (int)(a.ngroups - base < B ? a.ngroups - base : B);
