@@ -277,7 +277,12 @@ __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
             if (has_next) {
                 const float om = rec[k].om[e];
                 const bool live = !kFloor || om >= kFltMin;
-                const float rinv = live ? __builtin_amdgcn_rcpf(om) : 0.0f;
+                // 1/inf = 0 for a floored entry.  Selecting the reciprocal's
+                // input, not its result, leaves the two copies of the sweep
+                // (with and without the selects) no reciprocal in common, so
+                // the compiler does not compute them ahead of the choice and
+                // hold them in registers beside the records.
+                const float rinv = __builtin_amdgcn_rcpf(live ? om : __builtin_inff());
                 mubar = __builtin_fmaf(-abar[e], rinv, sbar[e]);
                 a_in[e] = live ? abar[e] : 0.0f;
             }

@@ -9,12 +9,26 @@
 namespace roi {
 namespace {
 
+// Waves per SIMD of a kernel of v VGPRs (512 per SIMD lane, allocated in
+// blocks of 8, at most 8 waves).
+constexpr int waves_for_vgprs(int v)
+{
+    const int w = 512 / ((v + 7) / 8 * 8);
+    return w < 8 ? w : 8;
+}
+
 // Backward; with kAdam the AdamW step on the logits is fused in (as in the
 // per-lane kernels).
 template <int M, int N, bool kAdam, int kQ>
 __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
 {
     constexpr int L = M / 4;
+    // A select-free copy of the sweep beside the one with floor selects.  At
+    // m = 32 the kernel holds about 28 + 8n VGPRs (8 per step of records) and
+    // the second copy 8 more; at tau != 1 or with AdamW it needs far more.
+    // It is taken where it costs no wave per SIMD.
+    constexpr bool kTwoSweeps =
+        L <= 4 || (kQ == 1 && !kAdam && waves_for_vgprs(36 + 8 * N) == waves_for_vgprs(28 + 8 * N));
     const BwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
@@ -50,9 +64,8 @@ __global__ __launch_bounds__(kBlock) void bwd_wide_kernel(BwdBatch a)
         float abar[4];
         // Where every group of the wave took the exp-domain recursion, no
         // floor was reached and the sweep drops its selects (the two forms give
-        // the same bits there, so this choice may be the wave's).  At m = 32
-        // a second copy of the sweep would cost a wave per SIMD in registers.
-        if (L <= 4 && __all(exp_domain))
+        // the same bits there, so this choice may be the wave's).
+        if (kTwoSweeps && __all(exp_domain))
             wide_relax_backward<L, N, kQ == 1, false>(rec, sbar, a.inv_tau, abar);
         else
             wide_relax_backward<L, N, kQ == 1, true>(rec, sbar, a.inv_tau, abar);
