@@ -25,12 +25,19 @@ if ROOT not in sys.path:
 
 METRIC = "masked weights/sec (mask fwd+bwd) and achieved HBM GB/s vs peak, 7B-class 2:4"
 HBM_PEAK_GBPS = 8000.0
+# MI355X fp32 vector peak: 256 CUs x 128 fp32 lanes x 2 flops (fused multiply-add)
+# x 2.4 GHz.
+FP32_VECTOR_PEAK_TFLOPS = 157.3
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "roi_mask_qwen7b_stack_2of4_traffic.json")
+VALU_FILE = os.path.join(ROOT, "profiles", "roi_mask_valu_counters.json")
 
 
 # The sources the benchmark's two kernels (fwd_lane_kernel, bwd_lane_kernel
 # for m = 4 and 8) are compiled from.
 KERNEL_SOURCES = ("roi.hip", "common.hpp", "noise.hpp", "relax.hpp", "host.hpp")
+# ... and those of every straight-through forward and backward kernel (the
+# counter record covers the lane and the wide kernels).
+ALL_KERNEL_SOURCES = KERNEL_SOURCES + ("wide.hpp", "wide_fwd.hip", "wide_bwd.hip")
 
 
 def code_only(text: str) -> str:
@@ -58,14 +65,14 @@ def code_only(text: str) -> str:
     return " ".join("".join(out).split())
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
     """Hash of the code of the measured kernels' sources (comments and
-    whitespace aside): measured traffic is reported only while it is
+    whitespace aside): measured counters are reported only while it is
     unchanged."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_23048_amd", "csrc")
-    for name in KERNEL_SOURCES:
+    for name in sources:
         h.update(name.encode())
         h.update(code_only(open(os.path.join(csrc, name)).read()).encode())
     return h.hexdigest()[:16]
@@ -156,6 +163,118 @@ def algorithmic_bytes(n: int, m: int) -> tuple[float, float]:
     logits (fp32) and writes W_masked (bf16) and n/m index bytes; backward
     reads grad_W_masked and W (bf16) and the logits, and writes grad_logits."""
     return 2 + 4 + 2 + n / m, 2 + 2 + 4 + 4
+
+
+def backward_flops(n: int) -> int:
+    """Floating-point operations per weight of the backward, counted from the
+    algorithm (Gumbel keys, §3.2's relaxation recursion with the stable
+    log(1 - mu), and its reverse sweep), whatever the kernel does to get
+    there.  Each add, multiply, divide, comparison, exp and log counts 1; a
+    fused multiply-add counts 2.
+      keys          g = -log(-log u): 2 logs + 2 negations; kappa = phi/lambda
+                    + g as one fused multiply-add                          6
+      upstream      sbar = grad * W                                        1
+      each of the n steps of the recursion, per entry: the group maximum
+                    (1), (alpha - max) / tau (2), exp (1), its share of the
+                    total (1), mu = e / T (1), omega = (sum of the others) / T
+                    (2)                                                    8
+                    before the last step: max(omega, FLT_MIN), log, add    3
+      each of the n steps of the sweep, per entry: its share of <mu, mubar>
+                    (2), mubar - <mu, mubar> (1), times mu (1), times 1/tau
+                    (1), accumulate (1)                                    6
+                    before the last step: mubar = sbar - abar / omega      2
+      output        grad_logits = abar / lambda                            1
+    The Philox noise is integer work and not counted.  Total 19 n + 3."""
+    return 6 + 1 + 8 * n + 3 * (n - 1) + 6 * n + 2 * (n - 1) + 1
+
+
+def step_rooflines(workload: str, n: int, m: int, numel: int, fwd_ms: float, bwd_ms: float,
+                   traffic) -> dict:
+    """The step's two rooflines.  HBM: algorithmic bytes of the slower kernel
+    over its event time, against 8 TB/s.  ALU: the backward's algorithmic
+    flops (backward_flops) over its event time, against the fp32 vector peak,
+    with the measured VALU instruction counts beside it when the committed
+    record matches the kernels.  `roofline` is the one that bounds the path:
+    HBM for m = 4 and 8, whose relaxation is at most 4 steps per weight; ALU
+    for m = 16 and 32 (8 and 16 steps per weight, 155 and 307 flops)."""
+    bf, bb = algorithmic_bytes(n, m)
+    slow = ("roi_mask_bwd", bb, bwd_ms) if bwd_ms >= fwd_ms else ("roi_mask_fwd", bf, fwd_ms)
+    hbm_gbps = slow[1] * numel / (slow[2] * 1e-3) / 1e9
+    hbm = {"kernel": slow[0], "bound": "hbm", "achieved": hbm_gbps, "peak": HBM_PEAK_GBPS,
+           "unit": "GB/s", "frac": hbm_gbps / HBM_PEAK_GBPS, "traffic": traffic}
+    flops = backward_flops(n)
+    tflops = flops * numel / (bwd_ms * 1e-3) / 1e12
+    alu = {"kernel": "roi_mask_bwd", "bound": "alu", "achieved": tflops,
+           "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
+           "frac": tflops / FP32_VECTOR_PEAK_TFLOPS, "traffic": None,
+           "flops_per_weight": flops, "valu": None}
+    rec = measured_valu(workload)
+    key = "bwd_wide_kernel" if m >= 16 else "bwd_lane_kernel"
+    if rec and key in rec:
+        per_w = rec[key]["valu_lane_insts_per_weight"]
+        rate = per_w * numel / (bwd_ms * 1e-3) / 1e12
+        alu["valu"] = {"lane_insts_per_weight": per_w,
+                       "trans_lane_insts_per_weight": rec[key]["trans_lane_insts_per_weight"],
+                       "lane_insts_per_s_T": rate,
+                       "issue_peak_T": FP32_VECTOR_PEAK_TFLOPS / 2,
+                       "issue_frac": rate / (FP32_VECTOR_PEAK_TFLOPS / 2)}
+    if m >= 16:
+        return {"roofline": alu, "hbm_roofline": hbm}
+    return {"roofline": hbm, "alu_roofline": alu}
+
+
+def measured_valu(workload: str):
+    """The VALU counters of a workload's kernels from the committed rocprofv3
+    summary, or None when missing or the kernels changed since."""
+    if not os.path.exists(VALU_FILE):
+        return None
+    rec = json.load(open(VALU_FILE))
+    if rec.get("kernel_source_hash") != kernel_source_hash(ALL_KERNEL_SOURCES):
+        return None
+    return rec.get("workloads", {}).get(workload)
+
+
+def valu_summary(insts_csv, workload: str) -> int:
+    """Add one workload's VALU counters to the committed record, from a
+    rocprofv3 --pmc CSV of SQ_INSTS_VALU, SQ_INSTS_VALU_TRANS_F32 and SQ_WAVES
+    (wave instructions, summed over the chip).  Per kernel: the mean over its
+    full-size dispatches, and the lane instructions per weight."""
+    import csv
+    from paper_2608_23048_amd import workloads as wl
+    numel = wl.WORKLOADS[workload].numel
+    kernels = {}
+    rows = list(csv.DictReader(open(insts_csv)))
+    for key in ("fwd_lane_kernel", "bwd_lane_kernel", "fwd_wide_kernel", "bwd_wide_kernel"):
+        per = {}  # counter -> dispatch -> value
+        for r in rows:
+            if key in r["Kernel_Name"]:
+                d = per.setdefault(r["Counter_Name"], {})
+                d[r["Dispatch_Id"]] = d.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+        insts = per.get("SQ_INSTS_VALU")
+        if not insts:
+            continue
+        big = [d for d, v in insts.items() if v >= 0.5 * max(insts.values())]
+
+        def mean(counter):
+            vals = [per.get(counter, {}).get(d) for d in big]
+            vals = [v for v in vals if v is not None]
+            return sum(vals) / len(vals) if vals else None
+
+        valu, trans, waves = mean("SQ_INSTS_VALU"), mean("SQ_INSTS_VALU_TRANS_F32"), mean("SQ_WAVES")
+        kernels[key] = {
+            "dispatches": len(big), "valu_insts": valu, "trans_insts": trans, "waves": waves,
+            "valu_insts_per_wave": valu / waves if waves else None,
+            "valu_lane_insts_per_weight": valu * 64 / numel,
+            "trans_lane_insts_per_weight": trans * 64 / numel if trans is not None else None,
+        }
+    rec = json.load(open(VALU_FILE)) if os.path.exists(VALU_FILE) else {}
+    h = kernel_source_hash(ALL_KERNEL_SOURCES)
+    if rec.get("kernel_source_hash") != h:
+        rec = {"kernel_source_hash": h, "workloads": {}}
+    rec["workloads"][workload] = kernels
+    json.dump(rec, open(VALU_FILE, "w"), indent=1, sort_keys=True)
+    print(json.dumps({workload: kernels}), flush=True)
+    return 0
 
 
 def cpu_baseline(W, L, G, work, n, m, tau):
@@ -465,12 +584,17 @@ def main() -> int:
                          "sampler")
     ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
                     help="only run a plain device copy of BYTES (PMC calibration)")
+    ap.add_argument("--valu-summary", metavar="INSTS_CSV",
+                    help="add the workload's VALU counters (rocprofv3 --pmc SQ_INSTS_VALU "
+                         "SQ_INSTS_VALU_TRANS_F32 SQ_WAVES) to the committed record")
     ap.add_argument("--pmc-summary", nargs=5,
                     metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE", "COPY_BYTES"),
                     help="write the traffic record from rocprofv3 --pmc counter CSVs")
     args = ap.parse_args()
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
+    if args.valu_summary:
+        return valu_summary(args.valu_summary, args.workload)
     if args.pmc_summary:
         from paper_2608_23048_amd import workloads as wl
         work = wl.WORKLOADS[args.workload]
@@ -542,13 +666,13 @@ def main() -> int:
     bf, bb = algorithmic_bytes(n, m)
     fwd_gbps = bf * numel / (fwd_avg * 1e-3) / 1e9
     bwd_gbps = bb * numel / (bwd_avg * 1e-3) / 1e9
-    dominant = ("roi_mask_bwd", bwd_gbps, bb) if bwd_avg >= fwd_avg else ("roi_mask_fwd", fwd_gbps, bf)
     traffic = None
     rec = measured_traffic() if work.name == "qwen2.5-7b-stack-2:4" else None
     if rec is not None:
-        key = "bwd_lane_kernel" if dominant[0] == "roi_mask_bwd" else "fwd_lane_kernel"
+        key = "bwd_lane_kernel" if bwd_avg >= fwd_avg else "fwd_lane_kernel"
         if key in rec["kernels"]:
             traffic = rec["kernels"][key]["traffic_bytes"]
+    rooflines = step_rooflines(work.name, n, m, numel, fwd_avg, bwd_avg, traffic)
     value = numel * args.steps / elapsed
     ms_per_step = elapsed * 1e3 / args.steps
     print(f"# timed {args.steps} steps: {ms_per_step:.3f} ms/step, fwd {fwd_avg:.3f} ms "
@@ -622,15 +746,7 @@ def main() -> int:
             "roi_mask_bwd": {"avg_ms": bwd_avg, "algorithmic_bytes_per_weight": bb,
                              "GBps": bwd_gbps},
         },
-        "roofline": {
-            "kernel": dominant[0],
-            "bound": "hbm",
-            "achieved": dominant[1],
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": dominant[1] / HBM_PEAK_GBPS,
-            "traffic": traffic,
-        },
+        **rooflines,
         "cpu_baseline": cpu,
         "grouped_calls": grouped,
     }

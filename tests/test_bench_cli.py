@@ -74,3 +74,34 @@ def test_pmc_summary_keeps_full_size_dispatches(tmp_path, monkeypatch):
     rec = json.load(open(out))
     assert rec["fetch_scale"] == pytest.approx(2.0) and rec["write_scale"] == pytest.approx(1.0)
     assert rec["kernels"]["fwd_lane_kernel"]["traffic_over_algorithmic"] == pytest.approx(1.0)
+
+
+def test_backward_flops_tally():
+    """19 flops per entry and step plus 3 per weight (keys 6, upstream 1,
+    output 1, less the 5 of the steps that have no successor)."""
+    assert bench.backward_flops(1) == 22
+    for n in range(1, 33):
+        assert bench.backward_flops(n) == 19 * n + 3
+
+
+def test_roofline_bound_follows_the_pattern():
+    """m = 4 and 8 report the HBM roofline first, m = 16 and 32 the ALU one;
+    each line carries both, and the ALU figure is the backward's flops over
+    its event time against the fp32 vector peak."""
+    numel = 1 << 30
+    r = bench.step_rooflines("none", 2, 4, numel, 8.0, 12.0, None)
+    assert r["roofline"]["bound"] == "hbm" and r["alu_roofline"]["bound"] == "alu"
+    assert r["roofline"]["achieved"] == pytest.approx(12 * numel / 12e-3 / 1e9)
+    r = bench.step_rooflines("none", 16, 32, numel, 3.0, 10.0, None)
+    assert r["roofline"]["bound"] == "alu" and r["hbm_roofline"]["bound"] == "hbm"
+    alu = r["roofline"]
+    assert alu["achieved"] == pytest.approx(307 * numel / 10e-3 / 1e12)
+    assert alu["frac"] == pytest.approx(alu["achieved"] / 157.3)
+    assert alu["valu"] is None  # no counter record for an unknown workload
+
+
+def test_valu_record_matches_the_kernel_sources():
+    rec = json.load(open(bench.VALU_FILE))
+    assert rec["kernel_source_hash"] == bench.kernel_source_hash(bench.ALL_KERNEL_SOURCES)
+    wide = rec["workloads"]["qwen2.5-1.5b-stack-16:32"]["bwd_wide_kernel"]
+    assert wide["valu_lane_insts_per_weight"] > bench.backward_flops(16) / 2
