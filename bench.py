@@ -209,7 +209,7 @@ def step_rooflines(workload: str, n: int, m: int, numel: int, fwd_ms: float, bwd
            "frac": tflops / FP32_VECTOR_PEAK_TFLOPS, "traffic": None,
            "flops_per_weight": flops, "valu": None}
     rec = measured_valu(workload)
-    key = "bwd_wide_kernel" if m >= 16 else "bwd_lane_kernel"
+    key = "bwd_wide_kernel" if m >= 8 else "bwd_lane_kernel"
     if rec and key in rec:
         per_w = rec[key]["valu_lane_insts_per_weight"]
         rate = per_w * numel / (bwd_ms * 1e-3) / 1e12

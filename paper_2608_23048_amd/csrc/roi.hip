@@ -127,19 +127,15 @@ namespace {
 #ifndef ROI_UNROLL_FWD_M8
 #define ROI_UNROLL_FWD_M8 1
 #endif
-#ifndef ROI_UNROLL_BWD_M4
-#define ROI_UNROLL_BWD_M4 1
-#endif
-#ifndef ROI_UNROLL_BWD_M8
-#define ROI_UNROLL_BWD_M8 1
+#ifndef ROI_UNROLL_BWD
+#define ROI_UNROLL_BWD 1
 #endif
 #ifndef ROI_LANE_BLOCK
 #define ROI_LANE_BLOCK 256
 #endif
 template <int M>
 constexpr int kUnrollFwd = M == 4 ? ROI_UNROLL_FWD_M4 : ROI_UNROLL_FWD_M8;
-template <int M>
-constexpr int kUnrollBwd = M == 4 ? ROI_UNROLL_BWD_M4 : ROI_UNROLL_BWD_M8;
+constexpr int kUnrollBwd = ROI_UNROLL_BWD; // groups per lane in the m = 4 backward
 constexpr int kLaneBlock = ROI_LANE_BLOCK;
 static_assert(kLaneBlock >= kLogCells + 64 && kLaneBlock % 64 == 0, "lane block size");
 
@@ -386,21 +382,20 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
     }
 }
 
-// Backward; with kAdam the AdamW step on the logits is fused in: the moments
-// are read with the group's other inputs, and the updated logits and moments
-// are written instead of (or besides, when pc.dphi is set) the gradient.
-// kQ as in fwd_lane_kernel.  At m = 8 and n <= 4 the plain backward is held
-// to 128 VGPRs, so that four waves share a SIMD (at larger n the records, and
-// with the optimizer step the moments, need more).
+// Backward for m = 4 (m = 8 and wider take the kernels of wide_bwd.hip);
+// with kAdam the AdamW step on the logits is fused in: the moments are read
+// with the group's other inputs, and the updated logits and moments are
+// written instead of (or besides, when pc.dphi is set) the gradient.  kQ as
+// in fwd_lane_kernel.
 template <int M, int N, bool kLambdaOne, bool kAdam, int kQ>
-__global__ __launch_bounds__(kLaneBlock)
-__attribute__((amdgpu_waves_per_eu(M == 8 && N <= 4 && !kAdam ? 4 : 1))) void bwd_lane_kernel(BwdBatch a)
+__global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
 {
+    static_assert(M == 4, "the lane backward serves m = 4");
     const BwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
     const int64_t ng = pc.ngroups;
-    constexpr int U = kUnrollBwd<M>;
+    constexpr int U = kUnrollBwd;
     const int64_t chunk = (int64_t)kLaneBlock * U;
     for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * chunk; base < ng;
          base += (int64_t)pc.nblocks * chunk) {
@@ -649,7 +644,6 @@ BwdFn select_bwd(int m, int n, bool l, bool adam, float tau)
 {
     const int q = tau_mode(tau);
     if (m == 4) return bwd_for_n<4>(n, l, adam, q, std::make_integer_sequence<int, 4>{});
-    if (m == 8) return bwd_for_n<8>(n, l, adam, q, std::make_integer_sequence<int, 8>{});
     return select_wide_bwd(m, n, adam, q);
 }
 
@@ -664,9 +658,8 @@ namespace {
 // Blocks one piece of `ngroups` groups needs in a launch.
 int64_t blocks_for(int64_t ngroups, int m, bool fwd)
 {
-    if (m > 8) return ceil_div(ngroups * (m / 4), kBlock);
-    const int u = fwd ? (m == 4 ? kUnrollFwd<4> : kUnrollFwd<8>)
-                      : (m == 4 ? kUnrollBwd<4> : kUnrollBwd<8>);
+    if (m > 8 || (m == 8 && !fwd)) return ceil_div(ngroups * (m / 4), kBlock); // wide kernels
+    const int u = fwd ? (m == 4 ? kUnrollFwd<4> : kUnrollFwd<8>) : kUnrollBwd;
     return ceil_div(ngroups, (int64_t)u * kLaneBlock);
 }
 
@@ -885,7 +878,7 @@ int mask_bwd_core(const char* what, const BwdDesc* t, int count, int n, int m, f
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     Launcher<BwdBatch, BwdPiece, BwdFn> L{};
     L.fn = fn;
-    L.block = m > 8 ? kBlock : kLaneBlock;
+    L.block = m >= 8 ? kBlock : kLaneBlock;
     L.m = m;
     L.fwd = false;
     L.stream = stream;

@@ -1,14 +1,14 @@
 // wide.hpp -- device helpers of the gfx950 kernels for groups of m = 16 and 32
-// weights (wide_fwd.hip, wide_bwd.hip).
+// weights (wide_fwd.hip, wide_bwd.hip), and of the backward for m = 8.
 //
 // Four consecutive elements per lane (one Philox call, one 16-byte logits load
 // and one 8-byte bf16 load per lane), a group spread over L = m / 4 adjacent
 // lanes of one wave.  Group-wide maxima and "sum over the other lanes" use
 // cross-lane butterflies: DPP quad permutations for lane distances 1..3 and
-// the DPP half-row mirror for distances 4..7.  Every group is whole inside a wave and either
-// all its lanes are active or none is, so the butterflies never read a lane
-// outside the group.  Same arithmetic as the per-lane kernels for m = 4 and 8:
-// the noise of noise.hpp, ranks with ties to the lower index, and the
+// the DPP half-row mirror for distances 4..7.  Every group is whole inside a
+// wave and either all its lanes are active or none is, so the butterflies
+// never read a lane outside the group.  Same arithmetic as the per-lane
+// kernels: the noise of noise.hpp, ranks with ties to the lower index, and the
 // relaxation of relax.hpp in its "all entries but j" form.
 #pragma once
 

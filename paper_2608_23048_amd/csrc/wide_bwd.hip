@@ -1,5 +1,7 @@
 // wide_bwd.hip -- the backward kernel (optionally with the fused AdamW step)
-// for groups of m = 16 and 32 weights (helpers and layout in wide.hpp).
+// for groups of m = 8, 16 and 32 weights (helpers and layout in wide.hpp).
+// At m = 8 a group spans two lanes: half the relaxation records per lane of
+// the one-group-per-lane layout, so twice the waves per SIMD.
 #include <hip/hip_runtime.h>
 
 #include <utility>
@@ -105,6 +107,7 @@ BwdFn wide_bwd_for_n(int n, bool adam, int q, std::integer_sequence<int, Ns...>)
 
 BwdFn select_wide_bwd(int m, int n, bool adam, int q)
 {
+    if (m == 8) return wide_bwd_for_n<8>(n, adam, q, std::make_integer_sequence<int, 8>{});
     if (m == 16) return wide_bwd_for_n<16>(n, adam, q, std::make_integer_sequence<int, 16>{});
     if (m == 32) return wide_bwd_for_n<32>(n, adam, q, std::make_integer_sequence<int, 32>{});
     return nullptr;
