@@ -299,6 +299,86 @@ def cpu_baseline(W, L, G, work, n, m, tau):
             "sample": f"layer 0 {names} ({end} weights), one mask fwd+bwd, {dt:.1f} s on 1 thread"}
 
 
+def forward_soft_flops(n: int) -> int:
+    """Floating-point operations per weight of the pure soft forward, counted
+    from the algorithm as in backward_flops: keys 6; each of the n steps of the
+    recursion 8, plus 1 for accumulating S; before the last step 3 (floor, log,
+    add); the product W S 1.  Total 12 n + 4."""
+    return 6 + 9 * n + 3 * (n - 1) + 1
+
+
+def run_soft(args) -> int:
+    """--mode soft: the step of the paper's default setting, without the
+    straight-through estimator: the pure soft forward W_soft = bf16(W (.) S)
+    (roi_mask_fwd_soft; no indices, S not stored) and the same backward."""
+    import torch
+
+    import paper_2608_23048_amd as roi
+    from paper_2608_23048_amd import workloads as wl
+
+    roi.lib()
+    work = wl.WORKLOADS[args.workload]
+    n, m = work.n, work.m
+    dev = torch.device("cuda:0")
+    numel = work.numel
+    print(f"# soft mode, workload {work.name}: {numel} weights, {n}:{m}", file=sys.stderr,
+          flush=True)
+    W, L, G = wl.fill_slab(work, dev, step=0)
+    Ws = torch.empty_like(W)
+    dphi = torch.empty_like(L)
+    sched = work.tau_schedule or (work.tau, work.tau, 1)
+
+    def step(t, ev=None):
+        tau = roi.anneal(sched[0], sched[1], t, sched[2])
+        if ev is not None:
+            ev[0].record()
+        roi.mask_fwd(W, L, n, m, tau, 1.0, 0, t, 0, want_soft=False, want_idx=False,
+                     out={"W_masked": Ws}, soft_forward=True)
+        if ev is not None:
+            ev[1].record()
+        roi.mask_bwd(G, W, L, n, m, tau, 1.0, 0, t, 0, out=dphi)
+        if ev is not None:
+            ev[2].record()
+
+    for i in range(args.warmup):
+        step(1000 + i)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.steps):
+        step(t, evs[t])
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    f_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    b_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    bf = 2 + 4 + 2  # W and logits read, W_soft written
+    _, bb = algorithmic_bytes(n, m)
+    ff = forward_soft_flops(n)
+    f_gbps = bf * numel / (f_ms * 1e-3) / 1e9
+    f_tflops = ff * numel / (f_ms * 1e-3) / 1e12
+    print(f"# soft step: {el * 1e3 / args.steps:.3f} ms/step, soft fwd {f_ms:.3f} ms "
+          f"({f_gbps:.0f} GB/s, {f_tflops:.1f} TFLOP/s), bwd {b_ms:.3f} ms", file=sys.stderr,
+          flush=True)
+    rooflines = step_rooflines(work.name, n, m, numel, f_ms, b_ms, None)
+    out = {"metric": "masked weights/sec (pure soft forward + backward)",
+           "value": numel * args.steps / el, "unit": "masked weights/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": el * 1e3 / args.steps,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic (as the default mode)",
+           "config": {"workload": work.name, "masked_weights": numel, "pattern": f"{n}:{m}",
+                      "forward": "pure soft, W_soft = bf16(W * S)"},
+           "kernels": {
+               "roi_mask_fwd_soft": {
+                   "avg_ms": f_ms, "algorithmic_bytes_per_weight": bf, "GBps": f_gbps,
+                   "hbm_frac": f_gbps / HBM_PEAK_GBPS, "flops_per_weight": ff,
+                   "TFLOPs": f_tflops, "alu_frac": f_tflops / FP32_VECTOR_PEAK_TFLOPS},
+               "roi_mask_bwd": {"avg_ms": b_ms, "algorithmic_bytes_per_weight": bb,
+                                "GBps": bb * numel / (b_ms * 1e-3) / 1e9}},
+           **rooflines}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def run_adamw(args) -> int:
     """--mode adamw: the training step with the optimizer, as the appendix
     trains the logits: forward (masked weights + indices) and the backward with
@@ -577,8 +657,9 @@ def main() -> int:
     ap.add_argument("--no-grouped", action="store_true",
                     help="skip the secondary timing through the grouped calls")
     ap.add_argument("--pattern", default=None, help="n:m for --mode cat (default: the workload's)")
-    ap.add_argument("--mode", choices=("st", "adamw", "export", "cat"), default="st",
-                    help="st: forward + backward (the headline); adamw: forward + backward "
+    ap.add_argument("--mode", choices=("st", "soft", "adamw", "export", "cat"), default="st",
+                    help="st: forward + backward (the headline); soft: the pure soft forward "
+                         "(no straight-through) + backward; adamw: forward + backward "
                          "with the AdamW step on the logits fused in; export: the final-mask "
                          "export after training; cat: the categorical sampler against the item "
                          "sampler")
@@ -604,6 +685,8 @@ def main() -> int:
               "runs and reports a single MI355X (pass --gpus 1).", file=sys.stderr)
         return 2
 
+    if args.mode == "soft":
+        return run_soft(args)
     if args.mode == "adamw":
         return run_adamw(args)
     if args.mode == "export":

@@ -212,6 +212,7 @@ ExportFn select_export(int m, int n);
 // Kernels for m = 16 and 32 (wide_fwd.hip, wide_bwd.hip): four consecutive elements per lane,
 // a group spread over m / 4 adjacent lanes.
 FwdFn select_wide_fwd(int m, int n, bool relax, int q); // q: tau_mode (roi.hip)
+FwdFn select_wide_soft_only(int m, int n, int q);
 BwdFn select_wide_bwd(int m, int n, bool adam, int q);
 
 } // namespace roi

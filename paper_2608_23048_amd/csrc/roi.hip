@@ -382,6 +382,56 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
     }
 }
 
+// Pure soft forward whose only output is W_soft = bf16(W (.) S) (neither S
+// nor the indices requested).  The relaxation runs on the hardware-log keys,
+// as in the backward: they are within the noise bound of noise.hpp of the
+// exact keys, which moves S by far less than the bf16 rounding of the
+// output.  No selection, no log cells.
+template <int M, int N, int kQ>
+__global__ __launch_bounds__(kLaneBlock) void fwd_soft_lane_kernel(FwdBatch a)
+{
+    const FwdPiece& pc = a.p[find_piece(a)];
+    NoiseKey key = a.key_base;
+    key.block_hi = pc.block_hi;
+    const int64_t ng = pc.ngroups;
+    constexpr int U = kUnrollFwd<M>;
+    const int64_t chunk = (int64_t)kLaneBlock * U;
+    for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * chunk; base < ng;
+         base += (int64_t)pc.nblocks * chunk) {
+        float phi[U][M];
+        uint32_t w[U][M];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t q = base + u * kLaneBlock + threadIdx.x;
+            if (q < ng) {
+                load_logits<M>(pc.phi + q * M, phi[u]);
+                load_bf16<M>(pc.W + q * M, w[u]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t q = base + u * kLaneBlock + threadIdx.x;
+            if (q >= ng) continue;
+            uint32_t x[M];
+            group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
+            float kappa[M]; // log2 units
+            fast_keys<M>(phi[u], x, a.key_c, kappa);
+            float S[M], b[M], bmax;
+            StepRec<M> unused[N]; // not written when records are not kept
+            const float span = scaled_keys<M>(kappa, a.inv_tau, b, bmax);
+            if (span <= a.exp_span)
+                relax_forward_exp<M, N, true, false, kQ>(b, bmax, a.inv_tau, S, unused);
+            else
+                relax_forward<M, N, true, false>(b, bmax, a.inv_tau, S, unused);
+            uint32_t ws[M];
+#pragma unroll
+            for (int j = 0; j < M; ++j)
+                ws[j] = float_to_bf16_rne(bf16_bits_to_float(w[u][j]) * S[j]);
+            store_pairs<M>(pc.Wm + q * M, ws);
+        }
+    }
+}
+
 // Backward for m = 4 (m = 8 and wider take the kernels of wide_bwd.hip);
 // with kAdam the AdamW step on the logits is fused in: the moments are read
 // with the group's other inputs, and the updated logits and moments are
@@ -632,6 +682,30 @@ BwdFn bwd_for_n(int n, bool l, bool adam, int q, std::integer_sequence<int, Ns..
     return f;
 }
 
+template <int M, int N>
+FwdFn pick_soft(int q)
+{
+    return q == 1 ? fwd_soft_lane_kernel<M, N, 1>
+                  : (q == 2 ? fwd_soft_lane_kernel<M, N, 2> : fwd_soft_lane_kernel<M, N, 0>);
+}
+
+template <int M, int... Ns>
+FwdFn soft_for_n(int n, int q, std::integer_sequence<int, Ns...>)
+{
+    FwdFn f = nullptr;
+    ((n == Ns + 1 ? (f = pick_soft<M, Ns + 1>(q), 0) : 0), ...);
+    return f;
+}
+
+// The soft forward with no output but W_soft (hardware-log keys).
+FwdFn select_soft_only(int m, int n, float tau)
+{
+    const int q = tau_mode(tau);
+    if (m == 4) return soft_for_n<4>(n, q, std::make_integer_sequence<int, 4>{});
+    if (m == 8) return soft_for_n<8>(n, q, std::make_integer_sequence<int, 8>{});
+    return select_wide_soft_only(m, n, q);
+}
+
 FwdFn select_fwd(int m, int n, bool s, bool i, bool l, float tau)
 {
     const int q = tau_mode(tau);
@@ -760,7 +834,9 @@ int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count
     }
     if (with_s < 0) return ok(); // nothing to do
     if (int st = check_overlaps(ranges)) return st;
-    FwdFn fn = select_fwd(m, n, soft || with_s == 1, with_idx == 1, lambda == 1.0f, tau);
+    FwdFn fn = soft && with_s == 0 && with_idx == 0
+                   ? select_soft_only(m, n, tau)
+                   : select_fwd(m, n, soft || with_s == 1, with_idx == 1, lambda == 1.0f, tau);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     Launcher<FwdBatch, FwdPiece, FwdFn> L{};
     L.fn = fn;

@@ -99,6 +99,52 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
     }
 }
 
+// Pure soft forward whose only output is bf16(W (.) S): the relaxation on the
+// hardware-log keys (as fwd_soft_lane_kernel in roi.hip), no selection.
+template <int M, int N, int kQ>
+__global__ __launch_bounds__(kBlock) void fwd_soft_wide_kernel(FwdBatch a)
+{
+    constexpr int L = M / 4;
+    const FwdPiece& pc = a.p[find_piece(a)];
+    NoiseKey key = a.key_base;
+    key.block_hi = pc.block_hi;
+    const int64_t nslots = pc.ngroups * L;
+    const int64_t stride = (int64_t)pc.nblocks * kBlock;
+    for (int64_t slot = (int64_t)(blockIdx.x - pc.first_block) * kBlock + threadIdx.x;
+         slot < nslots; slot += stride) {
+        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
+        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
+        const uint4 x = philox_block(pc.block0 + (uint32_t)slot, key);
+        const float kappa[4] = {fast_key_log2(pv.x, a.key_c, x.x), fast_key_log2(pv.y, a.key_c, x.y),
+                                fast_key_log2(pv.z, a.key_c, x.z), fast_key_log2(pv.w, a.key_c, x.w)};
+        float S[4];
+        StepRec<4> unused[N]; // not written when records are not kept
+        wide_relax_forward<L, N, false, kQ>(kappa, a.inv_tau, a.inv_tau, a.exp_span, true, S,
+                                            unused);
+        const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
+        const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
+        const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
+        const uint32_t h3 = float_to_bf16_rne(bf16_bits_to_float(wv.y >> 16) * S[3]);
+        const u32x2 out = {h0 | (h1 << 16), h2 | (h3 << 16)};
+        stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
+    }
+}
+
+template <int M, int N>
+FwdFn wide_soft_q(int q)
+{
+    return q == 1 ? fwd_soft_wide_kernel<M, N, 1>
+                  : (q == 2 ? fwd_soft_wide_kernel<M, N, 2> : fwd_soft_wide_kernel<M, N, 0>);
+}
+
+template <int M, int... Ns>
+FwdFn wide_soft_for_n(int n, int q, std::integer_sequence<int, Ns...>)
+{
+    FwdFn f = nullptr;
+    ((n == Ns + 1 ? (f = wide_soft_q<M, Ns + 1>(q), 0) : 0), ...);
+    return f;
+}
+
 template <int M, int N>
 FwdFn wide_fwd_q(bool relax, int q)
 {
@@ -116,6 +162,13 @@ FwdFn wide_fwd_for_n(int n, bool relax, int q, std::integer_sequence<int, Ns...>
 }
 
 } // namespace
+
+FwdFn select_wide_soft_only(int m, int n, int q)
+{
+    if (m == 16) return wide_soft_for_n<16>(n, q, std::make_integer_sequence<int, 16>{});
+    if (m == 32) return wide_soft_for_n<32>(n, q, std::make_integer_sequence<int, 32>{});
+    return nullptr;
+}
 
 FwdFn select_wide_fwd(int m, int n, bool relax, int q)
 {

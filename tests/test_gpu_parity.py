@@ -126,6 +126,7 @@ SMALL = [
     (61, 88, 7, 8, 1.0, 1.0, 8, 5, 8),
     (61, 88, 8, 8, 0.9, 1.0, 9, 6, 0),
     (17, 8, 6, 8, 0.25, 0.5, 4, 2**33, 2**36),
+    (23, 56, 5, 8, 2.0, 0.8, 3, 7, 0),           # tau > 1: the exp-domain power by exp2/log2
     # the Philox block index crosses a multiple of 2^32 inside the call
     (40, 64, 2, 4, 1.0, 1.0, 6, 3, 2**34 - 4 * 256),
     (25, 64, 4, 8, 0.5, 1.0, 6, 3, 2**35 - 8 * 100),
@@ -415,7 +416,8 @@ def test_grouped_against_oracle(dev):
 # --------------------------------------------------------------------------- fused AdamW
 ADAMW = [(37, 36, 2, 4, 1.0, 1.0, 1, 1e-3), (64, 96, 2, 4, 0.1, 1.0, 7, 4e-4),
          (33, 64, 3, 4, 0.7, 0.6, 3, 1e-3), (61, 88, 4, 8, 0.5, 1.0, 2, 1e-3),
-         (37, 48, 8, 16, 1.0, 1.0, 1, 1e-3), (13, 64, 5, 32, 0.3, 0.8, 12, 2e-4)]
+         (37, 48, 8, 16, 1.0, 1.0, 1, 1e-3), (13, 64, 5, 32, 0.3, 0.8, 12, 2e-4),
+         (29, 40, 7, 8, 0.4, 1.7, 5, 1e-3)]
 
 
 def adamw_state(rows, cols, seed):
@@ -930,3 +932,39 @@ def test_soft_forward(dev, case):
     got = (bf16_bits(Ws).astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1)
     ulp = np.where(ref != 0, 2.0 ** (np.floor(np.log2(np.abs(ref) + 1e-300)) - 7), 0.0)
     assert_close(got, ref, "W (.) S", floor=ulp)
+
+
+SOFT_ONLY = SOFT + [(61, 88, 6, 8, 0.1, 1.0, 3, 2, 0), (21, 80, 12, 16, 0.1, 0.7, 9, 1, 32),
+                    (13, 64, 24, 32, 0.15, 1.0, 2, 5, 0)]
+
+
+@pytest.mark.parametrize("case", SOFT_ONLY, ids=lambda c: "x".join(map(str, c[:5])))
+def test_soft_forward_alone(dev, case):
+    """The pure soft forward with W_soft as its only output (no S, no indices)
+    runs the relaxation on the hardware-log keys.  Against W (.) S from the
+    oracle's fp64 S it stays within one bf16 rounding step plus the float
+    tolerance, as the exact-key soft forward does, and it differs from that one
+    by at most one bf16 step per element."""
+    import torch
+    rows, cols, n, m, tau, lam, seed, step, off = case
+    say(f"soft forward alone rows={rows} cols={cols} {n}:{m} tau={tau} lam={lam}")
+    W, L, _ = wl.small_case(rows, cols, rows * 7 + cols, device=dev, w_std=1.0)
+    Ws, S, idx = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=False,
+                              want_idx=False, soft_forward=True)
+    assert S is None and idx is None
+    We, _, _ = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True,
+                            soft_forward=True)
+    torch.cuda.synchronize()
+    tau32, lam32 = float(np.float32(tau)), float(np.float32(lam))
+    _, S_o, _ = oracle.mask_fwd(bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
+    wf = (bf16_bits(W).astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1)
+    ref = wf * S_o.reshape(-1)
+    to_f = lambda t: (bf16_bits(t).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    got = to_f(Ws).reshape(-1)
+    ulp = np.where(ref != 0, 2.0 ** (np.floor(np.log2(np.abs(ref) + 1e-300)) - 7), 0.0)
+    assert_close(got, ref, "W (.) S from the hardware-log keys", floor=ulp)
+    # bf16 bit patterns of one sign are ordered like their values
+    a = bf16_bits(Ws).astype(np.int64).reshape(-1)
+    b = bf16_bits(We).astype(np.int64).reshape(-1)
+    assert np.abs(a - b).max() <= 1, "more than one bf16 step from the exact-key soft forward"
+    say(f"  {int((a != b).sum())} of {a.size} outputs one bf16 step from the exact-key ones")
