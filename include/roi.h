@@ -103,6 +103,12 @@ int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows, int64_t c
  * and soft_mask / sel_idx, when not NULL, receive S and the hard top-n indices
  * of the same keys.  The backward is roi_mask_bwd (the relaxation is the
  * differentiated path in both settings).
+ * Precision: when soft_mask or sel_idx is given, S comes from the exact keys,
+ * as in roi_mask_fwd, and W_soft is the bf16 rounding of W (.) S.  With both
+ * NULL, S is evaluated at keys from the hardware logarithm (within a proven
+ * bound of the exact keys, as in roi_mask_bwd).  W_soft is then within one
+ * bf16 rounding step of W (.) S at the exact keys: each element equals the
+ * exact-key output or its bf16 neighbour.
  */
 int roi_mask_fwd_soft(const uint16_t* W, const float* logits, int64_t rows, int64_t cols, int n,
                       int m, float tau, float lambda, uint64_t seed, uint64_t step,
