@@ -277,6 +277,32 @@ def valu_summary(insts_csv, workload: str) -> int:
     return 0
 
 
+def copy_reference(nbytes: int = 1 << 32, reps: int = 3) -> dict:
+    """The same GPU's streaming bandwidth for the sampler's access pattern:
+    roi_stream_copy of nbytes (nbytes read + nbytes written; 16 bytes per lane,
+    non-temporal, one-shot grid), timed with HIP events, best of reps."""
+    import torch
+
+    import paper_2608_23048_amd as roi
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    best = None
+    for _ in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        roi.stream_copy(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    ok = bool(torch.equal(a[:: 1 << 20], b[:: 1 << 20]))
+    del a, b
+    torch.cuda.empty_cache()
+    return {"kernel": "roi_stream_copy", "bytes_moved": 2 * nbytes, "ms": best,
+            "GBps": 2 * nbytes / (best * 1e-3) / 1e9, "checked": ok}
+
+
 def cpu_baseline(W, L, G, work, n, m, tau):
     """The CPU oracle, as it is, on a bounded sample of the same workload: the
     q, k, v, o and gate projections of layer 0 (about 10 s of one core), one
@@ -792,6 +818,12 @@ def main() -> int:
     grouped = None
     if not args.no_grouped:
         grouped = grouped_timing(grouped_step, args.steps, work)
+
+    copy = copy_reference()
+    rooflines["roofline"]["copy_reference"] = copy
+    if rooflines["roofline"]["bound"] == "hbm":
+        rooflines["roofline"]["frac_of_copy"] = rooflines["roofline"]["achieved"] / copy["GBps"]
+    print(f"# device copy: {copy['GBps']:.0f} GB/s", file=sys.stderr, flush=True)
 
     cpu = None
     if not args.no_cpu_baseline:

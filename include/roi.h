@@ -316,6 +316,16 @@ int roi_fast_noise_from_words(const uint32_t* words, int64_t count, float* out, 
  */
 float roi_anneal(float v_init, float v_end, int64_t t, int64_t t_anneal);
 
+/*
+ * roi_stream_copy -- not part of the method: a plain copy of nbytes from src
+ * to dst (device pointers, 16-byte aligned, not overlapping; nbytes a
+ * multiple of 16), with the sampler kernels' access pattern: 16 bytes per
+ * lane, non-temporal loads and stores, one pass of a one-shot grid.  The
+ * benchmark times it as the same GPU's achievable streaming bandwidth.
+ * Asynchronous on stream; ROI_E_INVAL for bad arguments before any launch.
+ */
+int roi_stream_copy(const void* src, void* dst, int64_t nbytes, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* roi_status_string(int status);
 /* Thread-local detail of the last failed call on this thread ("" if none). */

@@ -108,6 +108,8 @@ def lib() -> ctypes.CDLL:
         L.roi_gumbel_from_words.restype = _int
         L.roi_fast_noise_from_words.argtypes = [_vp, _i64, _vp, _vp]
         L.roi_fast_noise_from_words.restype = _int
+        L.roi_stream_copy.argtypes = [_vp, _vp, _i64, _vp]
+        L.roi_stream_copy.restype = _int
         L.roi_anneal.argtypes = [_f32, _f32, _i64, _i64]
         L.roi_anneal.restype = _f32
         L.roi_status_string.argtypes = [_int]
@@ -421,6 +423,16 @@ def gumbel_from_words(words):
     g = torch.empty(words.shape, dtype=torch.float32, device=words.device)
     _raise_on(lib().roi_gumbel_from_words(_ptr(words), words.numel(), _ptr(g), _stream(words)))
     return g
+
+
+def stream_copy(src, dst):
+    """Plain streaming copy of src into dst (device tensors of the same byte
+    size, a multiple of 16): the benchmark's data-movement reference."""
+    if src.numel() * src.element_size() != dst.numel() * dst.element_size():
+        raise ValueError("src and dst differ in size")
+    _raise_on(lib().roi_stream_copy(_ptr(src), _ptr(dst), src.numel() * src.element_size(),
+                                    _stream(src)))
+    return dst
 
 
 def fast_noise_from_words(words):

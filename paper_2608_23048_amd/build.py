@@ -21,7 +21,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libroi.so")
 SOURCES = [os.path.join(CSRC, "roi.hip"), os.path.join(CSRC, "wide_fwd.hip"),
            os.path.join(CSRC, "wide_bwd.hip"),
-           os.path.join(CSRC, "export.hip"), os.path.join(CSRC, "cat.hip")]
+           os.path.join(CSRC, "export.hip"), os.path.join(CSRC, "cat.hip"),
+           os.path.join(CSRC, "stream_copy.hip")]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -968,3 +968,21 @@ def test_soft_forward_alone(dev, case):
     b = bf16_bits(We).astype(np.int64).reshape(-1)
     assert np.abs(a - b).max() <= 1, "more than one bf16 step from the exact-key soft forward"
     say(f"  {int((a != b).sum())} of {a.size} outputs one bf16 step from the exact-key ones")
+
+
+def test_stream_copy(dev):
+    """The benchmark's data-movement reference copies every byte, including a
+    ragged tail of the last block, and rejects bad arguments before launching."""
+    import torch
+    n = 16 * (256 * 37 + 5)
+    src = torch.randint(0, 256, (n,), dtype=torch.uint8, device=dev)
+    dst = torch.zeros_like(src)
+    roi.stream_copy(src, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst)
+    L = roi.lib()
+    p = src.data_ptr()
+    assert L.roi_stream_copy(p, dst.data_ptr(), 24, None) == roi.ROI_E_INVAL      # not a multiple of 16
+    assert L.roi_stream_copy(p + 8, dst.data_ptr(), 32, None) == roi.ROI_E_INVAL  # misaligned
+    assert L.roi_stream_copy(p, p + 16, 64, None) == roi.ROI_E_INVAL              # overlap
+    assert L.roi_stream_copy(p, dst.data_ptr(), 0, None) == roi.ROI_OK
