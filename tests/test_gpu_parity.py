@@ -368,13 +368,14 @@ def grouped_inputs(dev, m, count=40, seed=5):
 def test_grouped_equals_single_calls(dev, n, m):
     """The grouped calls over separately allocated tensors give, bit for bit,
     the outputs of one single-tensor call per tensor (forward with and
-    without S and indices, soft forward, backward)."""
+    without S and indices, soft forward with them and alone, backward)."""
     import torch
     say(f"grouped vs single {n}:{m}")
     tensors, offs = grouped_inputs(dev, m)
     args = (n, m, 0.7, 1.0, 13, 4)
     for soft, want_soft, want_idx in ((False, False, True), (False, True, True),
-                                      (False, False, False), (True, True, True)):
+                                      (False, False, False), (True, True, True),
+                                      (True, False, False)):
         outs = roi.mask_fwd_grouped([(W, L) for W, L, _ in tensors], *args, offsets=offs,
                                     want_soft=want_soft, want_idx=want_idx, soft_forward=soft)
         for (W, L, _), off, (Wm, S, idx) in zip(tensors, offs, outs):
