@@ -105,14 +105,13 @@ int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows, int64_t c
  * differentiated path in both settings).
  * Precision: when soft_mask or sel_idx is given, S comes from the exact keys,
  * as in roi_mask_fwd, and W_soft is the bf16 rounding of W (.) S.  With both
- * NULL, S is evaluated at keys from the hardware logarithm, within a proven
- * bound of the exact keys (as in roi_mask_bwd).  For the keys and
- * temperatures of training, the change in S is far below the bf16 rounding
- * of W_soft.  The tests check it against the oracle to one bf16 step, and
- * against the exact-key output to one bf16 step per element, for n / tau up
- * to 160.  The key error's effect on S grows with n / tau and with |kappa|:
- * at extreme settings (|kappa| in the hundreds, tau near 0.05) pass
- * soft_mask to get the exact keys.
+ * NULL and n / (tau min(1, lambda)) <= 160, S is evaluated at keys from the
+ * hardware logarithm, within a proven bound of the exact keys (as in
+ * roi_mask_bwd).  The change in S is then far below the bf16 rounding of
+ * W_soft.  The tests check it against the oracle to one bf16 step, and
+ * against the exact-key output to one bf16 step per element, up to that
+ * limit.  Past the limit (the key error's effect on S grows with n / tau and
+ * with 1 / lambda) the exact keys are used.
  */
 int roi_mask_fwd_soft(const uint16_t* W, const float* logits, int64_t rows, int64_t cols, int n,
                       int m, float tau, float lambda, uint64_t seed, uint64_t step,

@@ -697,7 +697,10 @@ FwdFn soft_for_n(int n, int q, std::integer_sequence<int, Ns...>)
     return f;
 }
 
-// The soft forward with no output but W_soft (hardware-log keys).
+// The soft forward with no output but W_soft (hardware-log keys), and the
+// largest n / (tau min(1, lambda)) it serves.
+constexpr double kSoftFastLimit = 160.0;
+
 FwdFn select_soft_only(int m, int n, float tau)
 {
     const int q = tau_mode(tau);
@@ -834,7 +837,14 @@ int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count
     }
     if (with_s < 0) return ok(); // nothing to do
     if (int st = check_overlaps(ranges)) return st;
-    FwdFn fn = soft && with_s == 0 && with_idx == 0
+    // The soft forward alone runs on the hardware-log keys where the effect of
+    // their error on S stays in the range its parity tests cover: n / tau up
+    // to kSoftFastLimit, with the keys' magnitude growing as 1 / lambda below
+    // lambda = 1.  Elsewhere it takes the exact keys.
+    const bool soft_fast = soft && with_s == 0 && with_idx == 0 &&
+                           (double)n / ((double)tau * std::min(1.0, (double)lambda)) <=
+                               kSoftFastLimit;
+    FwdFn fn = soft_fast
                    ? select_soft_only(m, n, tau)
                    : select_fwd(m, n, soft || with_s == 1, with_idx == 1, lambda == 1.0f, tau);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);

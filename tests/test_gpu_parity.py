@@ -935,8 +935,10 @@ def test_soft_forward(dev, case):
     assert_close(got, ref, "W (.) S", floor=ulp)
 
 
-SOFT_ONLY = SOFT + [(61, 88, 6, 8, 0.1, 1.0, 3, 2, 0), (21, 80, 12, 16, 0.1, 0.7, 9, 1, 32),
-                    (13, 64, 24, 32, 0.15, 1.0, 2, 5, 0)]
+# n / (tau min(1, lambda)) up to 160: the hardware keys; (12:16, tau 0.1,
+# lambda 0.7) is past that limit and takes the exact keys.
+SOFT_ONLY = SOFT + [(61, 88, 6, 8, 0.1, 1.0, 3, 2, 0), (21, 80, 8, 16, 0.1, 0.7, 9, 1, 32),
+                    (21, 80, 12, 16, 0.1, 0.7, 9, 1, 32), (13, 64, 24, 32, 0.15, 1.0, 2, 5, 0)]
 
 
 @pytest.mark.parametrize("case", SOFT_ONLY, ids=lambda c: "x".join(map(str, c[:5])))
@@ -969,6 +971,21 @@ def test_soft_forward_alone(dev, case):
     b = bf16_bits(We).astype(np.int64).reshape(-1)
     assert np.abs(a - b).max() <= 1, "more than one bf16 step from the exact-key soft forward"
     say(f"  {int((a != b).sum())} of {a.size} outputs one bf16 step from the exact-key ones")
+    if n / (tau * min(1.0, lam)) > 160:  # the exact keys: the exact-key output, bit for bit
+        assert np.array_equal(a, b)
+
+
+def test_soft_forward_alone_takes_exact_keys_at_small_lambda(dev):
+    """Past n / (tau min(1, lambda)) = 160 (here lambda = 0.01: keys a hundred
+    times larger) the soft forward alone takes the exact keys, so its output
+    is the exact-key soft forward's, bit for bit."""
+    import torch
+    W, L, _ = wl.small_case(37, 48, 5, device=dev, w_std=1.0)
+    Ws, _, _ = roi.mask_fwd(W, L, 2, 4, 1.0, 0.01, 3, 1, 0, want_soft=False, want_idx=False,
+                            soft_forward=True)
+    We, _, _ = roi.mask_fwd(W, L, 2, 4, 1.0, 0.01, 3, 1, 0, want_soft=True, soft_forward=True)
+    torch.cuda.synchronize()
+    assert torch.equal(Ws.view(torch.int16), We.view(torch.int16))
 
 
 def test_stream_copy(dev):
