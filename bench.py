@@ -189,15 +189,19 @@ def backward_flops(n: int) -> int:
 
 
 def step_rooflines(workload: str, n: int, m: int, numel: int, fwd_ms: float, bwd_ms: float,
-                   traffic) -> dict:
+                   traffic, fwd_bytes: float | None = None) -> dict:
     """The step's two rooflines.  HBM: algorithmic bytes of the slower kernel
     over its event time, against 8 TB/s.  ALU: the backward's algorithmic
     flops (backward_flops) over its event time, against the fp32 vector peak,
     with the measured VALU instruction counts beside it when the committed
     record matches the kernels.  `roofline` is the one that bounds the path:
     HBM for m = 4 and 8, whose relaxation is at most 4 steps per weight; ALU
-    for m = 16 and 32 (8 and 16 steps per weight, 155 and 307 flops)."""
+    for m = 16 and 32 (8 and 16 steps per weight, 155 and 307 flops).  fwd_bytes
+    overrides the straight-through forward's bytes per weight (the soft
+    forward moves 8)."""
     bf, bb = algorithmic_bytes(n, m)
+    if fwd_bytes is not None:
+        bf = fwd_bytes
     slow = ("roi_mask_bwd", bb, bwd_ms) if bwd_ms >= fwd_ms else ("roi_mask_fwd", bf, fwd_ms)
     hbm_gbps = slow[1] * numel / (slow[2] * 1e-3) / 1e9
     hbm = {"kernel": slow[0], "bound": "hbm", "achieved": hbm_gbps, "peak": HBM_PEAK_GBPS,
@@ -385,7 +389,7 @@ def run_soft(args) -> int:
     print(f"# soft step: {el * 1e3 / args.steps:.3f} ms/step, soft fwd {f_ms:.3f} ms "
           f"({f_gbps:.0f} GB/s, {f_tflops:.1f} TFLOP/s), bwd {b_ms:.3f} ms", file=sys.stderr,
           flush=True)
-    rooflines = step_rooflines(work.name, n, m, numel, f_ms, b_ms, None)
+    rooflines = step_rooflines(work.name, n, m, numel, f_ms, b_ms, None, fwd_bytes=bf)
     out = {"metric": "masked weights/sec (pure soft forward + backward)",
            "value": numel * args.steps / el, "unit": "masked weights/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": el * 1e3 / args.steps,
