@@ -192,13 +192,9 @@ __device__ __forceinline__ void store_order(uint8_t* p, uint32_t packed)
 }
 
 // Selected indices in selection order: byte r holds the index of rank r.
-template <int M, int N>
-__device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
+template <int N>
+__device__ __forceinline__ void store_order_bytes(uint8_t* p, uint64_t packed)
 {
-    uint64_t packed = 0;
-#pragma unroll
-    for (int j = 0; j < M; ++j)
-        packed |= (rank[j] < N) ? ((uint64_t)j << (8 * rank[j])) : 0ull;
     if constexpr (N == 1) {
         stream_store((uint8_t)packed, p);
     } else if constexpr (N == 2) {
@@ -211,6 +207,31 @@ __device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
 #pragma unroll
         for (int r = 0; r < N; ++r) p[r] = (uint8_t)(packed >> (8 * r));
     }
+}
+
+// The kept indices of a group in selection order (rank r at byte r).
+template <int M, int N>
+__device__ __forceinline__ void store_idx(uint8_t* p, const int (&rank)[M])
+{
+    uint64_t packed = 0;
+#pragma unroll
+    for (int j = 0; j < M; ++j)
+        packed |= (rank[j] < N) ? ((uint64_t)j << (8 * rank[j])) : 0ull;
+    store_order_bytes<N>(p, packed);
+}
+
+// W with the entries outside keep_bits cleared (m = 8).
+__device__ __forceinline__ void store_kept8(uint16_t* p, const uint32_t (&w)[8], uint32_t keep_bits)
+{
+    uint32_t packed[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const uint32_t mask = ((keep_bits >> (2 * t)) & 1u ? 0x0000FFFFu : 0u) |
+                              ((keep_bits >> (2 * t + 1)) & 1u ? 0xFFFF0000u : 0u);
+        packed[t] = (w[2 * t] | (w[2 * t + 1] << 16)) & mask;
+    }
+    const u32x4 v = {packed[0], packed[1], packed[2], packed[3]};
+    stream_store(v, reinterpret_cast<u32x4*>(p));
 }
 
 // The m Philox words of a group (block = its first Philox block index).
@@ -243,6 +264,70 @@ __device__ __forceinline__ void fast_keys(const float (&phi)[M], const uint32_t 
 {
 #pragma unroll
     for (int j = 0; j < M; ++j) k[j] = fast_key_log2(phi[j], c, x[j]);
+}
+
+// Hard top-n of eight hardware-log keys by sorting 32-bit integers: each key's
+// bits mapped to an unsigned integer of the same order, the low 3 bits
+// replaced by the entry's index, then the 19 comparators of an 8-input sorting
+// network (Knuth, TAOCP vol. 3, 5.3.4), each one unsigned max and min.
+// Clearing the 3 bits lowers a key by less than 8 ulps (2^-20 |K|), so the
+// margin of noise.hpp widens to kFastPairMargin + 2^-19 max|K|, checked on
+// the 7 pairs adjacent in sorted order.  Returns whether the keys are that
+// far apart (then the order is the exact keys' order and none tie); sets
+// keep_bits (bit j: entry j is among the n largest) and order (the indices
+// of ranks 0..n-1, one per byte).
+__device__ __forceinline__ uint32_t sortable_bits(float f)
+{
+    const uint32_t u = __float_as_uint(f);
+    return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u); // negative: ~u; else set the sign bit
+}
+
+__device__ __forceinline__ float float_of_sortable(uint32_t v)
+{
+    return __uint_as_float(v ^ (~(uint32_t)((int32_t)v >> 31) | 0x80000000u));
+}
+
+template <int I, int J>
+__device__ __forceinline__ void sort_pair_desc(uint32_t (&p)[8])
+{
+    const uint32_t a = p[I], b = p[J];
+    p[I] = a > b ? a : b;
+    p[J] = a > b ? b : a;
+}
+
+template <int N>
+__device__ __forceinline__ bool top8_fast(const float (&k)[8], uint32_t& keep_bits, uint64_t& order)
+{
+    uint32_t p[8];
+    float big = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        p[j] = (sortable_bits(k[j]) & ~7u) | (uint32_t)j;
+        big = fmaxf(big, fabsf(k[j]));
+    }
+    sort_pair_desc<0, 2>(p); sort_pair_desc<1, 3>(p); sort_pair_desc<4, 6>(p); sort_pair_desc<5, 7>(p);
+    sort_pair_desc<0, 4>(p); sort_pair_desc<1, 5>(p); sort_pair_desc<2, 6>(p); sort_pair_desc<3, 7>(p);
+    sort_pair_desc<0, 1>(p); sort_pair_desc<2, 3>(p); sort_pair_desc<4, 5>(p); sort_pair_desc<6, 7>(p);
+    sort_pair_desc<2, 4>(p); sort_pair_desc<3, 5>(p);
+    sort_pair_desc<1, 4>(p); sort_pair_desc<3, 6>(p);
+    sort_pair_desc<1, 2>(p); sort_pair_desc<3, 4>(p); sort_pair_desc<5, 6>(p);
+    const float margin = __builtin_fmaf(big, 0x1p-19f, kFastPairMargin);
+    bool sep = true;
+    float prev = float_of_sortable(p[0] & ~7u);
+#pragma unroll
+    for (int r = 1; r < 8; ++r) {
+        const float cur = float_of_sortable(p[r] & ~7u);
+        sep &= prev - cur > margin;
+        prev = cur;
+    }
+    keep_bits = 0u;
+    order = 0u;
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        keep_bits |= 1u << (p[r] & 7u);
+        order |= (uint64_t)(p[r] & 7u) << (8 * r);
+    }
+    return sep;
 }
 
 // A block works on one piece of the batch (common.hpp).  Each iteration of a
@@ -312,6 +397,26 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
             if (!kLaneTable && q >= ng) continue;
             uint32_t x[M];
             group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
+            if constexpr (M == 8 && !kRelax) {
+                // Sort the hardware-log keys; a group with a pair closer than
+                // the margin takes the exact keys and their ranks instead.
+                float kf[8];
+                fast_keys<8>(phi[u], x, a.key_c, kf);
+                uint32_t keep_bits;
+                uint64_t order;
+                if (top8_fast<N>(kf, keep_bits, order)) {
+                    store_kept8(pc.Wm + q * M, w[u], keep_bits);
+                    if (kWantIdx) store_order_bytes<N>(pc.idx + q * N, order);
+                } else {
+                    float kappa[8];
+                    int rank[8];
+                    exact_keys<8, kLambdaOne>(phi[u], x, a.lambda, tab, kappa);
+                    rank_keys<8>(kappa, rank);
+                    store_masked<8>(pc.Wm + q * M, w[u], rank, N);
+                    if (kWantIdx) store_idx<8, N>(pc.idx + q * N, rank);
+                }
+                continue;
+            }
             float kappa[M];
             if constexpr (kRelax) {
                 // the relaxation's soft mask is an fp32 output: exact keys
