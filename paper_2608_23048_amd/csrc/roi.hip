@@ -490,8 +490,9 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
 // Pure soft forward whose only output is W_soft = bf16(W (.) S) (neither S
 // nor the indices requested).  The relaxation runs on the hardware-log keys,
 // as in the backward: they are within the noise bound of noise.hpp of the
-// exact keys, which moves S by far less than the bf16 rounding of the
-// output.  No selection, no log cells.
+// exact keys.  The host picks this kernel only up to n / (tau min(1, lambda))
+// = kSoftFastLimit, where that moves S by far less than the bf16 rounding of
+// the output.  No selection, no log cells.
 template <int M, int N, int kQ>
 __global__ __launch_bounds__(kLaneBlock) void fwd_soft_lane_kernel(FwdBatch a)
 {

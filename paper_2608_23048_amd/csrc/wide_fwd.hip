@@ -100,7 +100,8 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
 }
 
 // Pure soft forward whose only output is bf16(W (.) S): the relaxation on the
-// hardware-log keys (as fwd_soft_lane_kernel in roi.hip), no selection.
+// hardware-log keys, no selection (as fwd_soft_lane_kernel in roi.hip, and
+// under the same limit on n / (tau min(1, lambda))).
 template <int M, int N, int kQ>
 __global__ __launch_bounds__(kBlock) void fwd_soft_wide_kernel(FwdBatch a)
 {
