@@ -288,12 +288,16 @@ __device__ __forceinline__ void wide_relax_backward(const StepRec<4> (&rec)[N],
             }
             t[e] = rec[k].mu[e] * mubar;
         }
-        float q[4], tl;
-        sums_but_one<4>(t, q, tl);
-        const float ext = sum_other_lanes<L>(tl);
+        // Sum over the group's entries but e: the other lanes' sum enters the
+        // two pair sums of this lane, so each is one add from them (no
+        // subtraction).
+        const float pa = t[0] + t[1], pb = t[2] + t[3];
+        const float ext = sum_other_lanes<L>(pa + pb);
+        const float pae = pa + ext, pbe = pb + ext;
+        const float q[4] = {t[1] + pbe, t[0] + pbe, pae + t[3], pae + t[2]};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float x = __builtin_fmaf(rec[k].om[e], sbar[e], -(q[e] + ext));
+            const float x = __builtin_fmaf(rec[k].om[e], sbar[e], -q[e]);
             const float m_t = kTauIsOne ? rec[k].mu[e] : rec[k].mu[e] * inv_tau;
             abar[e] = has_next ? __builtin_fmaf(m_t, x - a_in[e], abar[e]) : m_t * x;
         }
