@@ -817,6 +817,40 @@ def test_full_qwen15b_stack_wide(dev, name, n, m):
     full_workload_check(dev, name, n, m, 1.0, 0, 20000)
 
 
+@pytest.mark.parametrize("name,n,m,tau,step", [("qwen2.5-7b-stack-2:4", 2, 4, 0.1, 9),
+                                                 ("qwen2.5-1.5b-stack-16:32", 16, 32, 1.0, 0)])
+def test_full_soft_forward_alone(dev, name, n, m, tau, step):
+    """The soft forward with W_soft as its only output over a whole stack in
+    one call, as `bench.py --mode soft` runs it: the 7B stack at its last
+    annealing step (tau = 0.1, one group per lane) and the 1.5B stack at
+    16:32 (a group over eight lanes).  Sampled groups against the oracle's
+    W (.) S: within one bf16 rounding step plus the float tolerance."""
+    import torch
+    work = wl.WORKLOADS[name]
+    say(f"full soft forward alone {name} {n}:{m} tau={tau}: allocating {work.numel} weights")
+    W, L, G = wl.fill_slab(work, dev, step=step)
+    del G
+    Ws, _, _ = roi.mask_fwd(W, L, n, m, tau, 1.0, 0, step, 0, want_soft=False, want_idx=False,
+                            soft_forward=True)
+    torch.cuda.synchronize()
+    ng = work.numel // m
+    picks = sample_groups(work, ng, m, np.random.default_rng(4321 + step), 20000)
+    say(f"  comparing {picks.size} sampled groups with the oracle")
+    pt = torch.from_numpy(picks).to(dev)
+    take = lambda t: t.view(-1, m).index_select(0, pt)
+    Wg, Lg = take(W), take(L)
+    ge = picks.astype(np.uint64) * np.uint64(m)
+    _, S_o, _ = oracle.mask_fwd_groups(bf16_bits(Wg), f32(Lg), ge, n, m, float(np.float32(tau)),
+                                       1.0, 0, step, want_soft=True)
+    wf = (bf16_bits(Wg).astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1)
+    ref = wf * S_o.reshape(-1)
+    got = (bf16_bits(take(Ws)).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    ulp = np.where(ref != 0, 2.0 ** (np.floor(np.log2(np.abs(ref) + 1e-300)) - 7), 0.0)
+    assert_close(got.reshape(-1), ref, f"W (.) S ({name})", floor=ulp)
+    del W, L, Ws
+    torch.cuda.empty_cache()
+
+
 def check_sampled(dev, W, L, G, Wm, idx, d, n, m, tau, step, picks):
     """Sampled groups of a one-call slab against the oracle (indices and masked
     weights bit for bit, gradient within the tolerance)."""
