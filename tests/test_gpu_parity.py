@@ -478,6 +478,45 @@ def test_bwd_adamw_against_oracle(dev, case):
     assert t == 1 or wrong.mean() > 0.5
 
 
+def test_full_bwd_adamw_7b_stack(dev):
+    """The fused backward + AdamW over the whole 7B stack in one call, as
+    `bench.py --mode adamw` runs it (step 3 of the annealing: tau, the
+    learning rate and AdamW's step count t = 4).  Sampled groups of the
+    gradient, both moments and the updated logits against the oracle's
+    backward followed by its AdamW step."""
+    import torch
+    name, n, m, step = "qwen2.5-7b-stack-2:4", 2, 4, 3
+    work = wl.WORKLOADS[name]
+    say(f"full bwd+adamw {name}: allocating {work.numel} weights and moments")
+    W, L, G = wl.fill_slab(work, dev, step=step)
+    gen = torch.Generator(device=dev).manual_seed(99)
+    mom = torch.empty_like(L).normal_(0.0, 2e-5, generator=gen)
+    sec = torch.empty_like(L).uniform_(0.0, 1e-9, generator=gen)
+    tau = roi.anneal(1.0, 0.1, step, 9)
+    lr = roi.anneal(1e-3, 1e-4, step, 9)
+    ng = work.numel // m
+    picks = sample_groups(work, ng, m, np.random.default_rng(777), 20000)
+    pt = torch.from_numpy(picks).to(dev)
+    take = lambda t: t.view(-1, m).index_select(0, pt)
+    L0, m0, v0 = f32(take(L)), f32(take(mom)), f32(take(sec))
+    d = torch.empty_like(L)
+    roi.mask_bwd_adamw(G, W, L, mom, sec, n, m, tau, 1.0, 0, step, 0,
+                       opt=roi.adamw_params(lr, t=step + 1), grad_out=d)
+    torch.cuda.synchronize()
+    say(f"  comparing {picks.size} sampled groups with the oracle")
+    ge = picks.astype(np.uint64) * np.uint64(m)
+    d_o = oracle.mask_bwd_groups(bf16_bits(take(G)), bf16_bits(take(W)), L0, ge, n, m,
+                                 float(np.float32(tau)), 1.0, 0, step)
+    hp = [float(np.float32(x)) for x in (lr, 0.9, 0.95, 1e-8, 0.05)]
+    p_o, m_o, v_o = oracle.adamw(d_o, L0, m0, v0, *hp, step + 1)
+    assert_close(f32(take(d)), d_o, "grad_logits (fused, full stack)")
+    assert_close(f32(take(mom)), m_o, "exp_avg (full stack)")
+    assert_close(f32(take(sec)), v_o, "exp_avg_sq (full stack)")
+    assert_close(f32(take(L)), p_o, "logits after AdamW (full stack)")
+    del W, L, G, mom, sec, d
+    torch.cuda.empty_cache()
+
+
 def test_bwd_adamw_three_steps(dev):
     """Three training steps (forward, fused backward + AdamW) with the
     temperatures and the learning rate annealed: the GPU state against the
