@@ -704,6 +704,41 @@ def test_cat_sampler_against_oracle(dev, case):
     assert_close(f32(d), d_o, "dL/dalpha")
 
 
+def test_full_cat_7b_stack_2of4(dev):
+    """The categorical sampler over the whole 7B stack at 2:4 in one call per
+    direction, as `bench.py --mode cat` runs it (6 candidates per group; the
+    backward staged through its LDS tile).  40 windows of 300 consecutive
+    groups at random, unaligned places (so they cut across the tiles) against
+    the oracle: choices and masked weights bit for bit, dL/dalpha within the
+    tolerance."""
+    import torch
+    name, n, m, tau = "qwen2.5-7b-stack-2:4", 2, 4, 1.0
+    work = wl.WORKLOADS[name]
+    C = roi.cat_num_candidates(n, m)
+    ng = work.numel // m
+    say(f"full categorical {name}: allocating {work.numel} weights, {ng} x {C} logits")
+    W, L, G = wl.fill_slab(work, dev)
+    del L
+    A = torch.empty((ng, C), dtype=torch.float32, device=dev)
+    A.normal_(0.0, 1.0, generator=torch.Generator(device=dev).manual_seed(2468))
+    Wm, _, ch = roi.cat_mask_fwd(W, A, n, m, tau, 1.0, 5, 2, 0)
+    d = roi.cat_mask_bwd(G, W, A, n, m, tau, 1.0, 5, 2, 0)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(13579)
+    starts = np.concatenate([[0, ng - 300], rng.integers(0, ng - 300, 38)])
+    for g0 in starts.tolist():
+        sl = slice(g0 * m, (g0 + 300) * m)
+        Wm_o, _, ch_o = oracle.cat_fwd(bf16_bits(W[sl]), f32(A[g0:g0 + 300]), n, m, tau, 1.0, 5,
+                                       2, g0, want_soft=False)
+        d_o = oracle.cat_bwd(bf16_bits(G[sl]), bf16_bits(W[sl]), f32(A[g0:g0 + 300]), n, m, tau,
+                             1.0, 5, 2, g0)
+        assert np.array_equal(ch[g0:g0 + 300].cpu().numpy(), ch_o), f"choices differ at {g0}"
+        assert np.array_equal(bf16_bits(Wm[sl]).reshape(-1), Wm_o), f"masked weights differ at {g0}"
+        assert_close(f32(d[g0:g0 + 300]), d_o, f"dL/dalpha at group {g0}")
+    del W, G, A, Wm, ch, d
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("n,m", [(2, 4), (4, 8), (2, 8)])
 def test_cat_ties_and_near_ties(dev, n, m):
     """Logits built from the oracle's noise so that candidate keys tie exactly
