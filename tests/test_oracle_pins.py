@@ -452,6 +452,159 @@ def test_backward_extreme_keys_mpmath(kappa, n, tau):
     assert np.allclose(S, Smp, rtol=1e-12, atol=1e-300)
 
 
+# The floored branch: where 1 - mu falls below FLT_MIN the log is floored at
+# log(FLT_MIN) and passes no derivative (the stable form of the §3.2 update).
+FLT_MIN = float(np.finfo(np.float32).tiny)
+
+
+def mp_relaxation_floored(kappa, n, tau, floor=True):
+    """The §3.2 recursion in mpmath with the floor written out: alpha_j +=
+    log(max(omega_j, FLT_MIN)) with omega_j the sum of the other entries over
+    the total.  Returns S and, per step, the omegas that fed an update."""
+    import mpmath as mp
+    fmin = mp.mpf(FLT_MIN)
+    alpha = list(kappa)
+    S = [mp.mpf(0)] * len(alpha)
+    omegas = []
+    for k in range(n):
+        a_max = max(alpha)
+        e = [mp.exp((a - a_max) / tau) for a in alpha]
+        t = mp.fsum(e)
+        mu = [x / t for x in e]
+        S = [s + x for s, x in zip(S, mu)]
+        om = [mp.fsum(e[:j] + e[j + 1:]) / t for j in range(len(e))]
+        if k + 1 < n:
+            omegas.append(om)
+        alpha = [a + mp.log(max(o, fmin) if floor else o) for a, o in zip(alpha, om)]
+    return S, omegas
+
+
+def mp_floored_gradient(kappa, n, tau, sbar, floor=True):
+    """60-digit central differences of sum_j sbar_j S_j; the step is far too
+    small to move any omega across the floor, so this is the exact derivative
+    of the floored recursion."""
+    import mpmath as mp
+    mp.mp.dps = 60
+    h = mp.mpf("1e-25")
+    out = []
+    for j in range(len(kappa)):
+        kp = [mp.mpf(x) for x in kappa]
+        km = [mp.mpf(x) for x in kappa]
+        kp[j] += h
+        km[j] -= h
+        sp, _ = mp_relaxation_floored(kp, n, mp.mpf(tau), floor)
+        sm, _ = mp_relaxation_floored(km, n, mp.mpf(tau), floor)
+        out.append(float(mp.fsum((a - b) * mp.mpf(float(s)) for a, b, s in zip(sp, sm, sbar))
+                         / (2 * h)))
+    return np.array(out)
+
+
+FLOOR_CASES = [
+    # The first pick's 1 - mu is ~e^-100 (or smaller), below FLT_MIN, and the
+    # floored entry's alpha = kappa + log(FLT_MIN) still counts at later steps,
+    # so the floor changes both S and its derivative.
+    ([100.0, 0.0, 0.5, -1.0], 2, 1.0),
+    ([100.0, 0.0, 0.5, -1.0], 3, 1.0),
+    ([89.5, 0.0, 0.5, -1.0], 3, 1.0),        # floored entry competes again at step 2
+    ([100.0, 0.0, 0.25, -0.5], 2, 0.5),
+    ([100.0, 0.0, 0.25, -0.5], 3, 0.5),
+    ([250.0, 0.0, 0.5, -1.0], 3, 1.0),       # floored at steps 1 and 2
+    ([200.0, 0.0, 1.0, -1.0, 0.4, -0.3, 0.8, 0.1], 4, 2.0),
+    ([100.0, 0.0, 0.3, -0.6, 0.1, -0.2, 0.5, 0.2], 3, 0.6),
+]
+
+
+@pytest.mark.parametrize("kappa,n,tau", FLOOR_CASES)
+def test_floored_branch_forward_and_backward_mpmath(kappa, n, tau):
+    """Forward S and backward dS of the oracle's floored branch (keep = 1 for
+    a floored entry's carried gradient, and no 1/omega term) against the
+    recursion with the floor written out in mpmath and differentiated by
+    60-digit central differences."""
+    import mpmath as mp
+    mp.mp.dps = 60
+    m = len(kappa)
+    sbar = np.random.default_rng(29 + m + n).normal(size=m)
+    S_mp, omegas = mp_relaxation_floored([mp.mpf(x) for x in kappa], n, mp.mpf(tau))
+    # the case really reaches the floor at an updating step, and no omega sits
+    # near it (the finite difference must not cross it)
+    om = np.array([[float(o) for o in row] for row in omegas])
+    assert (om < FLT_MIN).any(), "case does not reach the floor"
+    assert np.all((om < 0.5 * FLT_MIN) | (om > 2.0 * FLT_MIN))
+    S = oracle.relax_fwd(np.array(kappa), n, tau)
+    assert np.allclose(S, np.array([float(x) for x in S_mp]), rtol=1e-12, atol=1e-300)
+    ref = mp_floored_gradient(kappa, n, tau, sbar)
+    got = oracle.relax_bwd(np.array(kappa), n, tau, sbar)
+    assert np.allclose(got, ref, rtol=1e-9, atol=1e-12 * np.abs(sbar).max()), (got, ref)
+    # The floor changes the derivative: the unfloored recursion's gradient
+    # differs, so a sweep that ignored the floor would fail the check above.
+    unfloored = mp_floored_gradient(kappa, n, tau, sbar, floor=False)
+    assert np.abs(unfloored - ref).max() > 1e-3 * np.abs(ref).max()
+
+
+@pytest.mark.parametrize("kappa,n,tau", FLOOR_CASES)
+def test_floored_branch_matches_torch_autograd_with_clamp(kappa, n, tau):
+    """The same branch through torch fp64 autograd: the update written as
+    alpha + log(clamp(omega, min=FLT_MIN)), omega the sum of the other
+    exponentials over the total (clamp passes no gradient below its bound)."""
+    import torch
+    m = len(kappa)
+    sbar = np.random.default_rng(31 + m + n).normal(size=m)
+    k = torch.tensor(kappa, dtype=torch.float64, requires_grad=True)
+    others_of = 1.0 - torch.eye(m, dtype=torch.float64)
+    alpha, S = k, torch.zeros_like(k)
+    for step in range(n):
+        e = torch.exp((alpha - alpha.max().detach()) / tau)
+        t = e.sum()
+        S = S + e / t
+        if step + 1 < n:
+            alpha = alpha + torch.log(torch.clamp(others_of @ e / t, min=FLT_MIN))
+    (S * torch.tensor(sbar, dtype=torch.float64)).sum().backward()
+    got = oracle.relax_bwd(np.array(kappa), n, tau, sbar)
+    assert np.allclose(got, k.grad.numpy(), rtol=1e-9, atol=1e-12 * np.abs(sbar).max())
+    assert np.allclose(oracle.relax_fwd(np.array(kappa), n, tau), S.detach().numpy(), rtol=1e-12)
+
+
+def test_floored_branch_planted_mistake_is_caught():
+    """A plausible slip in the floored branch -- carrying a floored entry's
+    gradient with the unfloored factor (omega + tau - 1) / tau instead of 1 --
+    is far outside the tolerance of the pins above.  The slip is emulated on
+    the CPU by a literal fp64 sweep of the derivation, checked first to agree
+    with the oracle when written correctly."""
+    def sweep(kappa, n, tau, sbar, slip):
+        m = len(kappa)
+        alpha = np.array(kappa, dtype=np.float64)
+        recs = []
+        for _ in range(n):
+            e = np.exp((alpha - alpha.max()) / tau)
+            t = e.sum()
+            mu = e / t
+            om = np.array([(e.sum() - e[j]) if e[j] < 0.5 * t else np.delete(e, j).sum()
+                           for j in range(m)]) / t
+            fl = om < FLT_MIN
+            recs.append((mu, om, fl))
+            alpha = alpha + np.log(np.maximum(om, FLT_MIN))
+        a = np.zeros(m)
+        for k in range(n - 1, -1, -1):
+            mu, om, fl = recs[k]
+            nxt = k < n - 1
+            mubar = sbar - (np.where(fl, 0.0, a / om) if nxt else 0.0)
+            others = np.array([np.delete(mu * mubar, i).sum() for i in range(m)])
+            soft = mu / tau * (om * sbar - others)
+            keep = (om + (tau - 1.0)) / tau
+            if not slip:
+                keep = np.where(fl, 1.0, keep)
+            a = (a * keep if nxt else 0.0) + soft
+        return a
+
+    kappa, n, tau = [100.0, 0.0, 0.5, -1.0], 3, 1.0
+    sbar = np.random.default_rng(37).normal(size=4)
+    ref = mp_floored_gradient(kappa, n, tau, sbar)
+    tol = dict(rtol=1e-9, atol=1e-12 * np.abs(sbar).max())
+    assert np.allclose(sweep(kappa, n, tau, sbar, slip=False), ref, **tol)
+    assert np.allclose(oracle.relax_bwd(np.array(kappa), n, tau, sbar), ref, **tol)
+    assert not np.allclose(sweep(kappa, n, tau, sbar, slip=True), ref, **tol)
+
+
 def test_backward_uniform_upstream_is_zero():
     """sum_j S_j = N for every kappa, so a constant upstream gradient has zero
     derivative."""
