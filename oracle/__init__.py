@@ -29,7 +29,7 @@ GCC_FLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-f
 def build(verbose: bool = False) -> str:
     """Compile ``liboracle.so`` with gcc (always recompiles)."""
     tmp = f"{_LIB_PATH}.tmp{os.getpid()}"
-    cmd = ["gcc", *GCC_FLAGS, _SRC, "-o", tmp, "-lm"]
+    cmd = ["gcc", *GCC_FLAGS, _SRC, "-o", tmp, "-lm", "-lpthread"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
@@ -92,6 +92,14 @@ def lib():
         L.roi_oracle_bwd_groups.argtypes = [_u16p, _u16p, _f32p, _i64, _u64p, _int, _int, _f32,
                                             _f32, _u64, _u64, _f64p]
         L.roi_oracle_bwd_groups.restype = _int
+        L.roi_oracle_fwd_mt.argtypes = [_u16p, _f32p, _i64, _int, _int, _f32, _f32, _u64, _u64,
+                                        _u64, _u16p, _f64p, _u8p, _int]
+        L.roi_oracle_fwd_mt.restype = _int
+        L.roi_oracle_bwd_mt.argtypes = [_u16p, _u16p, _f32p, _i64, _int, _int, _f32, _f32, _u64,
+                                        _u64, _u64, _f64p, _int]
+        L.roi_oracle_bwd_mt.restype = _int
+        L.oracle_relax_bwd_groups.argtypes = [_f64p, _i64, _int, _int, _f64, _f64p, _f64p, _int]
+        L.oracle_relax_bwd_groups.restype = _int
         L.oracle_anneal.argtypes = [_f64, _f64, _f64, _f64]
         L.oracle_anneal.restype = _f64
         L.oracle_adamw.argtypes = [_f64p, _i64, _f64, _f64, _f64, _f64, _f64, _i64, _f32p, _f32p,
@@ -277,9 +285,25 @@ def cat_bwd(G_bits, W_bits, alpha, n: int, m: int, tau: float, lam: float, seed:
 
 
 # --------------------------------------------------------------------------- whole arrays
+# The CPU share of one GPU on the machines the suite runs on.
+MAX_THREADS = 16
+
+
+def host_threads() -> int:
+    """Threads for the threaded oracle: the cores this process may run on,
+    at most MAX_THREADS."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count() or 1
+    return max(1, min(MAX_THREADS, n))
+
+
 def mask_fwd(W_bits: np.ndarray, logits: np.ndarray, n: int, m: int, tau: float, lam: float,
-             seed: int, step: int, elem_offset: int = 0, want_soft: bool = True):
-    """Returns (W_masked bits uint16, soft mask float64 or None, sel_idx uint8 [G, n])."""
+             seed: int, step: int, elem_offset: int = 0, want_soft: bool = True,
+             threads: int = 1):
+    """Returns (W_masked bits uint16, soft mask float64 or None, sel_idx uint8 [G, n]).
+    threads > 1 splits the groups over that many threads (same bits)."""
     W = np.ascontiguousarray(W_bits, dtype=np.uint16).reshape(-1)
     p = np.ascontiguousarray(logits, dtype=np.float32).reshape(-1)
     assert W.size == p.size
@@ -287,22 +311,40 @@ def mask_fwd(W_bits: np.ndarray, logits: np.ndarray, n: int, m: int, tau: float,
     Wm = np.empty(numel, dtype=np.uint16)
     S = np.empty(numel, dtype=np.float64) if want_soft else None
     idx = np.empty(numel // m * n, dtype=np.uint8)
-    _check(lib().roi_oracle_fwd(_ptr(W, ctypes.c_uint16), _ptr(p, ctypes.c_float), numel, n, m,
-                                tau, lam, seed, step, elem_offset, _ptr(Wm, ctypes.c_uint16),
-                                _ptr(S, ctypes.c_double), _ptr(idx, ctypes.c_uint8)), "fwd")
+    args = (_ptr(W, ctypes.c_uint16), _ptr(p, ctypes.c_float), numel, n, m, tau, lam, seed,
+            step, elem_offset, _ptr(Wm, ctypes.c_uint16), _ptr(S, ctypes.c_double),
+            _ptr(idx, ctypes.c_uint8))
+    rc = lib().roi_oracle_fwd(*args) if threads <= 1 else lib().roi_oracle_fwd_mt(*args, threads)
+    _check(rc, "fwd")
     return Wm, S, idx.reshape(-1, n)
 
 
 def mask_bwd(G_bits: np.ndarray, W_bits: np.ndarray, logits: np.ndarray, n: int, m: int,
-             tau: float, lam: float, seed: int, step: int, elem_offset: int = 0) -> np.ndarray:
+             tau: float, lam: float, seed: int, step: int, elem_offset: int = 0,
+             threads: int = 1) -> np.ndarray:
     G = np.ascontiguousarray(G_bits, dtype=np.uint16).reshape(-1)
     W = np.ascontiguousarray(W_bits, dtype=np.uint16).reshape(-1)
     p = np.ascontiguousarray(logits, dtype=np.float32).reshape(-1)
     assert G.size == W.size == p.size
     d = np.empty(p.size, dtype=np.float64)
-    _check(lib().roi_oracle_bwd(_ptr(G, ctypes.c_uint16), _ptr(W, ctypes.c_uint16),
-                                _ptr(p, ctypes.c_float), p.size, n, m, tau, lam, seed, step,
-                                elem_offset, _ptr(d, ctypes.c_double)), "bwd")
+    args = (_ptr(G, ctypes.c_uint16), _ptr(W, ctypes.c_uint16), _ptr(p, ctypes.c_float), p.size,
+            n, m, tau, lam, seed, step, elem_offset, _ptr(d, ctypes.c_double))
+    rc = lib().roi_oracle_bwd(*args) if threads <= 1 else lib().roi_oracle_bwd_mt(*args, threads)
+    _check(rc, "bwd")
+    return d
+
+
+def relax_bwd_groups(kappa, n: int, tau: float, sbar, threads: int = 1) -> np.ndarray:
+    """The relaxation's backward on given keys: kappa, sbar [groups, m] (fp64);
+    returns dL/dkappa [groups, m]."""
+    k = np.ascontiguousarray(kappa, dtype=np.float64)
+    sb = np.ascontiguousarray(sbar, dtype=np.float64)
+    assert k.ndim == 2 and k.shape == sb.shape
+    d = np.empty(k.shape, dtype=np.float64)
+    _check(lib().oracle_relax_bwd_groups(_ptr(k, ctypes.c_double), k.shape[0], k.shape[1], n,
+                                         tau, _ptr(sb, ctypes.c_double),
+                                         _ptr(d, ctypes.c_double), max(1, threads)),
+           "relax_bwd_groups")
     return d
 
 

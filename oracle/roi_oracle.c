@@ -1,5 +1,5 @@
 /*
- * roi_oracle.c -- plain, slow, single-threaded CPU oracle of the RoI
+ * roi_oracle.c -- plain, slow, scalar CPU oracle of the RoI
  * differentiable N:M mask sampler (arxiv 2608.23048, "Reservoir of Importance").
  *
  * TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT.  Only the test suite, the
@@ -45,6 +45,7 @@
 
 #include <float.h>
 #include <math.h>
+#include <pthread.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -692,4 +693,142 @@ int oracle_cat_bwd(const uint16_t* G, const uint16_t* W, const float* alpha, int
             dalpha[q * C + c] = y[c] * (ybar[c] - dot) / (double)tau / (double)lambda;
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------- *
+ * 11. The whole-array forward and backward on several threads.  Groups are
+ *     independent (§4.1: each group of m weights gets its own mask; the noise
+ *     of an element depends only on its global index), so the groups are cut
+ *     into contiguous ranges, one per POSIX thread, and each thread runs the
+ *     scalar per-group code above on its range.  The outputs are the same
+ *     bits for every thread count.  Also the relaxation's backward on given
+ *     keys over many groups (the tests' fp32 rounding allowance).
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    int kind; /* 0 forward, 1 backward, 2 relaxation backward on given keys */
+    int64_t g0, g1;
+    const uint16_t *W, *G;
+    const float* logits;
+    const double *kappa, *sbar;
+    int n, m;
+    float tau, lambda;
+    double tau64; /* the relaxation's temperature for kind 2 */
+    uint64_t seed, step, elem_offset;
+    uint16_t* Wm;
+    double *S, *out;
+    uint8_t* idx;
+    int status;
+} mt_job;
+
+static void* mt_run(void* arg)
+{
+    mt_job* j = (mt_job*)arg;
+    relax_step* steps = (relax_step*)malloc(sizeof(relax_step) * (size_t)j->n);
+    if (!steps) {
+        j->status = -2;
+        return NULL;
+    }
+    const int m = j->m;
+    for (int64_t q = j->g0; q < j->g1; ++q) {
+        const int64_t base = q * m;
+        if (j->kind == 0) {
+            group_fwd(j->W + base, j->logits + base, j->n, m, j->tau, j->lambda, j->seed, j->step,
+                      j->elem_offset + (uint64_t)base, j->Wm + base, j->S ? j->S + base : NULL,
+                      j->idx ? j->idx + q * j->n : NULL, steps);
+        } else if (j->kind == 1) {
+            group_bwd(j->G + base, j->W + base, j->logits + base, j->n, m, j->tau, j->lambda,
+                      j->seed, j->step, j->elem_offset + (uint64_t)base, j->out + base, steps);
+        } else {
+            relax_forward(j->kappa + base, m, j->n, j->tau64, steps, NULL);
+            relax_backward(steps, m, j->n, j->tau64, j->sbar + base, j->out + base);
+        }
+    }
+    free(steps);
+    j->status = 0;
+    return NULL;
+}
+
+static int mt_launch(mt_job proto, int64_t ngroups, int threads)
+{
+    if (threads < 1) threads = 1;
+    if (threads > 256) threads = 256;
+    if ((int64_t)threads > ngroups) threads = ngroups > 0 ? (int)ngroups : 1;
+    mt_job jobs[256];
+    pthread_t tid[256];
+    int started[256];
+    int status = 0;
+    for (int t = 0; t < threads; ++t) {
+        jobs[t] = proto;
+        jobs[t].g0 = ngroups * t / threads;
+        jobs[t].g1 = ngroups * (t + 1) / threads;
+        jobs[t].status = -3;
+        started[t] = pthread_create(&tid[t], NULL, mt_run, &jobs[t]) == 0;
+        if (!started[t]) mt_run(&jobs[t]); /* run it here instead */
+    }
+    for (int t = 0; t < threads; ++t) {
+        if (started[t]) pthread_join(tid[t], NULL);
+        if (jobs[t].status) status = jobs[t].status;
+    }
+    return status;
+}
+
+int roi_oracle_fwd_mt(const uint16_t* W, const float* logits, int64_t numel, int n, int m,
+                      float tau, float lambda, uint64_t seed, uint64_t step, uint64_t elem_offset,
+                      uint16_t* W_masked, double* soft_mask, uint8_t* sel_idx, int threads)
+{
+    if (check_args(numel, n, m, tau, lambda) || numel % m != 0) return -1;
+    mt_job j;
+    memset(&j, 0, sizeof j);
+    j.kind = 0;
+    j.W = W;
+    j.logits = logits;
+    j.n = n;
+    j.m = m;
+    j.tau = tau;
+    j.lambda = lambda;
+    j.seed = seed;
+    j.step = step;
+    j.elem_offset = elem_offset;
+    j.Wm = W_masked;
+    j.S = soft_mask;
+    j.idx = sel_idx;
+    return mt_launch(j, numel / m, threads);
+}
+
+int roi_oracle_bwd_mt(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
+                      int64_t numel, int n, int m, float tau, float lambda, uint64_t seed,
+                      uint64_t step, uint64_t elem_offset, double* grad_logits, int threads)
+{
+    if (check_args(numel, n, m, tau, lambda) || numel % m != 0) return -1;
+    mt_job j;
+    memset(&j, 0, sizeof j);
+    j.kind = 1;
+    j.G = grad_W_masked;
+    j.W = W;
+    j.logits = logits;
+    j.n = n;
+    j.m = m;
+    j.tau = tau;
+    j.lambda = lambda;
+    j.seed = seed;
+    j.step = step;
+    j.elem_offset = elem_offset;
+    j.out = grad_logits;
+    return mt_launch(j, numel / m, threads);
+}
+
+int oracle_relax_bwd_groups(const double* kappa, int64_t ngroups, int m, int n, double tau,
+                            const double* sbar, double* dkappa, int threads)
+{
+    if (ngroups < 0 || m < 1 || m > ORACLE_MAX_M || n < 1 || n > m || !(tau > 0.0)) return -1;
+    mt_job j;
+    memset(&j, 0, sizeof j);
+    j.kind = 2;
+    j.kappa = kappa;
+    j.sbar = sbar;
+    j.n = n;
+    j.m = m;
+    j.tau64 = tau;
+    j.out = dkappa;
+    return mt_launch(j, ngroups, threads);
 }

@@ -7,7 +7,8 @@
  * smoke check and the benchmark's CPU-baseline leg may load this library.
  * It shares no code, header, table or constant with the HIP library.
  *
- * Every pointer is a host pointer.  Floating-point outputs of the relaxation
+ * Every pointer is a host pointer.  The arithmetic is scalar C; the *_mt
+ * entry points only split the groups over threads.  Floating-point outputs of the relaxation
  * and of the backward are fp64; keys are fp32 because the noise definition
  * fixes them in fp32 (see roi_oracle.c).
  */
@@ -52,6 +53,18 @@ int roi_oracle_fwd_groups(const uint16_t* W, const float* logits, int64_t ngroup
 int roi_oracle_bwd_groups(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
                           int64_t ngroups, const uint64_t* group_elem, int n, int m, float tau,
                           float lambda, uint64_t seed, uint64_t step, double* grad_logits);
+
+/* The whole-array forward and backward on `threads` POSIX threads (contiguous
+ * ranges of groups; the same bits for any thread count), and the relaxation's
+ * backward on given fp64 keys over ngroups groups of m. */
+int roi_oracle_fwd_mt(const uint16_t* W, const float* logits, int64_t numel, int n, int m,
+                      float tau, float lambda, uint64_t seed, uint64_t step, uint64_t elem_offset,
+                      uint16_t* W_masked, double* soft_mask, uint8_t* sel_idx, int threads);
+int roi_oracle_bwd_mt(const uint16_t* grad_W_masked, const uint16_t* W, const float* logits,
+                      int64_t numel, int n, int m, float tau, float lambda, uint64_t seed,
+                      uint64_t step, uint64_t elem_offset, double* grad_logits, int threads);
+int oracle_relax_bwd_groups(const double* kappa, int64_t ngroups, int m, int n, double tau,
+                            const double* sbar, double* dkappa, int threads);
 
 /* Exponential annealing of a temperature. */
 double oracle_anneal(double v_init, double v_end, double t, double t_anneal);
