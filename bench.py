@@ -309,24 +309,43 @@ def copy_reference(nbytes: int = 1 << 32, reps: int = 3) -> dict:
 
 def cpu_baseline(W, L, G, work, n, m, tau):
     """The CPU oracle, as it is, on a bounded sample of the same workload: the
-    q, k, v, o and gate projections of layer 0 (about 10 s of one core), one
-    forward + backward."""
+    seven tensors of layer 0 (one mask forward + backward) on the host's
+    cores -- the oracle's threaded entry points split the groups over POSIX
+    threads, at most the 16 cores that are one GPU's share of the host --
+    plus the single-threaded oracle on the 896x896 layer (2:4, tau = 1)."""
     import numpy as np
     import torch
 
     import oracle
+    from paper_2608_23048_amd import workloads as wl
 
-    sample = [t for t in work.tensors[:5]]
-    end = sample[-1].offset + sample[-1].numel
+    threads = oracle.host_threads()
+    layer = [t for t in work.tensors if t.name.startswith("layers.0.")] or list(work.tensors[:1])
+    end = layer[-1].offset + layer[-1].numel
     bits = lambda t: t[:end].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     Wb, Gb, Lf = bits(W), bits(G), L[:end].cpu().numpy()
     t0 = time.perf_counter()
-    oracle.mask_fwd(Wb, Lf, n, m, tau, 1.0, 0, 0, 0, want_soft=False)
-    oracle.mask_bwd(Gb, Wb, Lf, n, m, tau, 1.0, 0, 0, 0)
+    oracle.mask_fwd(Wb, Lf, n, m, tau, 1.0, 0, 0, 0, want_soft=False, threads=threads)
+    oracle.mask_bwd(Gb, Wb, Lf, n, m, tau, 1.0, 0, 0, 0, threads=threads)
     dt = time.perf_counter() - t0
-    names = "+".join(t.name.split(".")[-1] for t in sample)
-    return {"value": end / dt, "unit": "masked weights/s", "cores": 1, "kind": "oracle",
-            "sample": f"layer 0 {names} ({end} weights), one mask fwd+bwd, {dt:.1f} s on 1 thread"}
+    del Wb, Gb, Lf
+    # the single-threaded figure on the one-layer workload
+    single = wl.WORKLOADS["single-896x896-2:4"]
+    W1, L1, G1 = wl.fill_slab(single, "cpu")
+    b1 = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
+    t1 = time.perf_counter()
+    oracle.mask_fwd(b1(W1), L1.numpy(), single.n, single.m, single.tau, 1.0, 0, 0, 0,
+                    want_soft=False)
+    oracle.mask_bwd(b1(G1), b1(W1), L1.numpy(), single.n, single.m, single.tau, 1.0, 0, 0, 0)
+    dt1 = time.perf_counter() - t1
+    names = "+".join(t.name.split(".")[-1] for t in layer)
+    return {"value": end / dt, "unit": "masked weights/s", "cores": threads, "kind": "oracle",
+            "host_cpus": os.cpu_count(),
+            "sample": f"layer 0 ({names}, {end} weights), one mask fwd+bwd, {dt:.2f} s on "
+                      f"{threads} threads",
+            "single_thread": {"value": single.numel / dt1, "unit": "masked weights/s",
+                              "cores": 1, "sample": f"{single.name} ({single.numel} weights), "
+                                                    f"one mask fwd+bwd, {dt1:.2f} s"}}
 
 
 def forward_soft_flops(n: int) -> int:

@@ -103,15 +103,9 @@ int roi_mask_fwd(const uint16_t* W, const float* logits, int64_t rows, int64_t c
  * and soft_mask / sel_idx, when not NULL, receive S and the hard top-n indices
  * of the same keys.  The backward is roi_mask_bwd (the relaxation is the
  * differentiated path in both settings).
- * Precision: when soft_mask or sel_idx is given, S comes from the exact keys,
- * as in roi_mask_fwd, and W_soft is the bf16 rounding of W (.) S.  With both
- * NULL and n / (tau min(1, lambda)) <= 160, S is evaluated at keys from the
- * hardware logarithm, within a proven bound of the exact keys (as in
- * roi_mask_bwd).  The change in S is then far below the bf16 rounding of
- * W_soft.  The tests check it against the oracle to one bf16 step, and
- * against the exact-key output to one bf16 step per element, up to that
- * limit.  Past the limit (the key error's effect on S grows with n / tau and
- * with 1 / lambda) the exact keys are used.
+ * S is always evaluated at the exact keys (as in roi_mask_fwd), and W_soft is
+ * the bf16 rounding of W (.) S; with soft_mask and sel_idx both NULL a kernel
+ * without the selection runs, with the same W_soft bits.
  */
 int roi_mask_fwd_soft(const uint16_t* W, const float* logits, int64_t rows, int64_t cols, int n,
                       int m, float tau, float lambda, uint64_t seed, uint64_t step,
@@ -126,7 +120,8 @@ int roi_mask_fwd_soft(const uint16_t* W, const float* logits, int64_t rows, int6
  * relaxation as if W_masked = W (.) S.  So dL/dS = grad_W_masked (.) W (exact
  * in fp32), dL/dkappa is the reverse-mode derivative of the §3.2 recursion,
  * and dL/dphi = dL/dkappa / lambda.  The keys are regenerated from
- * (seed, step, elem_offset) and must match the forward call's arguments.
+ * (seed, step, elem_offset) and must match the forward call's arguments: the
+ * derivative is taken at exactly the fp32 keys the forward sampled.
  *
  *  grad_W_masked bf16 [rows, cols]       (read)
  *  W, logits, rows, cols, n, m, tau, lambda, seed, step, elem_offset: as in
@@ -304,10 +299,10 @@ int roi_gumbel_from_words(const uint32_t* words, int64_t count, float* gumbel,
 /*
  * roi_fast_noise_from_words -- the noise in log2 units from the hardware
  * logarithm, K(x) = -log2(-log2 u(x)) = g log2(e) + log2(ln 2) up to a few
- * ulp: the form the kernels use where fp32 accuracy suffices (the backward's
- * relaxation; the forward's key comparisons, which fall back to the exact
- * keys whenever two keys are closer than the proven bound of this form's
- * error).  words uint32 [count] (read), out fp32 [count] (written).
+ * ulp: the form the straight-through forwards use for their key comparisons,
+ * falling back to the exact keys whenever two keys are closer than the proven
+ * bound of this form's error (no relaxation uses it).  words uint32 [count]
+ * (read), out fp32 [count] (written).
  */
 int roi_fast_noise_from_words(const uint32_t* words, int64_t count, float* out, hipStream_t stream);
 

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(PKG, "libroi.so")
 SOURCES = [os.path.join(CSRC, "roi.hip"), os.path.join(CSRC, "wide_fwd.hip"),
            os.path.join(CSRC, "wide_bwd.hip"),
            os.path.join(CSRC, "export.hip"), os.path.join(CSRC, "cat.hip"),
-           os.path.join(CSRC, "stream_copy.hip")]
+           os.path.join(CSRC, "stream_copy.hip"), os.path.join(CSRC, "checks.cpp")]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

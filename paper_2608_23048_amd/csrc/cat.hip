@@ -12,7 +12,7 @@
 // the straight-through derivative through that softmax.  As in the item
 // sampler: the forward without S decides with the hardware-log keys when the
 // top two are further apart than their error margin (else with the exact
-// keys); S uses the exact keys; the backward uses the hardware-log keys.
+// keys); S and the backward use the exact keys.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -321,11 +321,16 @@ __global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_bwd_kernel
     constexpr int B = cat_block(C);
     constexpr bool kStage = cat_staged_bwd(C);
     __shared__ float tile[kStage ? B * C : 2];
+    // Every group takes the exact keys: each wave keeps its own copy of the
+    // log cells in LDS (noise.hpp).
+    __shared__ float4 wave_tabs[B / 64][kLogCells / 2];
+    const float2* tab = reinterpret_cast<const float2*>(wave_tabs[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)]);
     // The loop bound is uniform over the block (the tile copies are cooperative).
     for (int64_t base = (int64_t)blockIdx.x * B; base < a.ngroups; base += (int64_t)gridDim.x * B) {
         const int here = (int)(a.ngroups - base < B ? a.ngroups - base : B);
         const int64_t q = base + threadIdx.x;
         const bool live = (int)threadIdx.x < here;
+        const float4 cells = log_cells_of_lane();
         float alpha[C];
         if constexpr (kStage) {
             tile_in<B>(a.alpha + base * C, tile, here * C);
@@ -339,16 +344,19 @@ __global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_bwd_kernel
             load_cat_logits<C>(a.alpha + q * C, alpha);
         }
         float d[C];
-        if (live) {
         uint32_t w[M], g[M];
-        load_bf16<M>(a.W + q * M, w);
-        load_bf16<M>(a.G + q * M, g);
+        if (live) {
+            load_bf16<M>(a.W + q * M, w);
+            load_bf16<M>(a.G + q * M, g);
+        }
+        publish_wave_log_table(const_cast<float2*>(tab), cells);
+        if (live) {
         uint32_t x[C];
         cat_words<C>(a.group0 + (uint64_t)q, a.key, x);
+        // the keys the forward sampled: kappa = fl(fl(alpha / lambda) + g)
         float y[C];
-#pragma unroll
-        for (int c = 0; c < C; ++c) y[c] = fast_key_log2(alpha[c], a.key_c, x[c]);
-        cat_softmax<C>(y, a.inv_tau); // keys are in log2 units already
+        cat_exact_keys<C>(alpha, x, a.lambda, tab, y);
+        cat_softmax<C>(y, kLog2e * a.inv_tau);
         // Straight-through: dL/dS = dL/dW_masked (.) W; ybar_c = sum_{j in c} sbar_j.
         float sbar[M];
 #pragma unroll
@@ -420,39 +428,12 @@ int cat_run(bool fwd, const uint16_t* W, const float* alpha, const uint16_t* G, 
             hipStream_t stream)
 {
     const char* what = fwd ? "roi_cat_mask_fwd" : "roi_cat_mask_bwd";
-    if (rows < 0 || cols < 0) return fail(ROI_E_INVAL, "rows and cols must be >= 0");
-    if (m < 1 || n < 1 || n > m)
-        return fail(ROI_E_INVAL, "pattern n:m = %d:%d needs 1 <= n <= m", n, m);
-    if (m != 4 && m != 8)
-        return fail(ROI_E_UNSUPPORTED, "the categorical sampler is built for m = 4 and 8");
-    if (cols % m != 0) return fail(ROI_E_INVAL, "cols must be a multiple of m");
-    if (rows > 0 && cols > ((int64_t)1 << 62) / rows)
-        return fail(ROI_E_INVAL, "rows * cols must be below 2^62");
-    if (!(tau > 0.0f) || !std::isfinite(tau)) return fail(ROI_E_INVAL, "tau must be finite, > 0");
-    if (!(lambda > 0.0f) || !std::isfinite(lambda))
-        return fail(ROI_E_INVAL, "lambda must be finite and > 0");
-    const int C = binom(m, n);
-    const int64_t ngroups = rows * cols / m;
-    const uint64_t B = (uint64_t)(C + 3) / 4;
-    if (ngroups > 0 && group_offset > (UINT64_MAX / (4 * B)) - (uint64_t)ngroups)
-        return fail(ROI_E_INVAL, "group_offset + groups overflows the noise index space");
+    int64_t ngroups;
+    int C;
+    if (int st = validate_cat(fwd, W, alpha, G, rows, cols, n, m, tau, lambda, group_offset,
+                              W_masked, S, choice, dalpha, &ngroups, &C))
+        return st;
     if (ngroups == 0) return ok();
-    if (!W || !alpha || (fwd ? !W_masked : (!G || !dalpha)))
-        return fail(ROI_E_INVAL, "a required pointer is NULL");
-    const void* ptrs[] = {W, alpha, G, W_masked, S, choice, dalpha};
-    for (const void* p : ptrs)
-        if (p && ((uintptr_t)p & 15u))
-            return fail(ROI_E_INVAL, "device pointers must be 16-byte aligned");
-    const size_t numel = (size_t)ngroups * (size_t)m, nc = (size_t)ngroups * (size_t)C;
-    std::vector<Range> r;
-    add_range(r, W, numel * 2, false);
-    add_range(r, alpha, nc * 4, false);
-    add_range(r, G, numel * 2, false);
-    add_range(r, W_masked, numel * 2, true);
-    add_range(r, S, numel * 4, true);
-    add_range(r, choice, (size_t)ngroups, true);
-    add_range(r, dalpha, nc * 4, true);
-    if (int st = check_overlaps(r)) return st;
     void* fn = m == 4 ? (fwd ? cat_fwd_for_n<4>(n, S != nullptr, std::make_integer_sequence<int, 4>{})
                              : cat_bwd_for_n<4>(n, std::make_integer_sequence<int, 4>{}))
                       : (fwd ? cat_fwd_for_n<8>(n, S != nullptr, std::make_integer_sequence<int, 8>{})

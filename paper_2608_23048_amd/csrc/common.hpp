@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "checks.hpp"
 #include "noise.hpp"
 
 namespace roi {
@@ -46,6 +47,7 @@ struct FwdBatch {
     float lambda;
     float key_c; // fl(log2(e) / lambda): the scale of the hardware-log keys
     float inv_tau;
+    float key_scale; // fl(fl(log2(e)) * inv_tau): exact keys to softmax arguments in log2 units
     float exp_span; // key-span limit of the exp-domain relaxation (relax.hpp)
     int soft; // 1: W_masked = W (.) S (pure soft forward), 0: W (.) hard mask
 };
@@ -62,27 +64,16 @@ struct BwdPiece {
     uint32_t first_block, nblocks;
 };
 
-// One AdamW step folded into constants (host, fp64, rounded once):
-// phi <- phi * decay - step_size * m' / (sqrt(v') * inv_sqrt_bc2 + eps),
-// m' = beta1 m + (1 - beta1) g, v' = beta2 v + (1 - beta2) g^2.
-struct AdamStep {
-    float decay;        // 1 - lr * weight_decay
-    float beta1, beta2;
-    float one_m_beta1, one_m_beta2;
-    float step_size;    // lr / (1 - beta1^t)
-    float inv_sqrt_bc2; // 1 / sqrt(1 - beta2^t)
-    float eps;
-};
-
 struct BwdBatch {
     uint32_t starts[kMaxPieces]; // as in FwdBatch
     BwdPiece p[kMaxPieces];
     int count;
     NoiseKey key_base; // key_base.block_hi is replaced by the piece's
-    float key_c; // fl(log2(e) / lambda)
+    float lambda;
     float inv_lambda;
     float tau;
     float inv_tau;
+    float key_scale; // fl(fl(log2(e)) * inv_tau), as in FwdBatch
     float exp_span; // key-span limit of the exp-domain relaxation (relax.hpp)
     AdamStep adam;
 };
@@ -193,6 +184,28 @@ __device__ __forceinline__ void store_f32(float* p, const float (&x)[M])
     }
 }
 
+// The backward's inputs for four consecutive elements (one group of 4, or a
+// lane's part of a wider group), as loaded: bf16 pairs stay packed.
+template <bool kAdam>
+struct BwdSlot {
+    f32x4 phi;
+    u32x2 w, g;
+    f32x4 mom, sec; // AdamW moments (fused optimizer step only)
+};
+
+// Loads the slot of elements 4 s .. 4 s + 3 of a piece.
+template <bool kAdam>
+__device__ __forceinline__ void load_bwd_slot(const BwdPiece& pc, int64_t s, BwdSlot<kAdam>& in)
+{
+    in.phi = stream_load(reinterpret_cast<const f32x4*>(pc.phi + s * 4));
+    in.w = stream_load(reinterpret_cast<const u32x2*>(pc.W + s * 4));
+    in.g = stream_load(reinterpret_cast<const u32x2*>(pc.G + s * 4));
+    if constexpr (kAdam) {
+        in.mom = stream_load(reinterpret_cast<const f32x4*>(pc.m + s * 4));
+        in.sec = stream_load(reinterpret_cast<const f32x4*>(pc.v + s * 4));
+    }
+}
+
 using FwdFn = void (*)(FwdBatch);
 using BwdFn = void (*)(BwdBatch);
 
@@ -214,5 +227,7 @@ ExportFn select_export(int m, int n);
 FwdFn select_wide_fwd(int m, int n, bool relax, int q); // q: tau_mode (roi.hip)
 FwdFn select_wide_soft_only(int m, int n, int q);
 BwdFn select_wide_bwd(int m, int n, bool adam, int q);
+// Slots (four elements each) one block of the wide backward covers.
+int64_t wide_bwd_block_slots(int m);
 
 } // namespace roi

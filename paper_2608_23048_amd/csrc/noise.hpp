@@ -97,7 +97,7 @@ constexpr double ln_atanh_series(double v)
     return s * acc;
 }
 
-struct LogCells {
+struct alignas(16) LogCells {
     float2 cell[kLogCells]; // (inv, lg)
 };
 
@@ -136,11 +136,46 @@ __device__ __forceinline__ void fill_log_table(float2* tab)
     if (i < kLogCells) tab[i] = kLogCellTable.cell[i];
 }
 
+// A wave's own copy of the cells in LDS, for kernels in which every group
+// takes the exact keys.  Lane l holds cells 2l and 2l + 1 (16 bytes): it loads
+// them with log_cells_of_lane() and stores them into the wave's 1 KiB copy
+// with publish_wave_log_table().  The wave reads only its own copy, so no
+// block barrier is needed: its LDS writes are complete (lgkmcnt 0) before any
+// of its lanes reads.  Every lane of the wave must take part.  The load is
+// issued ahead of the kernel's HBM streams so that waiting for it (a cached
+// read) does not wait for them.
+__device__ __forceinline__ float4 log_cells_of_lane()
+{
+    // The empty asm keeps the load where it is written (inside the caller's
+    // loop): hoisted out of the loop, its four registers would stay live
+    // through the whole loop body.
+    int lane = (int)(threadIdx.x & 63);
+    asm volatile("" : "+v"(lane));
+    return reinterpret_cast<const float4*>(kLogCellTable.cell)[lane];
+}
+
+__device__ __forceinline__ void publish_wave_log_table(float2* wave_tab, float4 cells)
+{
+    reinterpret_cast<float4*>(wave_tab)[threadIdx.x & 63] = cells;
+    __builtin_amdgcn_s_waitcnt(0xC07F); // lgkmcnt(0); vmcnt and expcnt not waited for
+    __builtin_amdgcn_wave_barrier();
+}
+
+// The same with one copy shared by the block's waves: each wave writes all of
+// it (the same values at the same addresses, so a wave that reads after its
+// own writes have completed sees the cells whatever the other waves do), and
+// no wave waits for another.  The copy is the block's only LDS array, so its
+// address is a constant and a lookup needs no base register.
+__device__ __forceinline__ void publish_log_table(float2* tab, float4 cells)
+{
+    publish_wave_log_table(tab, cells);
+}
+
 // ln of the float whose bit pattern is ix.
 __device__ __forceinline__ float det_log_bits(uint32_t ix, const float2* tab)
 {
     const uint32_t t = ix - kLogZBaseBits;
-    const int cell = (int)((t >> 16) & (kLogCells - 1));
+    const uint32_t cell = __builtin_amdgcn_ubfe(t, 16, 7); // bits 16..22: one bit-field extract
     const int k = (int)t >> 23;
     const float z = __uint_as_float((t & 0x007FFFFFu) + kLogZBaseBits); // = ix - (t & 0xFF800000)
     const float2 c = tab[cell];
@@ -191,12 +226,12 @@ __device__ __forceinline__ float gumbel_from_word(uint32_t x, const float2* tab)
 //   <= 6.9e-6 + 2.98e-7 |K|              (log2(e) |kappa| <= |K| + 0.54).
 // Two keys i, j whose hardware keys differ by more than
 //   kFastPairMargin + 2^-20 max(|K_i|, |K_j|) > the sum of the two errors
-// are therefore ordered the same way by kappa, and are not equal.  The
-// backward's relaxation uses these keys directly (its outputs are fp32
-// values with a tolerance, and the key error is of the order of the
-// rounding of kappa itself); the straight-through forward uses them for its
-// comparisons and recomputes the exact keys for any group in which two keys
-// are closer than the margin, so its selections are those of the exact keys.
+// are therefore ordered the same way by kappa, and are not equal.  These keys
+// serve comparisons only: the straight-through forward ranks with them and
+// recomputes the exact keys for any group in which two keys are closer than
+// the margin, so its selections are those of the exact keys.  Every
+// relaxation (the soft mask, the soft forward and every backward) runs at the
+// exact keys.
 constexpr float kFastNoiseBound = 2.5e-6f;
 constexpr float kFastPairMargin = 3.2e-5f; // > 2 (kFastNoiseBound + 4.44e-6), with slack
 

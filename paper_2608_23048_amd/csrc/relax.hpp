@@ -80,6 +80,15 @@ __device__ __forceinline__ uint32_t top4_code(const float (&k)[4])
 template <int M>
 __device__ __forceinline__ void sums_but_one(const float (&x)[M], float (&out)[M], float& total)
 {
+    if constexpr (M == 4) { // pair sums: six adds, seven with the total
+        const float pa = x[0] + x[1], pb = x[2] + x[3];
+        out[0] = x[1] + pb;
+        out[1] = x[0] + pb;
+        out[2] = pa + x[3];
+        out[3] = pa + x[2];
+        total = pa + pb;
+        return;
+    }
     float pre[M], suf[M];
     pre[0] = x[0];
 #pragma unroll
@@ -109,7 +118,7 @@ struct StepRec {
 // largest b of its own step, so the entries that compete at a step are
 // compared without the rounding of a shift by an entry already selected
 // (which would cost about ulp(span) in every exponent).
-template <int M>
+template <int M, bool kSpan = true>
 __device__ __forceinline__ float scaled_keys(const float (&kappa)[M], float key_scale, float (&b)[M],
                                              float& bmax)
 {
@@ -117,12 +126,12 @@ __device__ __forceinline__ float scaled_keys(const float (&kappa)[M], float key_
 #pragma unroll
     for (int j = 1; j < M; ++j) {
         kmax = fmaxf(kmax, kappa[j]);
-        kmin = fminf(kmin, kappa[j]);
+        if (kSpan) kmin = fminf(kmin, kappa[j]);
     }
 #pragma unroll
     for (int j = 0; j < M; ++j) b[j] = kappa[j] * key_scale;
     bmax = kmax * key_scale; // = max b (rounding is monotone)
-    return (kmax - kmin) * key_scale;
+    return kSpan ? (kmax - kmin) * key_scale : 0.0f;
 }
 
 // Relaxation (§3.2 recursion, Algorithm 1) in fp32:

@@ -27,36 +27,9 @@
 #include "roi.h"
 
 // ----------------------------------------------------------------------------- host helpers
-// (declared in host.hpp; shared by the translation units of the library)
+// (declared in host.hpp; shared by the translation units of the library; the
+// argument checks themselves are in checks.cpp)
 namespace roi {
-thread_local std::string g_last_error;
-
-int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
-int fail(int status, const char* fmt, ...)
-{
-    char buf[512];
-    va_list ap;
-    va_start(ap, fmt);
-    std::vsnprintf(buf, sizeof buf, fmt, ap);
-    va_end(ap);
-    g_last_error = buf;
-    return status;
-}
-
-int ok()
-{
-    g_last_error.clear();
-    return ROI_OK;
-}
-
-bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
-
-bool overlap(const void* a, size_t na, const void* b, size_t nb)
-{
-    if (!a || !b || na == 0 || nb == 0) return false;
-    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
-    return a0 < b0 + nb && b0 < a0 + na;
-}
 
 // Grid for `items` work items of one thread each: one block per `block` items
 // (a one-shot grid dispatched in address order keeps the set of DRAM pages in
@@ -90,52 +63,29 @@ int launch_status(const char* what)
     return ok();
 }
 
-// Outputs may overlap nothing; inputs may overlap each other.  Sorted by
-// start, a range overlaps an earlier one exactly when it starts before the
-// largest end seen so far (of any range, for an output; of the outputs, for
-// an input).
-int check_overlaps(std::vector<Range>& r)
-{
-    std::sort(r.begin(), r.end(), [](const Range& a, const Range& b) { return a.p < b.p; });
-    uintptr_t end_any = 0, end_out = 0;
-    for (const Range& x : r) {
-        if (x.out ? x.p < end_any : x.p < end_out)
-            return fail(ROI_E_INVAL, "an output overlaps another input or output");
-        end_any = std::max(end_any, x.p + x.n);
-        if (x.out) end_out = std::max(end_out, x.p + x.n);
-    }
-    return ROI_OK;
-}
-
-void add_range(std::vector<Range>& r, const void* p, size_t n, bool out)
-{
-    if (p && n) r.push_back({(uintptr_t)p, n, out});
-}
-
 } // namespace roi
 
 namespace roi {
 namespace {
 
-// Groups each lane loads ahead before computing the first, per kernel and m,
-// and the block size of the per-lane kernels (measured on the 7B-class 2:4
-// stack; one group per lane is the fastest HBM stream for the backward's
-// three inputs).
+// Groups each lane of the forward loads ahead before computing the first, per
+// m, and the block size of the per-lane kernels.
 #ifndef ROI_UNROLL_FWD_M4
 #define ROI_UNROLL_FWD_M4 2
 #endif
 #ifndef ROI_UNROLL_FWD_M8
 #define ROI_UNROLL_FWD_M8 1
 #endif
-#ifndef ROI_UNROLL_BWD
-#define ROI_UNROLL_BWD 1
-#endif
+
 #ifndef ROI_LANE_BLOCK
 #define ROI_LANE_BLOCK 256
 #endif
+#ifndef ROI_BWD_CHUNKS
+#define ROI_BWD_CHUNKS 2
+#endif
 template <int M>
 constexpr int kUnrollFwd = M == 4 ? ROI_UNROLL_FWD_M4 : ROI_UNROLL_FWD_M8;
-constexpr int kUnrollBwd = ROI_UNROLL_BWD; // groups per lane in the m = 4 backward
+constexpr int kBwdChunks = ROI_BWD_CHUNKS; // chunks per block in the m = 4 backward
 constexpr int kLaneBlock = ROI_LANE_BLOCK;
 static_assert(kLaneBlock >= kLogCells + 64 && kLaneBlock % 64 == 0, "lane block size");
 
@@ -462,7 +412,7 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
             if (kRelax) {
                 float S[M], b[M], bmax;
                 StepRec<M> unused[N]; // not written when records are not kept
-                const float span = scaled_keys<M>(kappa, kLog2e * a.inv_tau, b, bmax);
+                const float span = scaled_keys<M>(kappa, a.key_scale, b, bmax);
                 if (span <= a.exp_span)
                     relax_forward_exp<M, N, true, false, kQ>(b, bmax, a.inv_tau, S, unused);
                 else
@@ -488,24 +438,27 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
 }
 
 // Pure soft forward whose only output is W_soft = bf16(W (.) S) (neither S
-// nor the indices requested).  The relaxation runs on the hardware-log keys,
-// as in the backward: they are within the noise bound of noise.hpp of the
-// exact keys.  The host picks this kernel only up to n / (tau min(1, lambda))
-// = kSoftFastLimit, where that moves S by far less than the bf16 rounding of
-// the output.  No selection, no log cells.
+// nor the indices requested): the relaxation at the exact keys, with no
+// selection.  Each wave keeps its own copy of the log cells in LDS
+// (noise.hpp), so a block starts streaming without a barrier.
 template <int M, int N, int kQ>
 __global__ __launch_bounds__(kLaneBlock) void fwd_soft_lane_kernel(FwdBatch a)
 {
+    __shared__ float4 wave_tabs[kLaneBlock / 64][kLogCells / 2];
+    const float2* tab = reinterpret_cast<const float2*>(wave_tabs[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)]);
     const FwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
     const int64_t ng = pc.ngroups;
+    const bool lambda_one = a.lambda == 1.0f;
     constexpr int U = kUnrollFwd<M>;
     const int64_t chunk = (int64_t)kLaneBlock * U;
     for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * chunk; base < ng;
          base += (int64_t)pc.nblocks * chunk) {
         float phi[U][M];
         uint32_t w[U][M];
+        const float4 cells = log_cells_of_lane();
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kLaneBlock + threadIdx.x;
@@ -514,17 +467,21 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_soft_lane_kernel(FwdBatch a)
                 load_bf16<M>(pc.W + q * M, w[u]);
             }
         }
+        publish_wave_log_table(const_cast<float2*>(tab), cells);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t q = base + u * kLaneBlock + threadIdx.x;
             if (q >= ng) continue;
             uint32_t x[M];
             group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
-            float kappa[M]; // log2 units
-            fast_keys<M>(phi[u], x, a.key_c, kappa);
+            float kappa[M];
+            if (lambda_one)
+                exact_keys<M, true>(phi[u], x, 1.0f, tab, kappa);
+            else
+                exact_keys<M, false>(phi[u], x, a.lambda, tab, kappa);
             float S[M], b[M], bmax;
             StepRec<M> unused[N]; // not written when records are not kept
-            const float span = scaled_keys<M>(kappa, a.inv_tau, b, bmax);
+            const float span = scaled_keys<M>(kappa, a.key_scale, b, bmax);
             if (span <= a.exp_span)
                 relax_forward_exp<M, N, true, false, kQ>(b, bmax, a.inv_tau, S, unused);
             else
@@ -538,80 +495,137 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_soft_lane_kernel(FwdBatch a)
     }
 }
 
+// The backward of one group of 4 (and, with kAdam, its AdamW step), given
+// the group's noise: ng = -g, computed before its inputs arrive.  kQ: the
+// exp-domain power mode of tau (relax.hpp), or -1 where that form is off.
+template <int N, bool kLambdaOne, bool kAdam, int kQ>
+__device__ __forceinline__ void bwd_group4(const BwdBatch& a, const BwdPiece& pc,
+                                           const float (&ng)[4], const BwdSlot<kAdam>& in,
+                                           int64_t q)
+{
+    constexpr int M = 4;
+    float phi[M] = {in.phi.x, in.phi.y, in.phi.z, in.phi.w};
+    // the keys the forward sampled: kappa = fl(fl(phi / lambda) + g) (noise.hpp)
+    float kappa[M];
+#pragma unroll
+    for (int j = 0; j < M; ++j) kappa[j] = (kLambdaOne ? phi[j] : phi[j] / a.lambda) - ng[j];
+    // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
+    const uint32_t w[M] = {in.w.x & 0xFFFFu, in.w.x >> 16, in.w.y & 0xFFFFu, in.w.y >> 16};
+    const uint32_t g[M] = {in.g.x & 0xFFFFu, in.g.x >> 16, in.g.y & 0xFFFFu, in.g.y >> 16};
+    float sbar[M];
+#pragma unroll
+    for (int j = 0; j < M; ++j) sbar[j] = bf16_bits_to_float(g[j]) * bf16_bits_to_float(w[j]);
+    // Relaxation forward keeping its records, then the reverse sweep: the
+    // exp-domain recursion where the group's key span allows it (the floor of
+    // log(1 - mu) is then out of reach), else the log-domain one with the
+    // floor's case in the sweep (relax.hpp).
+    StepRec<M> rec[N];
+    float S_unused[M], b[M], abar[M], bmax;
+    if constexpr (kQ < 0) { // the exp-domain form is off at this temperature
+        scaled_keys<M, false>(kappa, a.key_scale, b, bmax);
+        relax_forward<M, N, false, true>(b, bmax, a.inv_tau, S_unused, rec);
+        relax_backward<M, N, false, true>(rec, sbar, a.inv_tau, abar);
+    } else if (scaled_keys<M>(kappa, a.key_scale, b, bmax) <= a.exp_span) {
+        relax_forward_exp<M, N, false, true, kQ>(b, bmax, a.inv_tau, S_unused, rec);
+        relax_backward<M, N, kQ == 1, false>(rec, sbar, a.inv_tau, abar);
+    } else {
+        relax_forward<M, N, false, true>(b, bmax, a.inv_tau, S_unused, rec);
+        relax_backward<M, N, false, true>(rec, sbar, a.inv_tau, abar);
+    }
+    float grad[M]; // dL/dphi = dL/dkappa / lambda
+#pragma unroll
+    for (int j = 0; j < M; ++j) grad[j] = kLambdaOne ? abar[j] : abar[j] * a.inv_lambda;
+    if (!kAdam || pc.dphi) store_f32<M>(pc.dphi + q * M, grad);
+    if constexpr (kAdam) {
+        float mom[M] = {in.mom.x, in.mom.y, in.mom.z, in.mom.w};
+        float sec[M] = {in.sec.x, in.sec.y, in.sec.z, in.sec.w};
+#pragma unroll
+        for (int j = 0; j < M; ++j) adamw_update(a.adam, grad[j], phi[j], mom[j], sec[j]);
+        store_f32<M>(const_cast<float*>(pc.phi) + q * M, phi);
+        store_f32<M>(pc.m + q * M, mom);
+        store_f32<M>(pc.v + q * M, sec);
+    }
+}
+
+// The noise of a lane's group (ng = -g for its four elements, noise.hpp).
+__device__ __forceinline__ void group_noise4(uint32_t block, const NoiseKey& key, const float2* tab,
+                                             float (&ng)[4])
+{
+    uint32_t x[4];
+    group_words<4>(block, key, x);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ng[j] = neg_gumbel_from_word(x[j], tab);
+}
+
+// kBwdChunks chunks of kLaneBlock groups from `base`, one group per lane and
+// chunk.  The loads go out first (the group's inputs, the log cells, and with
+// more than one chunk the next chunk's inputs); the noise -- the Philox words
+// and both logarithms of every element, about half of the arithmetic --
+// needs none of them, so each chunk's noise runs while loads are in flight.
+// kFull: every group of the span is inside the piece, so there is no
+// per-lane condition and each wait for a load is exactly for that load (a
+// condition around a load makes the compiler wait for every load at the
+// join).
+template <int N, bool kLambdaOne, bool kAdam, int kQ, bool kFull>
+__device__ __forceinline__ void bwd_lane_span(const BwdBatch& a, const BwdPiece& pc,
+                                              const NoiseKey& key, float2* tab, int64_t base,
+                                              int64_t ng_total)
+{
+    constexpr int K = kBwdChunks;
+    const int64_t q0 = base + threadIdx.x;
+    BwdSlot<kAdam> in[2];
+    if (kFull || q0 < ng_total) load_bwd_slot<kAdam>(pc, q0, in[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    const float4 cells = log_cells_of_lane();
+    __builtin_amdgcn_sched_barrier(0);
+    if (K > 1 && (kFull || q0 + kLaneBlock < ng_total))
+        load_bwd_slot<kAdam>(pc, q0 + kLaneBlock, in[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    float ng[2][4];
+    {
+        uint32_t x[4];
+        group_words<4>(pc.block0 + (uint32_t)q0, key, x);
+        publish_log_table(tab, cells);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) ng[0][j] = neg_gumbel_from_word(x[j], tab);
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int64_t q = q0 + (int64_t)k * kLaneBlock;
+        if (k + 1 < K) group_noise4(pc.block0 + (uint32_t)(q + kLaneBlock), key, tab, ng[(k + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (kFull || q < ng_total)
+            bwd_group4<N, kLambdaOne, kAdam, kQ>(a, pc, ng[k & 1], in[k & 1], q);
+        if (k + 2 < K && (kFull || q + 2 * kLaneBlock < ng_total))
+            load_bwd_slot<kAdam>(pc, q + 2 * kLaneBlock, in[k & 1]);
+    }
+}
+
 // Backward for m = 4 (m = 8 and wider take the kernels of wide_bwd.hip);
 // with kAdam the AdamW step on the logits is fused in: the moments are read
 // with the group's other inputs, and the updated logits and moments are
 // written instead of (or besides, when pc.dphi is set) the gradient.  kQ as
-// in fwd_lane_kernel.
+// in fwd_lane_kernel.  A block takes kBwdChunks consecutive chunks of
+// kLaneBlock groups.
 template <int M, int N, bool kLambdaOne, bool kAdam, int kQ>
 __global__ __launch_bounds__(kLaneBlock) void bwd_lane_kernel(BwdBatch a)
 {
     static_assert(M == 4, "the lane backward serves m = 4");
+    // Every group takes the exact keys; the block's waves share one copy of
+    // the log cells in LDS (noise.hpp).
+    __shared__ float4 tab4[kLogCells / 2];
+    float2* tab = reinterpret_cast<float2*>(tab4);
     const BwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
     const int64_t ng = pc.ngroups;
-    constexpr int U = kUnrollBwd;
-    const int64_t chunk = (int64_t)kLaneBlock * U;
-    for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * chunk; base < ng;
-         base += (int64_t)pc.nblocks * chunk) {
-        float phi[U][M];
-        uint32_t w[U][M], g[U][M];
-        float mom[kAdam ? U : 1][kAdam ? M : 1], sec[kAdam ? U : 1][kAdam ? M : 1];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q < ng) {
-                load_logits<M>(pc.phi + q * M, phi[u]);
-                load_bf16<M>(pc.W + q * M, w[u]);
-                load_bf16<M>(pc.G + q * M, g[u]);
-                if constexpr (kAdam) {
-                    load_logits<M>(pc.m + q * M, mom[u]);
-                    load_logits<M>(pc.v + q * M, sec[u]);
-                }
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q >= ng) continue;
-            // keys from the hardware logarithm, in log2 units (noise.hpp)
-            uint32_t x[M];
-            group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
-            float kappa[M];
-            fast_keys<M>(phi[u], x, kLambdaOne ? kLog2e : a.key_c, kappa);
-            // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32 (bf16 x bf16).
-            float sbar[M];
-#pragma unroll
-            for (int j = 0; j < M; ++j)
-                sbar[j] = bf16_bits_to_float(g[u][j]) * bf16_bits_to_float(w[u][j]);
-            // Relaxation forward keeping its records, then the reverse sweep:
-            // the exp-domain recursion where the group's key span allows it
-            // (the floor of log(1 - mu) is then out of reach), else the
-            // log-domain one with the floor's case in the sweep (relax.hpp).
-            StepRec<M> rec[N];
-            float S_unused[M], b[M], abar[M], bmax;
-            const float span = scaled_keys<M>(kappa, a.inv_tau, b, bmax);
-            if (span <= a.exp_span) {
-                relax_forward_exp<M, N, false, true, kQ>(b, bmax, a.inv_tau, S_unused, rec);
-                relax_backward<M, N, kQ == 1, false>(rec, sbar, a.inv_tau, abar);
-            } else {
-                relax_forward<M, N, false, true>(b, bmax, a.inv_tau, S_unused, rec);
-                relax_backward<M, N, false, true>(rec, sbar, a.inv_tau, abar);
-            }
-            float grad[M]; // dL/dphi = dL/dkappa / lambda
-#pragma unroll
-            for (int j = 0; j < M; ++j) grad[j] = kLambdaOne ? abar[j] : abar[j] * a.inv_lambda;
-            if (!kAdam || pc.dphi) store_f32<M>(pc.dphi + q * M, grad);
-            if constexpr (kAdam) {
-#pragma unroll
-                for (int j = 0; j < M; ++j)
-                    adamw_update(a.adam, grad[j], phi[u][j], mom[u][j], sec[u][j]);
-                store_f32<M>(const_cast<float*>(pc.phi) + q * M, phi[u]);
-                store_f32<M>(pc.m + q * M, mom[u]);
-                store_f32<M>(pc.v + q * M, sec[u]);
-            }
-        }
+    const int64_t span = (int64_t)kLaneBlock * kBwdChunks;
+    for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * span; base < ng;
+         base += (int64_t)pc.nblocks * span) {
+        if (base + span <= ng)
+            bwd_lane_span<N, kLambdaOne, kAdam, kQ, true>(a, pc, key, tab, base, ng);
+        else
+            bwd_lane_span<N, kLambdaOne, kAdam, kQ, false>(a, pc, key, tab, base, ng);
     }
 }
 
@@ -658,66 +672,21 @@ __global__ __launch_bounds__(kBlock) void gumbel_words_kernel(const uint32_t* wo
 }
 
 // ----------------------------------------------------------------------------- host side
-struct Shape {
-    int64_t numel = 0;
-    int64_t ngroups = 0;
-};
-
-int check_shape(int64_t rows, int64_t cols, int n, int m, float tau, float lambda,
-                uint64_t elem_offset, Shape* sh)
-{
-    if (rows < 0 || cols < 0) return fail(ROI_E_INVAL, "rows (%lld) and cols (%lld) must be >= 0",
-                                          (long long)rows, (long long)cols);
-    if (m < 1 || n < 1 || n > m)
-        return fail(ROI_E_INVAL, "pattern n:m = %d:%d needs 1 <= n <= m", n, m);
-    if (m != 4 && m != 8 && m != 16 && m != 32)
-        return fail(ROI_E_UNSUPPORTED, "m = %d is not built (supported: 4, 8, 16, 32)", m);
-    if (cols % m != 0) return fail(ROI_E_INVAL, "cols (%lld) must be a multiple of m (%d)",
-                                   (long long)cols, m);
-    if (rows > 0 && cols > ((int64_t)1 << 62) / rows)
-        return fail(ROI_E_INVAL, "rows * cols must be below 2^62");
-    if (!(tau > 0.0f) || !std::isfinite(tau))
-        return fail(ROI_E_INVAL, "tau must be finite and > 0");
-    if (!(lambda > 0.0f) || !std::isfinite(lambda))
-        return fail(ROI_E_INVAL, "lambda must be finite and > 0");
-    if (elem_offset % (uint64_t)m != 0)
-        return fail(ROI_E_INVAL, "elem_offset (%llu) must be a multiple of m (%d)",
-                    (unsigned long long)elem_offset, m);
-    const int64_t numel = rows * cols;
-    if (elem_offset > UINT64_MAX - (uint64_t)numel)
-        return fail(ROI_E_INVAL, "elem_offset + rows * cols overflows 64 bits");
-    sh->numel = numel;
-    sh->ngroups = numel / m;
-    return ROI_OK;
-}
-
-// Calls launch(first, count, elem0) for consecutive pieces of [0, items) --
-// items of `per_item` elements starting at global element elem_offset -- so
-// that within a piece every Philox block index (element / 4) has the same high
-// 32 bits.  Pieces end at multiples of 2^34 elements, which per_item divides.
-template <typename F>
-int for_each_piece(uint64_t elem_offset, int64_t items, int64_t per_item, F&& launch)
-{
-    int64_t done = 0;
-    while (done < items) {
-        const uint64_t e0 = elem_offset + (uint64_t)done * (uint64_t)per_item;
-        const uint64_t boundary = ((e0 >> 34) + 1) << 34;
-        const uint64_t fit = (boundary - e0) / (uint64_t)per_item;
-        const int64_t left = items - done;
-        const int64_t count = fit < (uint64_t)left ? (int64_t)fit : left;
-        if (int st = launch(done, count, e0)) return st;
-        done += count;
-    }
-    return ROI_OK;
-}
-
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // ---- dispatch tables over (m, n) and the boolean variants
 
 // How the exp-domain recursion raises omega to 1 / tau: 1 or 2 when 1 / tau
 // is that integer (by multiplication), else 0 (exp2 and log2).
-int tau_mode(float tau) { return tau == 1.0f ? 1 : (tau == 0.5f ? 2 : 0); }
+// -1 where the exp-domain form is off (q = 1 / tau above 2.25, see
+// exp_span_limit): the backward then has a log-domain-only variant.  The
+// forwards treat -1 as 0 (their exp-domain branch is never taken there).
+int tau_mode(float tau)
+{
+    if (tau == 1.0f) return 1;
+    if (tau == 0.5f) return 2;
+    return 1.0 / (double)tau > 2.25 ? -1 : 0;
+}
 
 // Largest key span (units of b, relax.hpp) for which a group may take the
 // exp-domain recursion: kExpSpanAccuracy, and kExpNormalBound - log2 m -
@@ -761,6 +730,7 @@ FwdFn pick_fwd(bool want_s, bool want_idx, bool lam1, int q)
 template <int M, int N, bool L, bool A>
 BwdFn pick_bwd_q(int q)
 {
+    if (q < 0) return bwd_lane_kernel<M, N, L, A, -1>;
     return q == 1 ? bwd_lane_kernel<M, N, L, A, 1>
                   : (q == 2 ? bwd_lane_kernel<M, N, L, A, 2> : bwd_lane_kernel<M, N, L, A, 0>);
 }
@@ -803,13 +773,10 @@ FwdFn soft_for_n(int n, int q, std::integer_sequence<int, Ns...>)
     return f;
 }
 
-// The soft forward with no output but W_soft (hardware-log keys), and the
-// largest n / (tau min(1, lambda)) it serves.
-constexpr double kSoftFastLimit = 160.0;
-
+// The soft forward with no output but W_soft.
 FwdFn select_soft_only(int m, int n, float tau)
 {
-    const int q = tau_mode(tau);
+    const int q = std::max(0, tau_mode(tau));
     if (m == 4) return soft_for_n<4>(n, q, std::make_integer_sequence<int, 4>{});
     if (m == 8) return soft_for_n<8>(n, q, std::make_integer_sequence<int, 8>{});
     return select_wide_soft_only(m, n, q);
@@ -817,7 +784,7 @@ FwdFn select_soft_only(int m, int n, float tau)
 
 FwdFn select_fwd(int m, int n, bool s, bool i, bool l, float tau)
 {
-    const int q = tau_mode(tau);
+    const int q = std::max(0, tau_mode(tau));
     if (m == 4) return fwd_for_n<4>(n, s, i, l, q, std::make_integer_sequence<int, 4>{});
     if (m == 8) return fwd_for_n<8>(n, s, i, l, q, std::make_integer_sequence<int, 8>{});
     return select_wide_fwd(m, n, s, q);
@@ -841,8 +808,9 @@ namespace {
 // Blocks one piece of `ngroups` groups needs in a launch.
 int64_t blocks_for(int64_t ngroups, int m, bool fwd)
 {
-    if (m > 8 || (m == 8 && !fwd)) return ceil_div(ngroups * (m / 4), kBlock); // wide kernels
-    const int u = fwd ? (m == 4 ? kUnrollFwd<4> : kUnrollFwd<8>) : kUnrollBwd;
+    if (m > 8 || (m == 8 && !fwd)) // wide kernels: m / 4 slots per group
+        return ceil_div(ngroups * (m / 4), fwd ? (int64_t)kBlock : wide_bwd_block_slots(m));
+    const int u = fwd ? (m == 4 ? kUnrollFwd<4> : kUnrollFwd<8>) : kBwdChunks;
     return ceil_div(ngroups, (int64_t)u * kLaneBlock);
 }
 
@@ -890,67 +858,15 @@ struct Launcher {
     }
 };
 
-int check_common(int n, int m, float tau, float lambda)
-{
-    if (m < 1 || n < 1 || n > m)
-        return fail(ROI_E_INVAL, "pattern n:m = %d:%d needs 1 <= n <= m", n, m);
-    if (m != 4 && m != 8 && m != 16 && m != 32)
-        return fail(ROI_E_UNSUPPORTED, "m = %d is not built (supported: 4, 8, 16, 32)", m);
-    if (!(tau > 0.0f) || !std::isfinite(tau))
-        return fail(ROI_E_INVAL, "tau must be finite and > 0");
-    if (!(lambda > 0.0f) || !std::isfinite(lambda))
-        return fail(ROI_E_INVAL, "lambda must be finite and > 0");
-    return ROI_OK;
-}
-
-int check_count(const void* t, int count)
-{
-    if (count < 0) return fail(ROI_E_INVAL, "count must be >= 0");
-    if (count > 0 && !t) return fail(ROI_E_INVAL, "tensors must not be NULL");
-    return ROI_OK;
-}
-
 int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count, int n, int m,
                  float tau, float lambda, uint64_t seed, uint64_t step, hipStream_t stream)
 {
-    if (int st = check_common(n, m, tau, lambda)) return st;
-    if (int st = check_count(t, count)) return st;
-    std::vector<Range> ranges;
-    int with_s = -1, with_idx = -1; // -1: no nonempty tensor seen yet
-    for (int i = 0; i < count; ++i) {
-        Shape sh;
-        if (int st = check_shape(t[i].rows, t[i].cols, n, m, tau, lambda, t[i].elem_offset, &sh))
-            return count > 1 ? fail(st, "tensor %d: %s", i, g_last_error.c_str()) : st;
-        if (sh.numel == 0) continue;
-        if (!t[i].W || !t[i].logits || !t[i].W_masked)
-            return fail(ROI_E_INVAL, "tensor %d: W, logits and W_masked must not be NULL", i);
-        if (!aligned16(t[i].W) || !aligned16(t[i].logits) || !aligned16(t[i].W_masked) ||
-            (t[i].soft_mask && !aligned16(t[i].soft_mask)) ||
-            (t[i].sel_idx && !aligned16(t[i].sel_idx)))
-            return fail(ROI_E_INVAL, "tensor %d: device pointers must be 16-byte aligned", i);
-        const int s_i = t[i].soft_mask != nullptr, x_i = t[i].sel_idx != nullptr;
-        if ((with_s >= 0 && s_i != with_s) || (with_idx >= 0 && x_i != with_idx))
-            return fail(ROI_E_INVAL,
-                        "soft_mask and sel_idx must each be given for every tensor or for none");
-        with_s = s_i;
-        with_idx = x_i;
-        const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
-        add_range(ranges, t[i].W, nb2, false);
-        add_range(ranges, t[i].logits, nb4, false);
-        add_range(ranges, t[i].W_masked, nb2, true);
-        add_range(ranges, t[i].soft_mask, nb4, true);
-        add_range(ranges, t[i].sel_idx, (size_t)sh.ngroups * (size_t)n, true);
-    }
+    int with_s, with_idx;
+    if (int st = validate_fwd(t, count, n, m, tau, lambda, &with_s, &with_idx)) return st;
     if (with_s < 0) return ok(); // nothing to do
-    if (int st = check_overlaps(ranges)) return st;
-    // The soft forward alone runs on the hardware-log keys where the effect of
-    // their error on S stays in the range its parity tests cover: n / tau up
-    // to kSoftFastLimit, with the keys' magnitude growing as 1 / lambda below
-    // lambda = 1.  Elsewhere it takes the exact keys.
-    const bool soft_fast = soft && with_s == 0 && with_idx == 0 &&
-                           (double)n / ((double)tau * std::min(1.0, (double)lambda)) <=
-                               kSoftFastLimit;
-    FwdFn fn = soft_fast
+    // The soft forward alone needs no selection: a kernel of its own.
+    const bool soft_only = soft && with_s == 0 && with_idx == 0;
+    FwdFn fn = soft_only
                    ? select_soft_only(m, n, tau)
                    : select_fwd(m, n, soft || with_s == 1, with_idx == 1, lambda == 1.0f, tau);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
@@ -965,6 +881,7 @@ int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count
     L.batch.lambda = lambda;
     L.batch.key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
     L.batch.inv_tau = (float)(1.0 / (double)tau);
+    L.batch.key_scale = kLog2e * L.batch.inv_tau;
     L.batch.exp_span = exp_span_limit(n, m, tau);
     L.batch.soft = soft ? 1 : 0;
     for (int i = 0; i < count; ++i) {
@@ -988,84 +905,15 @@ int mask_fwd_run(const char* what, bool soft, const roi_fwd_tensor* t, int count
     return L.flush();
 }
 
-// One tensor of a backward call; phi is overwritten with the updated logits
-// when the AdamW step is fused (m and v set).
-struct BwdDesc {
-    const uint16_t* G;
-    const uint16_t* W;
-    const float* phi;
-    float* dphi;
-    float* m;
-    float* v;
-    int64_t rows, cols;
-    uint64_t off;
-};
-
-int check_adamw(const roi_adamw_params* o, AdamStep* st)
-{
-    if (!o) return fail(ROI_E_INVAL, "the AdamW parameters must not be NULL");
-    if (!(o->lr >= 0.0f) || !std::isfinite(o->lr))
-        return fail(ROI_E_INVAL, "AdamW lr must be finite and >= 0");
-    if (!(o->beta1 >= 0.0f && o->beta1 < 1.0f) || !(o->beta2 >= 0.0f && o->beta2 < 1.0f))
-        return fail(ROI_E_INVAL, "AdamW betas must lie in [0, 1)");
-    if (!(o->eps > 0.0f) || !std::isfinite(o->eps))
-        return fail(ROI_E_INVAL, "AdamW eps must be finite and > 0");
-    if (!(o->weight_decay >= 0.0f) || !std::isfinite(o->weight_decay))
-        return fail(ROI_E_INVAL, "AdamW weight_decay must be finite and >= 0");
-    if (o->t < 1) return fail(ROI_E_INVAL, "AdamW step count t must be >= 1");
-    const double lr = o->lr, b1 = o->beta1, b2 = o->beta2;
-    const double bc1 = 1.0 - std::pow(b1, (double)o->t);
-    const double bc2 = 1.0 - std::pow(b2, (double)o->t);
-    st->decay = (float)(1.0 - lr * (double)o->weight_decay);
-    st->beta1 = o->beta1;
-    st->beta2 = o->beta2;
-    st->one_m_beta1 = (float)(1.0 - b1);
-    st->one_m_beta2 = (float)(1.0 - b2);
-    st->step_size = (float)(lr / bc1);
-    st->inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
-    st->eps = o->eps;
-    return ROI_OK;
-}
-
 int mask_bwd_core(const char* what, const BwdDesc* t, int count, int n, int m, float tau,
                   float lambda, uint64_t seed, uint64_t step, const roi_adamw_params* opt,
                   hipStream_t stream)
 {
-    if (int st = check_common(n, m, tau, lambda)) return st;
     const bool adam = opt != nullptr;
     AdamStep astep{};
-    if (adam)
-        if (int st = check_adamw(opt, &astep)) return st;
-    std::vector<Range> ranges;
-    bool any = false;
-    for (int i = 0; i < count; ++i) {
-        Shape sh;
-        if (int st = check_shape(t[i].rows, t[i].cols, n, m, tau, lambda, t[i].off, &sh))
-            return count > 1 ? fail(st, "tensor %d: %s", i, g_last_error.c_str()) : st;
-        if (sh.numel == 0) continue;
-        if (!t[i].G || !t[i].W || !t[i].phi || (!adam && !t[i].dphi) ||
-            (adam && (!t[i].m || !t[i].v)))
-            return fail(ROI_E_INVAL, adam ? "tensor %d: grad_W_masked, W, logits, exp_avg and "
-                                            "exp_avg_sq must not be NULL"
-                                          : "tensor %d: grad_W_masked, W, logits and grad_logits "
-                                            "must not be NULL", i);
-        if (!aligned16(t[i].G) || !aligned16(t[i].W) || !aligned16(t[i].phi) ||
-            (t[i].dphi && !aligned16(t[i].dphi)) || (t[i].m && !aligned16(t[i].m)) ||
-            (t[i].v && !aligned16(t[i].v)))
-            return fail(ROI_E_INVAL, "tensor %d: device pointers must be 16-byte aligned", i);
-        const size_t nb2 = (size_t)sh.numel * 2, nb4 = (size_t)sh.numel * 4;
-        add_range(ranges, t[i].G, nb2, false);
-        add_range(ranges, t[i].W, nb2, false);
-        add_range(ranges, t[i].phi, nb4, adam); // updated in place by the AdamW step
-        add_range(ranges, t[i].dphi, nb4, true);
-        if (adam) {
-            add_range(ranges, t[i].m, nb4, true);
-            add_range(ranges, t[i].v, nb4, true);
-        }
-        any = true;
-    }
+    bool any;
+    if (int st = validate_bwd(t, count, n, m, tau, lambda, opt, &astep, &any)) return st;
     if (!any) return ok();
-    if (int st = check_overlaps(ranges)) return st;
     BwdFn fn = select_bwd(m, n, lambda == 1.0f, adam, tau);
     if (!fn) return fail(ROI_E_UNSUPPORTED, "no kernel for %d:%d", n, m);
     Launcher<BwdBatch, BwdPiece, BwdFn> L{};
@@ -1076,10 +924,11 @@ int mask_bwd_core(const char* what, const BwdDesc* t, int count, int n, int m, f
     L.stream = stream;
     L.what = what;
     L.batch.key_base = make_key(seed, step, 0);
-    L.batch.key_c = (float)(1.4426950408889634 / (double)lambda); // log2(e) / lambda
+    L.batch.lambda = lambda;
     L.batch.inv_lambda = (float)(1.0 / (double)lambda);
     L.batch.tau = tau;
     L.batch.inv_tau = (float)(1.0 / (double)tau);
+    L.batch.key_scale = kLog2e * L.batch.inv_tau;
     L.batch.exp_span = exp_span_limit(n, m, tau);
     L.batch.adam = astep;
     for (int i = 0; i < count; ++i) {

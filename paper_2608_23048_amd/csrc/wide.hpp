@@ -205,8 +205,9 @@ __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], floa
         b[e] = kappa[e] * c;
         S[e] = 0.0f;
     }
-    const float span = (kmax - group_min<L>(min4(kappa))) * c;
-    if (span <= exp_span) { // the same on all lanes of the group
+    // kQ < 0: the exp-domain form is off at this temperature (no span needed)
+    const float span = kQ < 0 ? 0.0f : (kmax - group_min<L>(min4(kappa))) * c;
+    if (kQ >= 0 && span <= exp_span) { // the same on all lanes of the group
         float ex[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) ex[e] = __builtin_amdgcn_exp2f(b[e] - bmax0);
@@ -226,7 +227,7 @@ __device__ __forceinline__ bool wide_relax_forward(const float (&kappa)[4], floa
                     rec[k].mu[e] = mu;
                     rec[k].om[e] = om;
                 }
-                if (k + 1 < N) ex[e] = mu * pow_q<kQ>(om, inv_tau);
+                if (k + 1 < N) ex[e] = mu * pow_q<kQ < 0 ? 0 : kQ>(om, inv_tau);
             }
         }
         return true;

@@ -81,7 +81,7 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
         if constexpr (kRelax) {
             float S[4];
             StepRec<4> unused[N]; // not written when records are not kept
-            wide_relax_forward<L, N, false, kQ>(kappa, kLog2e * a.inv_tau, a.inv_tau, a.exp_span,
+            wide_relax_forward<L, N, false, kQ>(kappa, a.key_scale, a.inv_tau, a.exp_span,
                                                 true, S, unused);
             if (pc.S) {
                 const f32x4 sv = {S[0], S[1], S[2], S[3]};
@@ -99,29 +99,42 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
     }
 }
 
-// Pure soft forward whose only output is bf16(W (.) S): the relaxation on the
-// hardware-log keys, no selection (as fwd_soft_lane_kernel in roi.hip, and
-// under the same limit on n / (tau min(1, lambda))).
+// Pure soft forward whose only output is bf16(W (.) S): the relaxation at the
+// exact keys, no selection; each wave keeps its own copy of the log cells in
+// LDS (noise.hpp), as in fwd_soft_lane_kernel of roi.hip.
 template <int M, int N, int kQ>
 __global__ __launch_bounds__(kBlock) void fwd_soft_wide_kernel(FwdBatch a)
 {
     constexpr int L = M / 4;
+    __shared__ float4 wave_tabs[kBlock / 64][kLogCells / 2];
+    const float2* tab = reinterpret_cast<const float2*>(wave_tabs[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)]);
     const FwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
     const int64_t nslots = pc.ngroups * L;
     const int64_t stride = (int64_t)pc.nblocks * kBlock;
-    for (int64_t slot = (int64_t)(blockIdx.x - pc.first_block) * kBlock + threadIdx.x;
-         slot < nslots; slot += stride) {
-        const f32x4 pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
-        const u32x2 wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
-        const uint4 x = philox_block(pc.block0 + (uint32_t)slot, key);
-        const float kappa[4] = {fast_key_log2(pv.x, a.key_c, x.x), fast_key_log2(pv.y, a.key_c, x.y),
-                                fast_key_log2(pv.z, a.key_c, x.z), fast_key_log2(pv.w, a.key_c, x.w)};
+    for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * kBlock; base < nslots;
+         base += stride) {
+        const int64_t slot = base + threadIdx.x;
+        // a group's lanes are all live or all past the end (groups are whole in a wave)
+        const bool live = slot < nslots;
+        const float4 cells = log_cells_of_lane();
+        __builtin_amdgcn_sched_barrier(0);
+        f32x4 pv{};
+        u32x2 wv{};
+        if (live) {
+            pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
+            wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
+        }
+        publish_wave_log_table(const_cast<float2*>(tab), cells);
+        if (!live) continue;
+        const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
+        float kappa[4];
+        wide_keys(phi, pc.block0 + (uint32_t)slot, key, a.lambda, tab, kappa);
         float S[4];
         StepRec<4> unused[N]; // not written when records are not kept
-        wide_relax_forward<L, N, false, kQ>(kappa, a.inv_tau, a.inv_tau, a.exp_span, true, S,
-                                            unused);
+        wide_relax_forward<L, N, false, kQ>(kappa, a.key_scale, a.inv_tau, a.exp_span,
+                                            true, S, unused);
         const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
         const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
         const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);

@@ -6,8 +6,9 @@ bit-exact; the soft mask and grad_logits must be within 1e-5 relative /
 The straight-through forward decides with keys from the hardware logarithm
 and falls back to the exact keys where two keys are within its error margin;
 its selections are compared bit for bit, with and without the soft mask, and
-on inputs built so that keys tie or nearly tie.  The backward evaluates the
-relaxation at the hardware keys; its bound is pinned exhaustively here."""
+on inputs built so that keys tie or nearly tie (the margin's bound on the
+hardware noise is pinned exhaustively here).  Every relaxation -- the soft
+mask, the soft forward and every backward -- runs at the exact keys."""
 from __future__ import annotations
 
 import numpy as np
@@ -17,8 +18,7 @@ import oracle
 import paper_2608_23048_amd as roi
 from paper_2608_23048_amd import workloads as wl
 from tests.gpu_helpers import (HW_NOISE_A, HW_NOISE_B, HW_NOISE_MAX, LOG2_LN2, LOG2E,
-                               assert_close, backward_key_error, bf16_bits, f32, key_error_floor,
-                               say)
+                               assert_close, bf16_bits, f32, fp32_key_floor, sbar_of, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -57,22 +57,25 @@ def run_case(dev, rows, cols, n, m, tau, lam, seed, step, off, case_seed, w_std=
     assert np.array_equal(bf16_bits(Wm2).reshape(-1), Wm_o), "masked weights differ (no soft mask)"
     assert np.array_equal(bf16_bits(Wm3).reshape(-1), Wm_o), "masked weights differ (no indices)"
     rs = assert_close(f32(S), S_o, "soft mask")
-    floor = None
-    if scale_aware:
-        # unit-scale gradients at small tau are ill-conditioned in the keys:
-        # allow 4x the gradient's first-order change when every key moves by
-        # the error bound of the backward's keys
-        phi = f32(L).reshape(-1)
-        kappa = oracle.keys(phi, lam32, seed, step, off)
-        g = oracle.keys(np.zeros_like(phi), 1.0, seed, step, off)
-        a = (phi / np.float32(lam32)).astype(np.float32)
-        delta = backward_key_error(kappa, g, a)
-        sbar = (bf16_bits(G).astype(np.uint32) << 16).view(np.float32).astype(np.float64) * \
-               (bf16_bits(W).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-        floor = key_error_floor(oracle, kappa.reshape(-1, m), delta.reshape(-1, m),
-                                sbar.reshape(-1, m), n, tau32, lam32)
-    rd = assert_close(f32(d), d_o, "grad_logits", scale_aware=scale_aware, floor=floor)
-    say(f"  ok: soft-mask err/bound {rs:.3f}, grad err/bound {rd:.3f}")
+    check_grad(d, d_o, L, G, W, n, m, tau32, lam32, seed, step, off, scale_aware)
+    say(f"  ok: soft-mask err/bound {rs:.3f}")
+
+
+def check_grad(d, d_o, L, G, W, n, m, tau32, lam32, seed, step, off, scale_aware):
+    """grad_logits against the oracle.  At config scale: the plain bar
+    (1e-6 absolute + 1e-5 relative).  In every case also the relative bar:
+    1e-5 relative with the absolute term scaled to 1e-6 max|oracle|, plus
+    the fp32 rounding allowance of the keys (gpu_helpers)."""
+    got = f32(d).reshape(-1)
+    if not scale_aware:
+        assert_close(got, d_o, "grad_logits")
+    kappa = oracle.keys(f32(L).reshape(-1), lam32, seed, step, off).reshape(-1, m)
+    sbar = sbar_of(bf16_bits(G), bf16_bits(W)).reshape(-1, m)
+    floor = fp32_key_floor(oracle, kappa, sbar, n, tau32, lam32)
+    r = assert_close(got, d_o, "grad_logits (relative)", scale_aware=True, floor=floor)
+    plain = np.abs(got - d_o) <= 1e-6 * np.abs(d_o).max() + 1e-5 * np.abs(d_o)
+    say(f"  grad: err/bound {r:.3f}, {np.count_nonzero(~plain)}/{plain.size} elements "
+        f"need the fp32 allowance")
 
 
 # --------------------------------------------------------------------------- noise
@@ -153,9 +156,7 @@ def test_small_config_scale(dev, case):
 def test_small_unit_scale(dev, case):
     """Unit-scale W and upstream gradients (grad_logits of order 1/tau): the
     absolute 1e-6 term is scaled by the largest |oracle| value, and each
-    element also gets 4x its conditioning floor (the oracle gradient's
-    first-order change when each key moves by the error bound of the
-    backward's hardware-log keys)."""
+    element also gets the fp32 rounding allowance of its keys."""
     rows, cols, n, m, tau, lam, seed, step, off = case
     run_case(dev, rows, cols, n, m, tau, lam, seed, step, off, case_seed=7 + rows * cols,
              w_std=1.0, grad_std=1.0, logit_std=2.0, scale_aware=True)
@@ -428,17 +429,58 @@ def adamw_state(rows, cols, seed):
     return m, v
 
 
+def adamw_rounding_check(got_p, got_m, got_v, g, phi0, m0, v0, hp, t, what):
+    """The fused step's moments and logits against the oracle's AdamW applied
+    to the kernel's own fp32 gradient g, so that only the step's fp32
+    arithmetic is measured: each moment within a few units of rounding of its
+    two terms (fp32 products and a fused multiply-add), and the logit within
+    2 ulp plus 2e-6 of the update (approximate reciprocal and square root)."""
+    lr, b1, b2, eps, wd = hp
+    g = np.asarray(g, dtype=np.float64).reshape(-1)
+    m0 = np.asarray(m0, dtype=np.float64).reshape(-1)
+    v0 = np.asarray(v0, dtype=np.float64).reshape(-1)
+    p_r, m_r, v_r = oracle.adamw(g, phi0, m0.astype(np.float32), v0.astype(np.float32), *hp, t)
+    u = 2.0 ** -24
+    tol_m = 4 * u * (b1 * np.abs(m0) + (1 - b1) * np.abs(g)) + 2 * u * np.abs(m_r)
+    tol_v = 4 * u * (b2 * np.abs(v0) + (1 - b2) * g * g) + 2 * u * np.abs(v_r)
+    for got, ref, tol, name in ((got_m, m_r, tol_m, "exp_avg"), (got_v, v_r, tol_v, "exp_avg_sq")):
+        err = np.abs(np.asarray(got, dtype=np.float64).reshape(-1) - ref.reshape(-1))
+        assert np.all(err <= tol), f"{what}: {name} off by {float((err - tol).max()):.3g}"
+    decayed = np.asarray(phi0, dtype=np.float64).reshape(-1) * (1.0 - lr * wd)
+    upd = p_r.reshape(-1) - decayed
+    gp = np.asarray(got_p, dtype=np.float64).reshape(-1)
+    # the moments' own rounding carried into the update -s m' / (sqrt(v' / bc2) + eps)
+    step_size = lr / (1.0 - b1 ** t)
+    den = np.sqrt(v_r.reshape(-1) / (1.0 - b2 ** t)) + eps
+    carried = step_size * tol_m.reshape(-1) / den + \
+        np.abs(upd) * tol_v.reshape(-1) / np.maximum(2.0 * v_r.reshape(-1), 1e-300)
+    tol_p = 2 * np.spacing(np.abs(gp.astype(np.float32))).astype(np.float64) + \
+        2e-6 * np.abs(upd) + carried
+    err = np.abs(gp - p_r.reshape(-1))
+    assert np.all(err <= tol_p), f"{what}: logits off by {float((err - tol_p).max()):.3g}"
+    return tol_p
+
+
+@pytest.mark.parametrize("scale", ["config", "unit"])
 @pytest.mark.parametrize("case", ADAMW, ids=lambda c: "x".join(map(str, c[:4])) + f"-t{c[6]}")
-def test_bwd_adamw_against_oracle(dev, case):
+def test_bwd_adamw_against_oracle(dev, case, scale):
     """The fused backward + AdamW step against the oracle's backward followed by
     its AdamW step; the gradient it also writes equals roi_mask_bwd's bit for
-    bit."""
+    bit.  At config scale (and with unit-scale W and upstream gradients, where
+    the gradient is held to the relative bar with its fp32 allowance)."""
     import torch
     rows, cols, n, m, tau, lam, t, lr = case
     seed, step, off = 17, 3, 64
-    say(f"bwd+adamw {rows}x{cols} {n}:{m} tau={tau} lam={lam} t={t} lr={lr}")
-    W, L, G = wl.small_case(rows, cols, rows + cols, device=dev)
+    unit = scale == "unit"
+    say(f"bwd+adamw {rows}x{cols} {n}:{m} tau={tau} lam={lam} t={t} lr={lr} {scale} scale")
+    if unit:
+        W, L, G = wl.small_case(rows, cols, rows + cols + 1, device=dev, w_std=1.0, grad_std=1.0,
+                                logit_std=2.0)
+    else:
+        W, L, G = wl.small_case(rows, cols, rows + cols, device=dev)
     m0, v0 = adamw_state(rows, cols, t)
+    if unit:  # moments of the size a unit-scale gradient builds up
+        m0, v0 = (m0 * 5e3).astype(np.float32), (v0 * 1e7).astype(np.float32)
     opt = roi.adamw_params(lr, t=t)
     Lg, mg, vg = L.clone(), torch.from_numpy(m0).to(dev), torch.from_numpy(v0).to(dev)
     d = torch.empty_like(L)
@@ -448,34 +490,25 @@ def test_bwd_adamw_against_oracle(dev, case):
     assert torch.equal(d.view(torch.int32), d_ref.view(torch.int32))
     tau32, lam32 = float(np.float32(tau)), float(np.float32(lam))
     d_o = oracle.mask_bwd(bf16_bits(G), bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
-    p_o, m_o, v_o = oracle.adamw(d_o, f32(L), m0, v0, float(np.float32(lr)), float(np.float32(0.9)),
-                                 float(np.float32(0.95)), float(np.float32(1e-8)),
-                                 float(np.float32(0.05)), t)
-    assert_close(f32(d), d_o, "grad_logits (fused)")
-    assert_close(f32(mg), m_o, "exp_avg")
-    assert_close(f32(vg), v_o, "exp_avg_sq")
-    assert_close(f32(Lg), p_o, "logits after AdamW")
-    # The update term itself (beyond the decay) against the oracle's.  Its
-    # allowance: the worst change of the oracle's update when the gradient
-    # moves within the gradient's own tolerance, plus 1% for the fp32 step and
-    # one ulp of the stored logit.  A wrong step formula (a missing bias
-    # correction, swapped betas) moves the update by tens of percent.
+    check_grad(d, d_o, L, G, W, n, m, tau32, lam32, seed, step, off, scale_aware=unit)
     hp = [float(np.float32(x)) for x in (lr, 0.9, 0.95, 1e-8, 0.05)]
-    decayed = f32(L).astype(np.float64).reshape(-1) * (1.0 - hp[0] * hp[4])
-    got_upd = f32(Lg).astype(np.float64).reshape(-1) - decayed
-    ref_upd = p_o.reshape(-1) - decayed
-    tol_g = 1e-6 + 1e-5 * np.abs(d_o)
-    spread = np.zeros_like(ref_upd)
-    for sign in (-1.0, 1.0):
-        p_s, _, _ = oracle.adamw(d_o + sign * tol_g, f32(L), m0, v0, *hp, t)
-        spread = np.maximum(spread, np.abs(p_s.reshape(-1) - decayed - ref_upd))
-    ulp = np.spacing(np.abs(f32(Lg).reshape(-1))).astype(np.float64)
-    bad = np.abs(got_upd - ref_upd) > spread + 1e-2 * np.abs(ref_upd) + ulp
-    assert not bad.any(), f"{int(bad.sum())} update terms off"
-    # and the allowance is tight enough to see a missing bias correction
-    p_nb, _, _ = oracle.adamw(d_o, f32(L), m0, v0, *hp, 1)
-    wrong = np.abs(p_nb.reshape(-1) - decayed - ref_upd) > spread + 1e-2 * np.abs(ref_upd) + ulp
-    assert t == 1 or wrong.mean() > 0.5
+    # the step's own arithmetic, from the kernel's gradient
+    tol_p = adamw_rounding_check(f32(Lg), f32(mg), f32(vg), f32(d), f32(L), m0, v0, hp, t,
+                                 "fused AdamW")
+    # The check is tight enough to see a wrong step: without the bias
+    # corrections (t = 1) most logits fall outside it.
+    if t > 1:
+        p_nb, _, _ = oracle.adamw(f32(d).astype(np.float64), f32(L), m0, v0, *hp, 1)
+        wrong = np.abs(f32(Lg).astype(np.float64).reshape(-1) - p_nb.reshape(-1)) > tol_p
+        assert wrong.mean() > 0.5
+    # and the logits against the oracle's own backward + AdamW: the gradient's
+    # tolerance carried through the step (first order, from the oracle)
+    p_o, _, _ = oracle.adamw(d_o, f32(L), m0, v0, *hp, t)
+    got_d = f32(d).astype(np.float64).reshape(-1)
+    p_g, _, _ = oracle.adamw(got_d, f32(L), m0, v0, *hp, t)
+    moved = np.abs(p_g.reshape(-1) - p_o.reshape(-1))  # what the gradient difference moves
+    assert np.all(np.abs(f32(Lg).astype(np.float64).reshape(-1) - p_o.reshape(-1))
+                  <= moved + tol_p), "logits after AdamW"
 
 
 def test_full_bwd_adamw_7b_stack(dev):
@@ -510,8 +543,8 @@ def test_full_bwd_adamw_7b_stack(dev):
     hp = [float(np.float32(x)) for x in (lr, 0.9, 0.95, 1e-8, 0.05)]
     p_o, m_o, v_o = oracle.adamw(d_o, L0, m0, v0, *hp, step + 1)
     assert_close(f32(take(d)), d_o, "grad_logits (fused, full stack)")
-    assert_close(f32(take(mom)), m_o, "exp_avg (full stack)")
-    assert_close(f32(take(sec)), v_o, "exp_avg_sq (full stack)")
+    adamw_rounding_check(f32(take(L)), f32(take(mom)), f32(take(sec)), f32(take(d)), L0, m0, v0,
+                         hp, step + 1, "fused AdamW (full stack)")
     assert_close(f32(take(L)), p_o, "logits after AdamW (full stack)")
     del W, L, G, mom, sec, d
     torch.cuda.empty_cache()
@@ -537,16 +570,28 @@ def test_bwd_adamw_three_steps(dev):
         lr = roi.anneal(1e-3, 1e-4, t - 1, 3)
         say(f"adamw chain t={t} tau={tau:.4f} lam={lam:.4f} lr={lr:.2e}")
         G = (torch.randn(rows, cols, generator=gen) * 1e-3).to(torch.bfloat16).to(dev)
+        before = [f32(x) for x in (Lg, mg, vg)]
+        d = torch.empty_like(Lg)
         roi.mask_bwd_adamw(G, W, Lg, mg, vg, n, m, tau, lam, 0, t, 0,
-                           opt=roi.adamw_params(lr, t=t))
+                           opt=roi.adamw_params(lr, t=t), grad_out=d)
         torch.cuda.synchronize()
+        hp = [float(np.float32(x)) for x in (lr, 0.9, 0.95, 1e-8, 0.05)]
+        # this step's arithmetic from the GPU's own state and gradient
+        adamw_rounding_check(f32(Lg), f32(mg), f32(vg), f32(d), *before, hp, t,
+                             f"AdamW step {t}")
+        # the gradient at the GPU's logits, then the chain against the oracle
+        # carrying its own state
+        assert_close(f32(d), oracle.mask_bwd(bf16_bits(G), bf16_bits(W), before[0], n, m, tau,
+                                             lam, 0, t, 0), f"grad_logits at step {t}")
         d_o = oracle.mask_bwd(bf16_bits(G), bf16_bits(W), p_o, n, m, tau, lam, 0, t, 0)
-        p64, m64, v64 = oracle.adamw(d_o, p_o, m_o, v_o, lr, float(np.float32(0.9)),
-                                     float(np.float32(0.95)), float(np.float32(1e-8)),
-                                     float(np.float32(0.05)), t)
+        p64, m64, v64 = oracle.adamw(d_o, p_o, m_o, v_o, *hp, t)
         assert_close(f32(Lg), p64, f"logits after step {t}")
-        assert_close(f32(mg), m64, f"exp_avg after step {t}")
-        assert_close(f32(vg), v64, f"exp_avg_sq after step {t}")
+        tol_g = 1e-6 + 1e-5 * np.abs(d_o)
+        assert np.all(np.abs(f32(mg).reshape(-1) - m64) <= (1 - hp[1]) * tol_g + 1e-7 * np.abs(m64)
+                      + 2 * np.abs(before[1].reshape(-1) - m_o.reshape(-1))), f"exp_avg, step {t}"
+        assert np.all(np.abs(f32(vg).reshape(-1) - v64) <=
+                      (1 - hp[2]) * (2 * np.abs(d_o) + tol_g) * tol_g + 1e-7 * v64
+                      + 2 * np.abs(before[2].reshape(-1) - v_o.reshape(-1))), f"exp_avg_sq, step {t}"
         p_o, m_o, v_o = (x.astype(np.float32) for x in (p64, m64, v64))
 
 
@@ -675,19 +720,58 @@ CAT = [(37, 36, 2, 4, 1.0, 1.0, 0), (64, 96, 2, 4, 0.3, 0.6, 5), (33, 64, 1, 4, 
        (25, 64, 7, 8, 1.0, 1.0, 0), (19, 96, 3, 8, 0.8, 1.0, 2 ** 40)]
 
 
+def cat_fp32_floor(alpha, G_bits, W_bits, n, m, tau, lam, seed, step, goff):
+    """fp32 rounding allowance of the categorical gradient (as fp32_key_floor
+    for the item sampler): FP32_FLOOR_FACTOR times the first-order change of
+    the fp64 softmax derivative y (ybar - <y, ybar>) / (tau lambda) when each
+    fp32 key moves by one ulp.  The keys are the oracle's (candidate c of group
+    Q has the noise of element 4 ceil(C / 4) Q + c)."""
+    from tests.gpu_helpers import FP32_FLOOR_FACTOR
+    A = np.asarray(alpha, dtype=np.float32)
+    groups, C = A.shape
+    B = (C + 3) // 4
+    kappa = np.stack([oracle.keys(A[q], lam, seed, step, 4 * B * (goff + q))
+                      for q in range(groups)]).astype(np.float32)
+    masks = oracle.cat_candidates(n, m)
+    member = ((masks[:, None] >> np.arange(m)[None, :]) & 1).astype(np.float64)  # [C, m]
+    ybar = sbar_of(G_bits, W_bits).reshape(groups, m) @ member.T
+
+    def grad(k):
+        z = k / tau
+        y = np.exp(z - z.max(axis=1, keepdims=True))
+        y /= y.sum(axis=1, keepdims=True)
+        return y * (ybar - (y * ybar).sum(axis=1, keepdims=True)) / (tau * lam)
+
+    k64 = kappa.astype(np.float64)
+    base = grad(k64)
+    ulp = np.spacing(np.abs(kappa)).astype(np.float64)
+    floor = np.zeros_like(base)
+    for c in range(C):
+        kp = k64.copy()
+        kp[:, c] += ulp[:, c]
+        floor += np.abs(grad(kp) - base)
+    return FP32_FLOOR_FACTOR * floor
+
+
+@pytest.mark.parametrize("scale", ["config", "unit"])
 @pytest.mark.parametrize("case", CAT, ids=lambda c: "x".join(map(str, c[:4])))
-def test_cat_sampler_against_oracle(dev, case):
+def test_cat_sampler_against_oracle(dev, case, scale):
     """The categorical sampler: chosen candidates and masked weights bit-exact
     (with and without the soft mask), S and dL/dalpha within the float
     tolerance, against the oracle; large group offsets exercise Philox block
-    indices above 2^32."""
+    indices above 2^32.  With unit-scale W and upstream gradients the gradient
+    is also held to the relative bar with its fp32 allowance."""
     import torch
     rows, cols, n, m, tau, lam, goff = case
     C = roi.cat_num_candidates(n, m)
-    say(f"cat {rows}x{cols} {n}:{m} C={C} tau={tau} lam={lam} goff={goff}")
-    W, _, G = wl.small_case(rows, cols, rows + 3 * cols + n)
+    unit = scale == "unit"
+    say(f"cat {rows}x{cols} {n}:{m} C={C} tau={tau} lam={lam} goff={goff} {scale} scale")
+    if unit:
+        W, _, G = wl.small_case(rows, cols, rows + 3 * cols + n + 1, w_std=1.0, grad_std=1.0)
+    else:
+        W, _, G = wl.small_case(rows, cols, rows + 3 * cols + n)
     gen = torch.Generator(device="cpu").manual_seed(n * 100 + m)
-    A = torch.randn(rows * cols // m, C, generator=gen)
+    A = torch.randn(rows * cols // m, C, generator=gen) * (2.0 if unit else 1.0)
     W, G, A = W.to(dev), G.to(dev), A.to(dev)
     Wm, S, ch = roi.cat_mask_fwd(W, A, n, m, tau, lam, 9, 4, goff, want_soft=True)
     Wm2, _, ch2 = roi.cat_mask_fwd(W, A, n, m, tau, lam, 9, 4, goff)
@@ -701,7 +785,11 @@ def test_cat_sampler_against_oracle(dev, case):
     assert np.array_equal(ch.cpu().numpy(), ch_o), "chosen candidates differ"
     assert np.array_equal(bf16_bits(Wm).reshape(-1), Wm_o), "masked weights differ"
     assert_close(f32(S), S_o, "categorical soft mask")
-    assert_close(f32(d), d_o, "dL/dalpha")
+    if not unit:
+        assert_close(f32(d), d_o, "dL/dalpha")
+    floor = cat_fp32_floor(f32(A), bf16_bits(G), bf16_bits(W), n, m, tau32, lam32, 9, 4, goff)
+    r = assert_close(f32(d), d_o, "dL/dalpha (relative)", scale_aware=True, floor=floor)
+    say(f"  dL/dalpha err/bound {r:.3f}")
 
 
 def test_full_cat_7b_stack_2of4(dev):
@@ -821,9 +909,61 @@ def sample_groups(workload, ngroups, m, rng, count):
     return np.unique(picks)
 
 
-def full_workload_check(dev, name, n, m, tau, step, count):
+def check_grad_whole(got, ref, kappa_of, sbar_of_groups, n, m, tau32, what):
+    """Every element: the plain bar (1e-6 absolute + 1e-5 relative), then the
+    relative bar (absolute term 1e-6 max|oracle|) with the fp32 allowance of
+    the keys, which is computed only for the groups that need it."""
+    from tests.gpu_helpers import ATOL, RTOL
+    r = assert_close(got, ref, what)
+    bound = ATOL * np.abs(ref).max() + RTOL * np.abs(ref)
+    need = np.flatnonzero((np.abs(got - ref) > bound).reshape(-1, m).any(axis=1))
+    floor = np.zeros(got.size)
+    if need.size:
+        fl = fp32_key_floor(oracle, kappa_of(need), sbar_of_groups(need), n, tau32, 1.0)
+        floor.reshape(-1, m)[need] = fl
+    rr = assert_close(got, ref, what + " (relative)", scale_aware=True, floor=floor)
+    say(f"  {what}: err/bound {r:.3f}; relative bar {rr:.3f}, "
+        f"{need.size} of {got.size // m} groups need the fp32 allowance")
+
+
+def whole_layer_check(dev, work, tensors, W, L, G, Wm, S, idx, d, n, m, tau, step):
+    """Every group of the given consecutive tensors (whole layers of the stack)
+    against the oracle on the host's cores: indices and masked weights bit for
+    bit, the soft mask and the gradient elementwise."""
+    import time
+    t0, t1 = work.tensors[tensors[0]], work.tensors[tensors[-1]]
+    e0, e1 = t0.offset, t1.offset + t1.numel
+    g0, g1 = e0 // m, e1 // m
+    threads = oracle.host_threads()
+    say(f"  whole-layer check: tensors {t0.name} .. {t1.name}, {e1 - e0} weights, "
+        f"oracle on {threads} threads")
+    Wb, Lh, Gb = bf16_bits(W[e0:e1]), f32(L[e0:e1]).reshape(-1), bf16_bits(G[e0:e1])
+    tau32 = float(np.float32(tau))
+    start = time.time()
+    Wm_o, S_o, idx_o = oracle.mask_fwd(Wb, Lh, n, m, tau32, 1.0, 0, step, e0, want_soft=True,
+                                       threads=threads)
+    say(f"  oracle forward {time.time() - start:.1f} s")
+    assert np.array_equal(idx[g0:g1].cpu().numpy(), idx_o), "selected indices differ"
+    assert np.array_equal(bf16_bits(Wm[e0:e1]).reshape(-1), Wm_o), "masked weights differ"
+    del Wm_o, idx_o
+    r = assert_close(f32(S[e0:e1]).reshape(-1), S_o, "soft mask (whole layer)")
+    say(f"  soft mask err/bound {r:.3f}")
+    del S_o
+    start = time.time()
+    d_o = oracle.mask_bwd(Gb, Wb, Lh, n, m, tau32, 1.0, 0, step, e0, threads=threads)
+    say(f"  oracle backward {time.time() - start:.1f} s")
+    Wg, Gg, Lg = Wb.reshape(-1, m), Gb.reshape(-1, m), Lh.reshape(-1, m)
+    kappa_of = lambda q: np.stack([oracle.keys(Lg[i], 1.0, 0, step, e0 + int(i) * m) for i in q])
+    sbar_of_groups = lambda q: sbar_of(Gg[q], Wg[q])
+    check_grad_whole(f32(d[e0:e1]).reshape(-1), d_o, kappa_of, sbar_of_groups, n, m, tau32,
+                     "grad_logits (whole layer)")
+
+
+def full_workload_check(dev, name, n, m, tau, step, count, whole=None):
     """The whole stack in one call (the benchmark's launch configuration):
-    sampled groups against the oracle, structural properties on every group."""
+    sampled groups against the oracle, structural properties on every group,
+    and every group of the tensors in `whole` (whole layers) against the
+    oracle on the host's cores."""
     import torch
     work = wl.WORKLOADS[name]
     say(f"full workload {name} {n}:{m} tau={tau} step={step}: allocating {work.numel} weights")
@@ -831,6 +971,15 @@ def full_workload_check(dev, name, n, m, tau, step, count):
     Wm, _, idx = roi.mask_fwd(W, L, n, m, tau, 1.0, 0, step, 0, want_soft=False)
     d = roi.mask_bwd(G, W, L, n, m, tau, 1.0, 0, step, 0)
     torch.cuda.synchronize()
+    if whole is not None:
+        # the forward with the soft mask: the same selection, bit for bit
+        Wm_s, S, idx_s = roi.mask_fwd(W, L, n, m, tau, 1.0, 0, step, 0, want_soft=True)
+        torch.cuda.synchronize()
+        assert torch.equal(idx_s, idx) and torch.equal(Wm_s.view(torch.int16), Wm.view(torch.int16))
+        del Wm_s, idx_s
+        whole_layer_check(dev, work, whole, W, L, G, Wm, S, idx, d, n, m, tau, step)
+        del S
+        torch.cuda.empty_cache()
     say("  kernels done; checking properties")
     ng = work.numel // m
     chunk = 1 << 26
@@ -871,24 +1020,34 @@ def test_full_qwen05b_stack_2of4(dev):
     full_workload_check(dev, "qwen2.5-0.5b-stack-2:4", 2, 4, 1.0, 0, 20000)
 
 
+LAST_LAYER = list(range(27 * 7, 28 * 7))  # the seven tensors of layer 27 of a 28-layer stack
+
+
 def test_full_qwen7b_layer_2of4(dev):
-    full_workload_check(dev, "qwen2.5-7b-layer-2:4", 2, 4, 0.5, 0, 20000)
+    """The 7B-class layer at 2:4: every group against the oracle."""
+    full_workload_check(dev, "qwen2.5-7b-layer-2:4", 2, 4, 0.5, 0, 20000, whole=list(range(7)))
 
 
 def test_full_qwen7b_layer_4of8(dev):
-    full_workload_check(dev, "qwen2.5-7b-layer-4:8", 4, 8, 0.5, 0, 20000)
+    """The 7B-class layer at 4:8: every group against the oracle."""
+    full_workload_check(dev, "qwen2.5-7b-layer-4:8", 4, 8, 0.5, 0, 20000, whole=list(range(7)))
 
 
 @pytest.mark.parametrize("step", [0, 9])
 def test_full_qwen7b_stack_2of4(dev, step):
+    """The whole 7B stack in one call at the first and the last annealing
+    step: every group of its last layer (global offsets past 6e9) against the
+    oracle, sampled groups elsewhere."""
     tau = roi.anneal(1.0, 0.1, step, 9)
-    full_workload_check(dev, "qwen2.5-7b-stack-2:4", 2, 4, tau, step, 30000)
+    full_workload_check(dev, "qwen2.5-7b-stack-2:4", 2, 4, tau, step, 30000, whole=LAST_LAYER)
 
 
 @pytest.mark.parametrize("name,n,m", [("qwen2.5-1.5b-stack-8:16", 8, 16),
                                       ("qwen2.5-1.5b-stack-16:32", 16, 32)])
 def test_full_qwen15b_stack_wide(dev, name, n, m):
-    full_workload_check(dev, name, n, m, 1.0, 0, 20000)
+    """The 1.5B stack at 8:16 and 16:32 in one call: every group of its last
+    layer against the oracle, sampled groups elsewhere."""
+    full_workload_check(dev, name, n, m, 1.0, 0, 20000, whole=LAST_LAYER)
 
 
 @pytest.mark.parametrize("name,n,m,tau,step", [("qwen2.5-7b-stack-2:4", 2, 4, 0.1, 9),
@@ -1043,19 +1202,19 @@ def test_soft_forward(dev, case):
     assert_close(got, ref, "W (.) S", floor=ulp)
 
 
-# n / (tau min(1, lambda)) up to 160: the hardware keys; (12:16, tau 0.1,
-# lambda 0.7) is past that limit and takes the exact keys.
+# the soft forward cases plus small temperatures and lambda != 1
 SOFT_ONLY = SOFT + [(61, 88, 6, 8, 0.1, 1.0, 3, 2, 0), (21, 80, 8, 16, 0.1, 0.7, 9, 1, 32),
-                    (21, 80, 12, 16, 0.1, 0.7, 9, 1, 32), (13, 64, 24, 32, 0.15, 1.0, 2, 5, 0)]
+                    (21, 80, 12, 16, 0.1, 0.7, 9, 1, 32), (13, 64, 24, 32, 0.15, 1.0, 2, 5, 0),
+                    (37, 48, 2, 4, 1.0, 0.01, 3, 1, 0)]
 
 
-@pytest.mark.parametrize("case", SOFT_ONLY, ids=lambda c: "x".join(map(str, c[:5])))
+@pytest.mark.parametrize("case", SOFT_ONLY, ids=lambda c: "x".join(map(str, c[:6])))
 def test_soft_forward_alone(dev, case):
     """The pure soft forward with W_soft as its only output (no S, no indices)
-    runs the relaxation on the hardware-log keys.  Against W (.) S from the
-    oracle's fp64 S it stays within one bf16 rounding step plus the float
-    tolerance, as the exact-key soft forward does, and it differs from that one
-    by at most one bf16 step per element."""
+    has a kernel of its own (no selection).  It runs the relaxation at the
+    exact keys, so its output is the soft forward's with S requested, bit for
+    bit, and within one bf16 rounding step plus the float tolerance of
+    W (.) S from the oracle's fp64 S."""
     import torch
     rows, cols, n, m, tau, lam, seed, step, off = case
     say(f"soft forward alone rows={rows} cols={cols} {n}:{m} tau={tau} lam={lam}")
@@ -1066,34 +1225,15 @@ def test_soft_forward_alone(dev, case):
     We, _, _ = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True,
                             soft_forward=True)
     torch.cuda.synchronize()
+    assert torch.equal(Ws.view(torch.int16), We.view(torch.int16)), \
+        "the soft forward alone differs from the soft forward with S"
     tau32, lam32 = float(np.float32(tau)), float(np.float32(lam))
     _, S_o, _ = oracle.mask_fwd(bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
     wf = (bf16_bits(W).astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1)
     ref = wf * S_o.reshape(-1)
-    to_f = lambda t: (bf16_bits(t).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-    got = to_f(Ws).reshape(-1)
+    got = (bf16_bits(Ws).astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1)
     ulp = np.where(ref != 0, 2.0 ** (np.floor(np.log2(np.abs(ref) + 1e-300)) - 7), 0.0)
-    assert_close(got, ref, "W (.) S from the hardware-log keys", floor=ulp)
-    # bf16 bit patterns of one sign are ordered like their values
-    a = bf16_bits(Ws).astype(np.int64).reshape(-1)
-    b = bf16_bits(We).astype(np.int64).reshape(-1)
-    assert np.abs(a - b).max() <= 1, "more than one bf16 step from the exact-key soft forward"
-    say(f"  {int((a != b).sum())} of {a.size} outputs one bf16 step from the exact-key ones")
-    if n / (tau * min(1.0, lam)) > 160:  # the exact keys: the exact-key output, bit for bit
-        assert np.array_equal(a, b)
-
-
-def test_soft_forward_alone_takes_exact_keys_at_small_lambda(dev):
-    """Past n / (tau min(1, lambda)) = 160 (here lambda = 0.01: keys a hundred
-    times larger) the soft forward alone takes the exact keys, so its output
-    is the exact-key soft forward's, bit for bit."""
-    import torch
-    W, L, _ = wl.small_case(37, 48, 5, device=dev, w_std=1.0)
-    Ws, _, _ = roi.mask_fwd(W, L, 2, 4, 1.0, 0.01, 3, 1, 0, want_soft=False, want_idx=False,
-                            soft_forward=True)
-    We, _, _ = roi.mask_fwd(W, L, 2, 4, 1.0, 0.01, 3, 1, 0, want_soft=True, soft_forward=True)
-    torch.cuda.synchronize()
-    assert torch.equal(Ws.view(torch.int16), We.view(torch.int16))
+    assert_close(got, ref, "W (.) S", floor=ulp)
 
 
 def test_stream_copy(dev):

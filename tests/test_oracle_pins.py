@@ -665,6 +665,33 @@ def test_groups_entry_matches_contiguous():
     assert np.array_equal(dg, d.reshape(-1, m)[sel])
 
 
+@pytest.mark.parametrize("threads", [2, 3, 7, 16])
+def test_threaded_oracle_is_the_scalar_oracle(threads):
+    """The threaded entry points only split the groups over threads: the same
+    bits as the scalar loop for any thread count, including more threads than
+    groups and a ragged split."""
+    rng = np.random.default_rng(41 + threads)
+    for m, n, groups, tau, lam in [(4, 2, 1001, 1.0, 1.0), (8, 4, 13, 0.5, 0.7),
+                                   (32, 16, 5, 1.0, 1.0), (16, 8, 2, 0.3, 1.0)]:
+        numel = m * groups
+        W = (rng.normal(0, 0.02, numel).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        G = (rng.normal(0, 1e-3, numel).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        phi = rng.normal(size=numel).astype(np.float32)
+        off = 4 * 777
+        ref = oracle.mask_fwd(W, phi, n, m, tau, lam, 9, 4, off)
+        got = oracle.mask_fwd(W, phi, n, m, tau, lam, 9, 4, off, threads=threads)
+        for a, b in zip(ref, got):
+            assert np.array_equal(a, b)
+        d_ref = oracle.mask_bwd(G, W, phi, n, m, tau, lam, 9, 4, off)
+        d_got = oracle.mask_bwd(G, W, phi, n, m, tau, lam, 9, 4, off, threads=threads)
+        assert np.array_equal(d_ref, d_got)
+        kappa = rng.normal(scale=2.0, size=(groups, m))
+        sbar = rng.normal(size=(groups, m))
+        many = oracle.relax_bwd_groups(kappa, n, tau, sbar, threads=threads)
+        for q in range(groups):
+            assert np.array_equal(many[q], oracle.relax_bwd(kappa[q], n, tau, sbar[q]))
+
+
 def test_bwd_chains_straight_through_and_lambda():
     """dL/dphi = (1/lambda) dS/dkappa^T (G (.) W): the straight-through backward
     treats W_masked as W (.) S."""
