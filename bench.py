@@ -90,69 +90,158 @@ def measured_traffic():
     return rec
 
 
-def copy_calibration(nbytes: int) -> int:
-    """A plain device-to-device copy of nbytes (torch's copy kernel), run under
-    rocprofv3 --pmc to learn what FETCH_SIZE / WRITE_SIZE read for known bytes."""
+# Hardware-counter passes of the traffic record (rocprofv3 --pmc, one pass
+# each; a pass holds at most four TCC counters).  FETCH_SIZE and WRITE_SIZE
+# are the derived memory-side kilobytes per dispatch.  The second estimates
+# come from other counters: the read requests to memory counted by size
+# (128, 64 and 32 bytes), and the 32-byte sectors of the write requests that
+# reach the L2 from the compute units.
+COUNTER_PASSES = {
+    "fetch": ["FETCH_SIZE"],
+    "write": ["WRITE_SIZE", "TCC_WRITE_SECTORS_sum"],
+    "reads": ["TCC_EA0_RDREQ_128B_sum", "TCC_EA0_RDREQ_64B_sum", "TCC_EA0_RDREQ_32B_sum"],
+}
+
+
+def counter_calibration(nbytes: int) -> int:
+    """Three kernels that move known bytes, for the counter passes: the
+    library's streaming copy (reads and writes nbytes, with the access pattern
+    of the sampler's kernels), a sum over nbytes (reads only) and a fill of
+    nbytes (writes only)."""
     import torch
+
+    import paper_2608_23048_amd as roi
+    # The contents do not matter, only the bytes moved: the buffers are left
+    # uninitialized, so that the fill below is the program's only fill, and the
+    # sum runs over fp32 (an integer sum would first widen the data).
     a = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
-    a.fill_(1)
     b = torch.empty_like(a)
     torch.cuda.synchronize()
-    b.copy_(a)
+    roi.stream_copy(a, b)
     torch.cuda.synchronize()
-    print(json.dumps({"copy_bytes": nbytes}), flush=True)
+    a.view(torch.float32).sum()
+    torch.cuda.synchronize()
+    b.fill_(3)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration_bytes": nbytes}), flush=True)
     return 0
 
 
-def pmc_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes, numel, n,
-                m) -> int:
-    """Turn four rocprofv3 --pmc counter CSVs (FETCH_SIZE and WRITE_SIZE of the
-    benchmark and of the calibration copy) into the committed traffic record."""
+def _dispatch_counters(path):
+    """{dispatch id: (kernel name, {counter: value})} from a rocprofv3 --pmc CSV."""
     import csv
+    out = {}
+    for r in csv.DictReader(open(path)):
+        d = out.setdefault(r["Dispatch_Id"], (r["Kernel_Name"], {}))
+        d[1][r["Counter_Name"]] = d[1].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return out
+
+
+def _bytes_of(c):
+    """Byte estimates of one dispatch from whatever counters it carries."""
+    est = {}
+    if "FETCH_SIZE" in c:
+        est["fetch_size"] = c["FETCH_SIZE"] * 1024.0
+    if "WRITE_SIZE" in c:
+        est["write_size"] = c["WRITE_SIZE"] * 1024.0
+    if "TCC_EA0_RDREQ_128B_sum" in c:
+        est["read_requests"] = (128.0 * c["TCC_EA0_RDREQ_128B_sum"] +
+                                64.0 * c["TCC_EA0_RDREQ_64B_sum"] +
+                                32.0 * c["TCC_EA0_RDREQ_32B_sum"])
+    if "TCC_WRITE_SECTORS_sum" in c:
+        est["write_requests"] = 32.0 * c["TCC_WRITE_SECTORS_sum"]
+    return est
+
+
+def _largest(disp, key):
+    """Mean byte estimates over the full-size dispatches (within a factor 2 of
+    the largest) of the kernels whose name contains key."""
+    rows = [_bytes_of(c) for name, c in disp.values() if key in name]
+    rows = [r for r in rows if r]
+    if not rows:
+        return None
+    out = {}
+    for k in rows[0]:
+        vals = [r[k] for r in rows if k in r]
+        big = [v for v in vals if v >= 0.5 * max(vals)] or vals
+        out[k] = sum(big) / len(big)
+    return out
+
+
+def _total(disp, key):
+    """Byte estimates summed over every dispatch of the kernels whose name
+    contains key (a library may split one operation into several launches)."""
+    out = {}
+    for name, c in disp.values():
+        if key in name:
+            for k, v in _bytes_of(c).items():
+                out[k] = out.get(k, 0.0) + v
+    return out
+
+
+def traffic_summary(bench_csvs, calib_csvs, calib_bytes: int, numel: int, n: int, m: int) -> int:
+    """The committed traffic record from the counter passes of the benchmark
+    and of the calibration run (one CSV per pass, in COUNTER_PASSES order).
+    FETCH_SIZE and WRITE_SIZE are scaled by what they read for the streaming
+    copy of known size; the read-only and write-only kernels and the
+    request-size counters check those scales."""
     import json as _json
+    bench, calib = {}, {}
+    for path in bench_csvs:
+        for k, v in _dispatch_counters(path).items():
+            bench.setdefault(k + "@" + path, v)
+    for path in calib_csvs:
+        for k, v in _dispatch_counters(path).items():
+            calib.setdefault(k + "@" + path, v)
 
-    def per_kernel(path, counter):
-        vals = {}
-        for r in csv.DictReader(open(path)):
-            if r.get("Counter_Name") != counter:
-                continue
-            name = r["Kernel_Name"]
-            vals.setdefault(name, []).append(float(r["Counter_Value"]))
-        return vals
+    def merged(disp, key, per_launch=True):
+        est = {}
+        for path in set(p.split("@", 1)[1] for p in disp):
+            sub = {k: v for k, v in disp.items() if k.endswith("@" + path)}
+            e = _largest(sub, key) if per_launch else _total(sub, key)
+            if e:
+                est.update(e)
+        return est
 
-    def pick(vals, key):
-        # mean over the full-size dispatches of the kernel (within a factor 2 of
-        # the largest), so that smaller launches of the same kernel do not count
-        hits = [v for k, v in vals.items() if key in k]
-        flat = [x for v in hits for x in v]
-        if not flat:
-            return None
-        big = [x for x in flat if x >= 0.5 * max(flat)]
-        return sum(big) / len(big)
-
-    cf = per_kernel(copy_fetch_csv, "FETCH_SIZE")
-    cw = per_kernel(copy_write_csv, "WRITE_SIZE")
-    copy_bytes = int(copy_bytes)
-    # the calibration copy is the HIP runtime's device-to-device copy kernel
-    copy_fetch = pick(cf, "copyBuffer")
-    copy_write = pick(cw, "copyBuffer")
-    fetch_scale = copy_bytes / (copy_fetch * 1024.0) if copy_fetch else None
-    write_scale = copy_bytes / (copy_write * 1024.0) if copy_write else None
-    f = per_kernel(fetch_csv, "FETCH_SIZE")
-    w = per_kernel(write_csv, "WRITE_SIZE")
+    B = float(calib_bytes)
+    known = {"stream_copy": (B, B), "reduce": (B, 0.0), "fill": (0.0, B)}
+    cal = {}
+    for key, (rd, wr) in known.items():
+        pattern = {"stream_copy": "stream_copy_kernel", "reduce": "reduce_kernel",
+                   "fill": "FillFunctor"}[key]
+        e = merged(calib, pattern, per_launch=False)
+        cal[key] = {"known_read_bytes": rd, "known_write_bytes": wr, **e}
+    sc = cal["stream_copy"]
+    fetch_scale = B / sc["fetch_size"] if sc.get("fetch_size") else None
+    write_scale = B / sc["write_size"] if sc.get("write_size") else None
+    for key, e in cal.items():
+        rd, wr = known[key]
+        if rd and e.get("fetch_size"):
+            e["fetch_size_over_known"] = e["fetch_size"] / rd
+        if rd and e.get("read_requests"):
+            e["read_requests_over_known"] = e["read_requests"] / rd
+        if wr and e.get("write_size"):
+            e["write_size_over_known"] = e["write_size"] / wr
+        if wr and e.get("write_requests"):
+            e["write_requests_over_known"] = e["write_requests"] / wr
     bf, bb = algorithmic_bytes(n, m)
-    out = {"kernel_source_hash": kernel_source_hash(), "copy_bytes": copy_bytes,
-           "fetch_scale": fetch_scale, "write_scale": write_scale, "kernels": {}}
+    out = {"kernel_source_hash": kernel_source_hash(), "calibration_bytes": calib_bytes,
+           "fetch_scale": fetch_scale, "write_scale": write_scale, "calibration": cal,
+           "kernels": {}}
     for key, alg in (("fwd_lane_kernel", bf), ("bwd_lane_kernel", bb)):
-        fk, wk = pick(f, key), pick(w, key)
-        if fk is None or wk is None:
+        e = merged(bench, key)
+        if not e or "fetch_size" not in e or "write_size" not in e:
             continue
-        rd = fk * 1024.0 * fetch_scale
-        wr = wk * 1024.0 * write_scale
-        out["kernels"][key] = {"fetch_kib": fk, "write_kib": wk, "read_bytes": rd,
-                               "write_bytes": wr, "traffic_bytes": rd + wr,
-                               "algorithmic_bytes": alg * numel,
-                               "traffic_over_algorithmic": (rd + wr) / (alg * numel)}
+        rd = e["fetch_size"] * fetch_scale
+        wr = e["write_size"] * write_scale
+        rec = {"fetch_kib": e["fetch_size"] / 1024.0, "write_kib": e["write_size"] / 1024.0,
+               "read_bytes": rd, "write_bytes": wr, "traffic_bytes": rd + wr,
+               "algorithmic_bytes": alg * numel,
+               "traffic_over_algorithmic": (rd + wr) / (alg * numel)}
+        if "read_requests" in e and "write_requests" in e:
+            rec["request_counters_bytes"] = e["read_requests"] + e["write_requests"]
+            rec["request_counters_over_algorithmic"] = rec["request_counters_bytes"] / (alg * numel)
+        out["kernels"][key] = rec
     _json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
     print(_json.dumps(out), flush=True)
     return 0
@@ -712,23 +801,27 @@ def main() -> int:
                          "with the AdamW step on the logits fused in; export: the final-mask "
                          "export after training; cat: the categorical sampler against the item "
                          "sampler")
-    ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
-                    help="only run a plain device copy of BYTES (PMC calibration)")
+    ap.add_argument("--counter-calibration", type=int, metavar="BYTES",
+                    help="only run three kernels that move BYTES (copy, read, write): the "
+                         "known-size references of the traffic counters")
     ap.add_argument("--valu-summary", metavar="INSTS_CSV",
                     help="add the workload's VALU counters (rocprofv3 --pmc SQ_INSTS_VALU "
                          "SQ_INSTS_VALU_TRANS_F32 SQ_WAVES) to the committed record")
-    ap.add_argument("--pmc-summary", nargs=5,
-                    metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE", "COPY_BYTES"),
-                    help="write the traffic record from rocprofv3 --pmc counter CSVs")
+    ap.add_argument("--traffic-summary", nargs=7,
+                    metavar=("B_FETCH", "B_WRITE", "B_READS", "C_FETCH", "C_WRITE", "C_READS",
+                             "BYTES"),
+                    help="write the traffic record from the rocprofv3 --pmc CSVs of the "
+                         "counter passes (benchmark, then calibration) and the calibration size")
     args = ap.parse_args()
-    if args.copy_calibration:
-        return copy_calibration(args.copy_calibration)
+    if args.counter_calibration:
+        return counter_calibration(args.counter_calibration)
     if args.valu_summary:
         return valu_summary(args.valu_summary, args.workload)
-    if args.pmc_summary:
+    if args.traffic_summary:
         from paper_2608_23048_amd import workloads as wl
         work = wl.WORKLOADS[args.workload]
-        return pmc_summary(*args.pmc_summary, work.numel, work.n, work.m)
+        t = args.traffic_summary
+        return traffic_summary(t[0:3], t[3:6], int(t[6]), work.numel, work.n, work.m)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the sampler needs no collectives, and this build "
               "runs and reports a single MI355X (pass --gpus 1).", file=sys.stderr)

@@ -48,37 +48,71 @@ def test_source_hash_ignores_comments_only():
 
 def _counters(path, rows):
     with open(path, "w", newline="") as f:
-        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Counter_Name", "Counter_Value"])
+        w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name",
+                                          "Counter_Value"])
         w.writeheader()
         for r in rows:
             w.writerow(r)
 
 
-def test_pmc_summary_keeps_full_size_dispatches(tmp_path, monkeypatch):
-    """Two full-size dispatches and a small one of the same kernel: the small
-    one does not dilute the per-launch figure; the copy calibration scales
-    FETCH_SIZE by 2 when it reads half the bytes."""
+def _pass_rows(dispatches, counters_of):
+    """CSV rows of one counter pass: dispatches is [(id, kernel, read, write)]."""
+    rows = []
+    for did, name, rd, wr in dispatches:
+        for c, v in counters_of(rd, wr).items():
+            rows.append({"Dispatch_Id": did, "Kernel_Name": name, "Counter_Name": c,
+                         "Counter_Value": v})
+    return rows
+
+
+# what each pass reads for `rd` bytes read and `wr` written, on a device
+# whose FETCH_SIZE sees half the bytes read (128-byte requests counted as 64)
+PASSES = {
+    "fetch": lambda rd, wr: {"FETCH_SIZE": rd / 2 / 1024},
+    "write": lambda rd, wr: {"WRITE_SIZE": wr / 1024, "TCC_WRITE_SECTORS_sum": wr / 32},
+    "reads": lambda rd, wr: {"TCC_EA0_RDREQ_128B_sum": rd / 128, "TCC_EA0_RDREQ_64B_sum": 0,
+                             "TCC_EA0_RDREQ_32B_sum": 0},
+}
+
+
+def test_traffic_summary_calibrates_and_keeps_full_size_dispatches(tmp_path, monkeypatch):
+    """Two full-size dispatches and a small one of each kernel: the small one
+    does not dilute the per-launch figure; FETCH_SIZE is scaled by what it
+    reads for the calibration copy, and the read-only, write-only and
+    request-size figures are recorded against the known bytes."""
     numel, n, m = 1 << 20, 2, 4
     bf, bb = bench.algorithmic_bytes(n, m)
-    f_full, w_full = bf * numel / 2 / 1024 * 0.75, bf * numel / 1024 * 0.25
-    rows_f = [{"Kernel_Name": "fwd_lane_kernel<4,2>", "Counter_Name": "FETCH_SIZE",
-               "Counter_Value": v} for v in (f_full, f_full, f_full / 50)]
-    rows_w = [{"Kernel_Name": "fwd_lane_kernel<4,2>", "Counter_Name": "WRITE_SIZE",
-               "Counter_Value": v} for v in (w_full, w_full, w_full / 50)]
-    copy = 1 << 30
-    _counters(tmp_path / "f.csv", rows_f)
-    _counters(tmp_path / "w.csv", rows_w)
-    _counters(tmp_path / "cf.csv", [{"Kernel_Name": "__amd_rocclr_copyBuffer",
-                                     "Counter_Name": "FETCH_SIZE", "Counter_Value": copy / 2048}])
-    _counters(tmp_path / "cw.csv", [{"Kernel_Name": "__amd_rocclr_copyBuffer",
-                                     "Counter_Name": "WRITE_SIZE", "Counter_Value": copy / 1024}])
+    fwd_rd, fwd_wr = 6 * numel, (bf - 6) * numel
+    bench_disp = [("1", "fwd_lane_kernel<4,2>", fwd_rd, fwd_wr),
+                  ("2", "fwd_lane_kernel<4,2>", fwd_rd, fwd_wr),
+                  ("3", "fwd_lane_kernel<4,2>", fwd_rd / 50, fwd_wr / 50),
+                  ("4", "bwd_lane_kernel<4,2>", 8 * numel, 4 * numel)]
+    B = 1 << 30
+    # the library splits the sum and the fill into several launches
+    calib_disp = [("1", "roi::stream_copy_kernel(...)", B, B),
+                  ("2", "at::native::reduce_kernel<...>", B / 4, 0),
+                  ("3", "at::native::reduce_kernel<...>", 3 * B / 4, 0),
+                  ("4", "at::native::FillFunctor<...>", 0, B / 2),
+                  ("5", "at::native::FillFunctor<...>", 0, B / 2)]
+    paths = []
+    for who, disp in (("b", bench_disp), ("c", calib_disp)):
+        for name, fn in PASSES.items():
+            path = tmp_path / f"{who}_{name}.csv"
+            _counters(path, _pass_rows(disp, fn))
+            paths.append(str(path))
     out = tmp_path / "traffic.json"
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(out))
-    assert bench.pmc_summary(tmp_path / "f.csv", tmp_path / "w.csv", tmp_path / "cf.csv",
-                             tmp_path / "cw.csv", copy, numel, n, m) == 0
+    assert bench.traffic_summary(paths[0:3], paths[3:6], B, numel, n, m) == 0
     rec = json.load(open(out))
     assert rec["fetch_scale"] == pytest.approx(2.0) and rec["write_scale"] == pytest.approx(1.0)
-    assert rec["kernels"]["fwd_lane_kernel"]["traffic_over_algorithmic"] == pytest.approx(1.0)
+    cal = rec["calibration"]
+    assert cal["reduce"]["fetch_size_over_known"] == pytest.approx(0.5)
+    assert cal["reduce"]["read_requests_over_known"] == pytest.approx(1.0)
+    assert cal["fill"]["write_size_over_known"] == pytest.approx(1.0)
+    assert cal["fill"]["write_requests_over_known"] == pytest.approx(1.0)
+    for k in ("fwd_lane_kernel", "bwd_lane_kernel"):
+        assert rec["kernels"][k]["traffic_over_algorithmic"] == pytest.approx(1.0)
+        assert rec["kernels"][k]["request_counters_over_algorithmic"] == pytest.approx(1.0)
 
 
 def test_backward_flops_tally():
