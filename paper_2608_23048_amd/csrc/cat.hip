@@ -171,11 +171,13 @@ template <int C>
 __device__ __forceinline__ void cat_exact_keys(const float (&alpha)[C], const uint32_t (&x)[C],
                                                float lambda, const float2* tab, float (&k)[C])
 {
-    const bool lam1 = lambda == 1.0f;
+    // a wave-uniform branch, so that lambda = 1 does not run the division
+    if (__builtin_amdgcn_readfirstlane(__float_as_uint(lambda)) == 0x3F800000u) {
 #pragma unroll
-    for (int c = 0; c < C; ++c) {
-        const float ng = neg_gumbel_from_word(x[c], tab);
-        k[c] = (lam1 ? alpha[c] : alpha[c] / lambda) - ng;
+        for (int c = 0; c < C; ++c) k[c] = alpha[c] - neg_gumbel_from_word(x[c], tab);
+    } else {
+#pragma unroll
+        for (int c = 0; c < C; ++c) k[c] = alpha[c] / lambda - neg_gumbel_from_word(x[c], tab);
     }
 }
 

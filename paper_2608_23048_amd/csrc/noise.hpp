@@ -266,6 +266,21 @@ __device__ __forceinline__ bool fast_keys_separated(const float (&k)[M])
     return sep;
 }
 
+// phi / lambda for the four elements of a slot, correctly rounded; lambda == 1
+// (wave-uniform) takes phi as it is.  The division is a separate branch on
+// purpose: a select between phi and the quotient would run the division's
+// whole IEEE sequence at lambda = 1 too.
+__device__ __forceinline__ void scaled_logits4(const float (&phi)[4], float lambda, float (&a)[4])
+{
+    if (__builtin_amdgcn_readfirstlane(__float_as_uint(lambda)) == 0x3F800000u) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a[e] = phi[e];
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a[e] = phi[e] / lambda;
+    }
+}
+
 // kappa = fl(fl(phi / lambda) + g); for lambda == 1 the quotient is phi exactly.
 template <bool kLambdaOne>
 __device__ __forceinline__ float key_of(float phi, float lambda, uint32_t word, const float2* tab)

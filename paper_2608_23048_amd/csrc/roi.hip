@@ -437,61 +437,97 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
     }
 }
 
+// Keys from the logits and the noise ng = -g of m elements (four at a time).
+template <int M>
+__device__ __forceinline__ void keys_from_noise(const float (&phi)[M], const float (&ng)[M],
+                                                float lambda, float (&kappa)[M])
+{
+#pragma unroll
+    for (int t = 0; t < M / 4; ++t) {
+        const float p4[4] = {phi[4 * t], phi[4 * t + 1], phi[4 * t + 2], phi[4 * t + 3]};
+        float a4[4];
+        scaled_logits4(p4, lambda, a4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) kappa[4 * t + e] = a4[e] - ng[4 * t + e];
+    }
+}
+
+// One chunk of the soft forward alone: U groups per lane, loads first (the
+// log cells, then the groups' inputs), the noise while they are in flight,
+// no per-lane condition in a full chunk (see bwd_lane_span).
+template <int M, int N, int kQ, bool kFull>
+__device__ __forceinline__ void soft_lane_chunk(const FwdBatch& a, const FwdPiece& pc,
+                                                const NoiseKey& key, float2* tab, int64_t base,
+                                                int64_t ng_total)
+{
+    constexpr int U = kUnrollFwd<M>;
+    const float4 cells = log_cells_of_lane();
+    __builtin_amdgcn_sched_barrier(0);
+    float phi[U][M];
+    uint32_t w[U][M];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t q = base + u * kLaneBlock + threadIdx.x;
+        if (kFull || q < ng_total) {
+            load_logits<M>(pc.phi + q * M, phi[u]);
+            load_bf16<M>(pc.W + q * M, w[u]);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    float ng[U][M];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t q = base + u * kLaneBlock + threadIdx.x;
+        uint32_t x[M];
+        group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
+        if (u == 0) publish_log_table(tab, cells);
+#pragma unroll
+        for (int j = 0; j < M; ++j) ng[u][j] = neg_gumbel_from_word(x[j], tab);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t q = base + u * kLaneBlock + threadIdx.x;
+        if (!kFull && q >= ng_total) continue;
+        float kappa[M];
+        keys_from_noise<M>(phi[u], ng[u], a.lambda, kappa);
+        float S[M], b[M], bmax;
+        StepRec<M> unused[N]; // not written when records are not kept
+        if constexpr (kQ < 0) {
+            scaled_keys<M, false>(kappa, a.key_scale, b, bmax);
+            relax_forward<M, N, true, false>(b, bmax, a.inv_tau, S, unused);
+        } else if (scaled_keys<M>(kappa, a.key_scale, b, bmax) <= a.exp_span) {
+            relax_forward_exp<M, N, true, false, kQ>(b, bmax, a.inv_tau, S, unused);
+        } else {
+            relax_forward<M, N, true, false>(b, bmax, a.inv_tau, S, unused);
+        }
+        uint32_t ws[M];
+#pragma unroll
+        for (int j = 0; j < M; ++j) ws[j] = float_to_bf16_rne(bf16_bits_to_float(w[u][j]) * S[j]);
+        store_pairs<M>(pc.Wm + q * M, ws);
+    }
+}
+
 // Pure soft forward whose only output is W_soft = bf16(W (.) S) (neither S
 // nor the indices requested): the relaxation at the exact keys, with no
-// selection.  Each wave keeps its own copy of the log cells in LDS
+// selection.  The block's waves share one copy of the log cells in LDS
 // (noise.hpp), so a block starts streaming without a barrier.
 template <int M, int N, int kQ>
 __global__ __launch_bounds__(kLaneBlock) void fwd_soft_lane_kernel(FwdBatch a)
 {
-    __shared__ float4 wave_tabs[kLaneBlock / 64][kLogCells / 2];
-    const float2* tab = reinterpret_cast<const float2*>(wave_tabs[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)]);
+    __shared__ float4 tab4[kLogCells / 2];
+    float2* tab = reinterpret_cast<float2*>(tab4);
     const FwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
     const int64_t ng = pc.ngroups;
-    const bool lambda_one = a.lambda == 1.0f;
-    constexpr int U = kUnrollFwd<M>;
-    const int64_t chunk = (int64_t)kLaneBlock * U;
+    const int64_t chunk = (int64_t)kLaneBlock * kUnrollFwd<M>;
     for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * chunk; base < ng;
          base += (int64_t)pc.nblocks * chunk) {
-        float phi[U][M];
-        uint32_t w[U][M];
-        const float4 cells = log_cells_of_lane();
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q < ng) {
-                load_logits<M>(pc.phi + q * M, phi[u]);
-                load_bf16<M>(pc.W + q * M, w[u]);
-            }
-        }
-        publish_wave_log_table(const_cast<float2*>(tab), cells);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t q = base + u * kLaneBlock + threadIdx.x;
-            if (q >= ng) continue;
-            uint32_t x[M];
-            group_words<M>(pc.block0 + (uint32_t)q * (M / 4), key, x);
-            float kappa[M];
-            if (lambda_one)
-                exact_keys<M, true>(phi[u], x, 1.0f, tab, kappa);
-            else
-                exact_keys<M, false>(phi[u], x, a.lambda, tab, kappa);
-            float S[M], b[M], bmax;
-            StepRec<M> unused[N]; // not written when records are not kept
-            const float span = scaled_keys<M>(kappa, a.key_scale, b, bmax);
-            if (span <= a.exp_span)
-                relax_forward_exp<M, N, true, false, kQ>(b, bmax, a.inv_tau, S, unused);
-            else
-                relax_forward<M, N, true, false>(b, bmax, a.inv_tau, S, unused);
-            uint32_t ws[M];
-#pragma unroll
-            for (int j = 0; j < M; ++j)
-                ws[j] = float_to_bf16_rne(bf16_bits_to_float(w[u][j]) * S[j]);
-            store_pairs<M>(pc.Wm + q * M, ws);
-        }
+        if (base + chunk <= ng)
+            soft_lane_chunk<M, N, kQ, true>(a, pc, key, tab, base, ng);
+        else
+            soft_lane_chunk<M, N, kQ, false>(a, pc, key, tab, base, ng);
     }
 }
 
@@ -761,6 +797,7 @@ BwdFn bwd_for_n(int n, bool l, bool adam, int q, std::integer_sequence<int, Ns..
 template <int M, int N>
 FwdFn pick_soft(int q)
 {
+    if (q < 0) return fwd_soft_lane_kernel<M, N, -1>;
     return q == 1 ? fwd_soft_lane_kernel<M, N, 1>
                   : (q == 2 ? fwd_soft_lane_kernel<M, N, 2> : fwd_soft_lane_kernel<M, N, 0>);
 }
@@ -776,7 +813,7 @@ FwdFn soft_for_n(int n, int q, std::integer_sequence<int, Ns...>)
 // The soft forward with no output but W_soft.
 FwdFn select_soft_only(int m, int n, float tau)
 {
-    const int q = std::max(0, tau_mode(tau));
+    const int q = tau_mode(tau);
     if (m == 4) return soft_for_n<4>(n, q, std::make_integer_sequence<int, 4>{});
     if (m == 8) return soft_for_n<8>(n, q, std::make_integer_sequence<int, 8>{});
     return select_wide_soft_only(m, n, q);

@@ -310,13 +310,10 @@ __device__ __forceinline__ void wide_keys(const float (&phi)[4], uint32_t block,
 {
     const uint4 x = philox_block(block, key);
     const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-    const bool lam_one = lambda == 1.0f;
+    float phi_bar[4];
+    scaled_logits4(phi, lambda, phi_bar);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const float ng = neg_gumbel_from_word(w[e], tab);
-        const float phi_bar = lam_one ? phi[e] : phi[e] / lambda;
-        kappa[e] = phi_bar - ng;
-    }
+    for (int e = 0; e < 4; ++e) kappa[e] = phi_bar[e] - neg_gumbel_from_word(w[e], tab);
 }
 
 } // namespace

@@ -47,10 +47,10 @@ __device__ __forceinline__ void bwd_wide_slot(const BwdBatch& a, const BwdPiece&
         (L <= 4 || (kQ == 1 && !kAdam && waves_for_vgprs(36 + 8 * N) == waves_for_vgprs(28 + 8 * N)));
     float phi[4] = {in.phi.x, in.phi.y, in.phi.z, in.phi.w};
     // the keys the forward sampled: kappa = fl(fl(phi / lambda) + g) (noise.hpp)
-    const bool lam_one = a.lambda == 1.0f;
     float kappa[4];
+    scaled_logits4(phi, a.lambda, kappa);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) kappa[e] = (lam_one ? phi[e] : phi[e] / a.lambda) - ng[e];
+    for (int e = 0; e < 4; ++e) kappa[e] -= ng[e];
     // Straight-through: dL/dS = dL/dW_masked (.) W, exact in fp32.
     const float sbar[4] = {
         bf16_bits_to_float(in.g.x & 0xFFFFu) * bf16_bits_to_float(in.w.x & 0xFFFFu),

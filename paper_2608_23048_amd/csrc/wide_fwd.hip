@@ -99,54 +99,78 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
     }
 }
 
+// One slot of the pure soft forward: the loads go out first, the slot's noise
+// is computed while they are in flight, and a kFull pass has no per-lane
+// condition (as the backward's spans, wide_bwd.hip).
+template <int M, int N, int kQ, bool kFull>
+__device__ __forceinline__ void soft_wide_slot(const FwdBatch& a, const FwdPiece& pc,
+                                               const NoiseKey& key, float2* tab, int64_t slot,
+                                               int64_t nslots)
+{
+    constexpr int L = M / 4;
+    const float4 cells = log_cells_of_lane();
+    __builtin_amdgcn_sched_barrier(0);
+    f32x4 pv{};
+    u32x2 wv{};
+    if (kFull || slot < nslots) {
+        pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
+        wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    float ng[4];
+    {
+        const uint4 x = philox_block(pc.block0 + (uint32_t)slot, key);
+        const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+        publish_log_table(tab, cells);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ng[e] = neg_gumbel_from_word(w[e], tab);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // a group's lanes are all live or all past the end (groups are whole in a wave)
+    if (!kFull && slot >= nslots) return;
+    const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
+    float kappa[4];
+    scaled_logits4(phi, a.lambda, kappa);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) kappa[e] -= ng[e];
+    float S[4];
+    StepRec<4> unused[N]; // not written when records are not kept
+    wide_relax_forward<L, N, false, kQ>(kappa, a.key_scale, a.inv_tau, a.exp_span, true, S,
+                                        unused);
+    const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
+    const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
+    const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
+    const uint32_t h3 = float_to_bf16_rne(bf16_bits_to_float(wv.y >> 16) * S[3]);
+    const u32x2 out = {h0 | (h1 << 16), h2 | (h3 << 16)};
+    stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
+}
+
 // Pure soft forward whose only output is bf16(W (.) S): the relaxation at the
-// exact keys, no selection; each wave keeps its own copy of the log cells in
-// LDS (noise.hpp), as in fwd_soft_lane_kernel of roi.hip.
+// exact keys, no selection.  The block's waves share one copy of the log
+// cells in LDS (noise.hpp), so a block starts streaming without a barrier.
 template <int M, int N, int kQ>
 __global__ __launch_bounds__(kBlock) void fwd_soft_wide_kernel(FwdBatch a)
 {
-    constexpr int L = M / 4;
-    __shared__ float4 wave_tabs[kBlock / 64][kLogCells / 2];
-    const float2* tab = reinterpret_cast<const float2*>(wave_tabs[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)]);
+    __shared__ float4 tab4[kLogCells / 2];
+    float2* tab = reinterpret_cast<float2*>(tab4);
     const FwdPiece& pc = a.p[find_piece(a)];
     NoiseKey key = a.key_base;
     key.block_hi = pc.block_hi;
-    const int64_t nslots = pc.ngroups * L;
+    const int64_t nslots = pc.ngroups * (M / 4);
     const int64_t stride = (int64_t)pc.nblocks * kBlock;
     for (int64_t base = (int64_t)(blockIdx.x - pc.first_block) * kBlock; base < nslots;
          base += stride) {
-        const int64_t slot = base + threadIdx.x;
-        // a group's lanes are all live or all past the end (groups are whole in a wave)
-        const bool live = slot < nslots;
-        const float4 cells = log_cells_of_lane();
-        __builtin_amdgcn_sched_barrier(0);
-        f32x4 pv{};
-        u32x2 wv{};
-        if (live) {
-            pv = stream_load(reinterpret_cast<const f32x4*>(pc.phi + slot * 4));
-            wv = stream_load(reinterpret_cast<const u32x2*>(pc.W + slot * 4));
-        }
-        publish_wave_log_table(const_cast<float2*>(tab), cells);
-        if (!live) continue;
-        const float phi[4] = {pv.x, pv.y, pv.z, pv.w};
-        float kappa[4];
-        wide_keys(phi, pc.block0 + (uint32_t)slot, key, a.lambda, tab, kappa);
-        float S[4];
-        StepRec<4> unused[N]; // not written when records are not kept
-        wide_relax_forward<L, N, false, kQ>(kappa, a.key_scale, a.inv_tau, a.exp_span,
-                                            true, S, unused);
-        const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
-        const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
-        const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
-        const uint32_t h3 = float_to_bf16_rne(bf16_bits_to_float(wv.y >> 16) * S[3]);
-        const u32x2 out = {h0 | (h1 << 16), h2 | (h3 << 16)};
-        stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
+        if (base + kBlock <= nslots)
+            soft_wide_slot<M, N, kQ, true>(a, pc, key, tab, base + threadIdx.x, nslots);
+        else
+            soft_wide_slot<M, N, kQ, false>(a, pc, key, tab, base + threadIdx.x, nslots);
     }
 }
 
 template <int M, int N>
 FwdFn wide_soft_q(int q)
 {
+    if (q < 0) return fwd_soft_wide_kernel<M, N, -1>;
     return q == 1 ? fwd_soft_wide_kernel<M, N, 1>
                   : (q == 2 ? fwd_soft_wide_kernel<M, N, 2> : fwd_soft_wide_kernel<M, N, 0>);
 }

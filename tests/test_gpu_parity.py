@@ -921,9 +921,13 @@ def check_grad_whole(got, ref, kappa_of, sbar_of_groups, n, m, tau32, what):
     if need.size:
         fl = fp32_key_floor(oracle, kappa_of(need), sbar_of_groups(need), n, tau32, 1.0)
         floor.reshape(-1, m)[need] = fl
-    rr = assert_close(got, ref, what + " (relative)", scale_aware=True, floor=floor)
-    say(f"  {what}: err/bound {r:.3f}; relative bar {rr:.3f}, "
-        f"{need.size} of {got.size // m} groups need the fp32 allowance")
+    assert_close(got, ref, what + " (relative)", scale_aware=True, floor=floor)
+    worst = 0.0
+    if need.size:
+        e = np.abs(got - ref).reshape(-1, m)[need]
+        worst = float((e / (bound.reshape(-1, m)[need] + floor.reshape(-1, m)[need])).max())
+    say(f"  {what}: err/bound {r:.3f}; {need.size} of {got.size // m} groups over the relative "
+        f"bar, worst at {worst:.3f} of it with the fp32 allowance")
 
 
 def whole_layer_check(dev, work, tensors, W, L, G, Wm, S, idx, d, n, m, tau, step):
