@@ -97,8 +97,10 @@ constexpr double ln_atanh_series(double v)
     return s * acc;
 }
 
+// The cells in reverse order: entry j holds (inv, lg) of cell 127 - j, the
+// order in which det_log_bits() indexes them.
 struct alignas(16) LogCells {
-    float2 cell[kLogCells]; // (inv, lg)
+    float2 cell[kLogCells];
 };
 
 // The cell constants, evaluated by the compiler (IEEE fp64, round to nearest).
@@ -120,8 +122,8 @@ constexpr LogCells make_log_cells()
             inv = (float)(1.0 / centre);
             lg = (float)(-ln_atanh_series((double)inv));
         }
-        t.cell[i].x = inv;
-        t.cell[i].y = lg;
+        t.cell[kLogCells - 1 - i].x = inv;
+        t.cell[kLogCells - 1 - i].y = lg;
     }
     return t;
 }
@@ -171,21 +173,28 @@ __device__ __forceinline__ void publish_log_table(float2* tab, float4 cells)
     publish_wave_log_table(tab, cells);
 }
 
-// ln of the float whose bit pattern is ix.
+// ln of the float whose bit pattern is ix.  With t = ix - kLogZBaseBits the
+// exponent is k = floor(t / 2^23), z = x 2^-k and the cell is bits 16..22 of
+// t.  The code forms v = 0x7FFFFF - t instead: its low 23 bits are those of t
+// complemented and -k = floor(v / 2^23), so v gives -k by one shift, the cell
+// by its bits 16..22 (counted from the top, hence the reversed table), and z
+// as ix + (-k) 2^23.  fma(-k, -ln 2, s) equals fma(k, ln 2, s).
 __device__ __forceinline__ float det_log_bits(uint32_t ix, const float2* tab)
 {
-    const uint32_t t = ix - kLogZBaseBits;
-    const uint32_t cell = __builtin_amdgcn_ubfe(t, 16, 7); // bits 16..22: one bit-field extract
-    const int k = (int)t >> 23;
-    const float z = __uint_as_float((t & 0x007FFFFFu) + kLogZBaseBits); // = ix - (t & 0xFF800000)
-    const float2 c = tab[cell];
+    const uint32_t v = (0x7FFFFFu + kLogZBaseBits) - ix;
+    int nk = (int)v >> 23;
+    // Hides that nk came from v: the compiler would otherwise fold the shifts
+    // into a mask and an add, one instruction more than the shift-add.
+    asm("" : "+v"(nk));
+    const float z = __uint_as_float(ix + ((uint32_t)nk << 23));
+    const float2 c = tab[(v >> 16) & 0x7Fu];
     const float r = __builtin_fmaf(z, c.x, -1.0f);
     float p = __builtin_fmaf(r, -0.25f, kThird);
     p = __builtin_fmaf(r, p, -0.5f);
     const float r2 = r * r;
     const float l1p = __builtin_fmaf(r2, p, r);
     const float s = c.y + l1p;
-    return __builtin_fmaf((float)k, kLn2f, s);
+    return __builtin_fmaf((float)nk, -kLn2f, s);
 }
 
 __device__ __forceinline__ float det_log(float x, const float2* tab)

@@ -141,7 +141,9 @@ __device__ __forceinline__ float scaled_keys(const float (&kappa)[M], float key_
 // exp2(b - max b) and the update is b += log2(1 - mu) / tau: the same values
 // with one multiply fewer per element and step.  1 - mu_j is evaluated as
 // (sum of the other exponentials) / total, which never cancels, and
-// log(1 - mu) is floored at log(FLT_MIN).
+// log(1 - mu) is floored at log(FLT_MIN).  The records of the updating steps
+// hold max(1 - mu, FLT_MIN), the value whose log was taken: a floored entry
+// shows as exactly FLT_MIN (relax_backward).
 template <int M, int N, bool kWantS, bool kKeep>
 __device__ __forceinline__ void relax_forward(float (&b)[M], float bmax0, float inv_tau,
                                               float (&S)[M], StepRec<M> (&rec)[N])
@@ -169,13 +171,13 @@ __device__ __forceinline__ void relax_forward(float (&b)[M], float bmax0, float 
         for (int j = 0; j < M; ++j) {
             const float mu = e[j] * inv_total;
             const float om = others[j] * inv_total;
+            const float om_floor = k + 1 < N ? fmaxf(om, kFltMin) : om;
             if (kWantS) S[j] += mu;
             if (kKeep) {
                 rec[k].mu[j] = mu;
-                rec[k].om[j] = om;
+                rec[k].om[j] = om_floor;
             }
-            if (k + 1 < N)
-                b[j] = __builtin_fmaf(__builtin_amdgcn_logf(fmaxf(om, kFltMin)), inv_tau, b[j]);
+            if (k + 1 < N) b[j] = __builtin_fmaf(__builtin_amdgcn_logf(om_floor), inv_tau, b[j]);
         }
     }
 }
@@ -261,8 +263,12 @@ __device__ __forceinline__ void relax_forward_exp(const float (&b)[M], float bma
 // a_j, are negligible.
 // With kFloor, an entry whose 1 - mu fell below FLT_MIN at an updating step
 // had its log floored, so no derivative flows through it: mubar_j = sbar_j and
-// dL/dalpha^(k)_j = a_j + (mu_j / tau) X_j.  Without kFloor the caller has
-// ruled the floor out (the exp-domain form's span bound).
+// dL/dalpha^(k)_j = a_j + (mu_j / tau) X_j.  The records of relax_forward hold
+// max(1 - mu, FLT_MIN) there, so such an entry reads exactly FLT_MIN: it takes
+// a_j = 0 in both places, which also keeps a_j / omega_j finite.  X_j then uses
+// FLT_MIN for an omega_j below it, a change below FLT_MIN |sbar_j|.  Without
+// kFloor the caller has ruled the floor out (the exp-domain form's span
+// bound, whose records hold 1 - mu itself).
 template <int M, int N, bool kTauIsOne, bool kFloor>
 __device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const float (&sbar)[M],
                                                float inv_tau, float (&abar)[M])
@@ -277,10 +283,8 @@ __device__ __forceinline__ void relax_backward(const StepRec<M> (&rec)[N], const
             a_in[j] = 0.0f;
             if (has_next) {
                 const float om = rec[k].om[j];
-                const bool live = !kFloor || om >= kFltMin;
-                const float rinv = live ? __builtin_amdgcn_rcpf(om) : 0.0f;
-                mubar = __builtin_fmaf(-abar[j], rinv, sbar[j]);
-                a_in[j] = live ? abar[j] : 0.0f;
+                a_in[j] = !kFloor || om > kFltMin ? abar[j] : 0.0f;
+                mubar = __builtin_fmaf(-a_in[j], __builtin_amdgcn_rcpf(om), sbar[j]);
             }
             t[j] = rec[k].mu[j] * mubar;
         }
