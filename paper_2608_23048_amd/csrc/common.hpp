@@ -135,11 +135,24 @@ __device__ __forceinline__ void stream_store(const T& v, T* p)
 
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t b) { return __uint_as_float(b << 16); }
 
-// fp32 -> bf16 bits, round to nearest even (finite inputs).
-__device__ __forceinline__ uint32_t float_to_bf16_rne(float f)
+// The bf16 values nearest to lo and hi (ties to even), packed with lo in the
+// low half: one gfx950 v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi)
 {
-    const uint32_t b = __float_as_uint(f);
-    return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    const f32x2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// bf16(W (.) S) for four consecutive elements: w holds the bf16 patterns of W
+// in pairs (element 2i in the low half of w[i]).
+__device__ __forceinline__ u32x2 soft_product4(uint32_t w01, uint32_t w23, const float* S)
+{
+    return u32x2{bf16x2_rne(bf16_bits_to_float(w01 & 0xFFFFu) * S[0],
+                            bf16_bits_to_float(w01 >> 16) * S[1]),
+                 bf16x2_rne(bf16_bits_to_float(w23 & 0xFFFFu) * S[2],
+                            bf16_bits_to_float(w23 >> 16) * S[3])};
 }
 
 // Loads of one group: m fp32 logits (m/4 16-byte loads) and m bf16 values
@@ -169,6 +182,21 @@ __device__ __forceinline__ void load_bf16(const uint16_t* p, uint32_t (&w)[M])
         const u32x4 v = stream_load(reinterpret_cast<const u32x4*>(p));
         w[0] = v.x & 0xFFFFu; w[1] = v.x >> 16; w[2] = v.y & 0xFFFFu; w[3] = v.y >> 16;
         w[4] = v.z & 0xFFFFu; w[5] = v.z >> 16; w[6] = v.w & 0xFFFFu; w[7] = v.w >> 16;
+    }
+}
+
+// The same loads, the values left in pairs (element 2i in the low half of
+// word i).
+template <int M>
+__device__ __forceinline__ void load_bf16_pairs(const uint16_t* p, uint32_t (&w)[M / 2])
+{
+    if constexpr (M == 4) {
+        const u32x2 v = stream_load(reinterpret_cast<const u32x2*>(p));
+        w[0] = v.x; w[1] = v.y;
+    } else {
+        static_assert(M == 8, "m");
+        const u32x4 v = stream_load(reinterpret_cast<const u32x4*>(p));
+        w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
     }
 }
 

@@ -89,19 +89,16 @@ constexpr int kBwdChunks = ROI_BWD_CHUNKS; // chunks per block in the m = 4 back
 constexpr int kLaneBlock = ROI_LANE_BLOCK;
 static_assert(kLaneBlock >= kLogCells + 64 && kLaneBlock % 64 == 0, "lane block size");
 
-// m bf16 values (16-bit patterns in the low half of each word), stored packed.
+// bf16(W (.) S) of one group, stored: w holds the bf16 patterns of W in
+// pairs (load_bf16_pairs).
 template <int M>
-__device__ __forceinline__ void store_pairs(uint16_t* p, const uint32_t (&h)[M])
+__device__ __forceinline__ void store_soft_product(uint16_t* p, const uint32_t (&w)[M / 2],
+                                                   const float (&S)[M])
 {
-    if constexpr (M == 4) {
-        const u32x2 v = {h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
-        stream_store(v, reinterpret_cast<u32x2*>(p));
-    } else {
-        static_assert(M == 8, "m");
-        const u32x4 v = {h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                         h[6] | (h[7] << 16)};
-        stream_store(v, reinterpret_cast<u32x4*>(p));
-    }
+#pragma unroll
+    for (int t = 0; t < M / 4; ++t)
+        stream_store(soft_product4(w[2 * t], w[2 * t + 1], S + 4 * t),
+                     reinterpret_cast<u32x2*>(p) + t);
 }
 
 // Masked bf16 weights: the kept value, or +0.0 (bits 0x0000).
@@ -426,11 +423,10 @@ __global__ __launch_bounds__(kLaneBlock) void fwd_lane_kernel(FwdBatch a)
                     }
                 }
                 if (soft) { // pure soft forward: W (.) S, rounded to bf16
-                    uint32_t ws[M];
+                    uint32_t wp[M / 2];
 #pragma unroll
-                    for (int j = 0; j < M; ++j)
-                        ws[j] = float_to_bf16_rne(bf16_bits_to_float(w[u][j]) * S[j]);
-                    store_pairs<M>(pc.Wm + q * M, ws);
+                    for (int i = 0; i < M / 2; ++i) wp[i] = w[u][2 * i] | (w[u][2 * i + 1] << 16);
+                    store_soft_product<M>(pc.Wm + q * M, wp, S);
                 }
             }
         }
@@ -464,13 +460,13 @@ __device__ __forceinline__ void soft_lane_chunk(const FwdBatch& a, const FwdPiec
     const float4 cells = log_cells_of_lane();
     __builtin_amdgcn_sched_barrier(0);
     float phi[U][M];
-    uint32_t w[U][M];
+    uint32_t w[U][M / 2];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int64_t q = base + u * kLaneBlock + threadIdx.x;
         if (kFull || q < ng_total) {
             load_logits<M>(pc.phi + q * M, phi[u]);
-            load_bf16<M>(pc.W + q * M, w[u]);
+            load_bf16_pairs<M>(pc.W + q * M, w[u]);
         }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -501,10 +497,7 @@ __device__ __forceinline__ void soft_lane_chunk(const FwdBatch& a, const FwdPiec
         } else {
             relax_forward<M, N, true, false>(b, bmax, a.inv_tau, S, unused);
         }
-        uint32_t ws[M];
-#pragma unroll
-        for (int j = 0; j < M; ++j) ws[j] = float_to_bf16_rne(bf16_bits_to_float(w[u][j]) * S[j]);
-        store_pairs<M>(pc.Wm + q * M, ws);
+        store_soft_product<M>(pc.Wm + q * M, w[u], S);
     }
 }
 

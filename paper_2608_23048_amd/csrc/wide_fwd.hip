@@ -87,14 +87,8 @@ __global__ __launch_bounds__(kBlock) void fwd_wide_kernel(FwdBatch a)
                 const f32x4 sv = {S[0], S[1], S[2], S[3]};
                 stream_store(sv, reinterpret_cast<f32x4*>(pc.S + slot * 4));
             }
-            if (soft) { // pure soft forward: W (.) S, rounded to bf16
-                const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
-                const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
-                const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
-                const uint32_t h3 = float_to_bf16_rne(bf16_bits_to_float(wv.y >> 16) * S[3]);
-                const u32x2 out = {h0 | (h1 << 16), h2 | (h3 << 16)};
-                stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
-            }
+            if (soft) // pure soft forward: W (.) S, rounded to bf16
+                stream_store(soft_product4(wv.x, wv.y, S), reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
         }
     }
 }
@@ -137,12 +131,7 @@ __device__ __forceinline__ void soft_wide_slot(const FwdBatch& a, const FwdPiece
     StepRec<4> unused[N]; // not written when records are not kept
     wide_relax_forward<L, N, false, kQ>(kappa, a.key_scale, a.inv_tau, a.exp_span, true, S,
                                         unused);
-    const uint32_t h0 = float_to_bf16_rne(bf16_bits_to_float(wv.x & 0xFFFFu) * S[0]);
-    const uint32_t h1 = float_to_bf16_rne(bf16_bits_to_float(wv.x >> 16) * S[1]);
-    const uint32_t h2 = float_to_bf16_rne(bf16_bits_to_float(wv.y & 0xFFFFu) * S[2]);
-    const uint32_t h3 = float_to_bf16_rne(bf16_bits_to_float(wv.y >> 16) * S[3]);
-    const u32x2 out = {h0 | (h1 << 16), h2 | (h3 << 16)};
-    stream_store(out, reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
+    stream_store(soft_product4(wv.x, wv.y, S), reinterpret_cast<u32x2*>(pc.Wm + slot * 4));
 }
 
 // Pure soft forward whose only output is bf16(W (.) S): the relaxation at the

@@ -71,6 +71,25 @@ LOG2_LN2 = float(np.log2(np.log(2.0)))
 FP32_FLOOR_FACTOR = 8.0
 
 
+def bf16_rne_bits(x) -> np.ndarray:
+    """bf16 patterns of fp32 values, round to nearest with ties to even
+    (finite inputs)."""
+    b = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def soft_product_exact(W_bits, S, Ws_bits, what):
+    """W_soft is bf16(W (.) S) for the kernel's own fp32 S, bit for bit: the
+    fp32 product (one rounding) then the nearest bf16, ties to even."""
+    w = (np.asarray(W_bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).reshape(-1)
+    prod = w * np.asarray(S, dtype=np.float32).reshape(-1)  # fp32 multiply, round to nearest
+    want = bf16_rne_bits(prod)
+    got = np.asarray(Ws_bits, dtype=np.uint16).reshape(-1)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, (f"{what}: {bad.size} elements are not the rounded product; first at "
+                           f"{bad[0]}: got 0x{got[bad[0]]:04x}, want 0x{want[bad[0]]:04x}")
+
+
 def sbar_of(G_bits, W_bits) -> np.ndarray:
     """dL/dS = dL/dW_masked (.) W in fp64 (exact: a product of two bf16 values)."""
     g = (np.asarray(G_bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)

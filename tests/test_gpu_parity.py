@@ -18,7 +18,8 @@ import oracle
 import paper_2608_23048_amd as roi
 from paper_2608_23048_amd import workloads as wl
 from tests.gpu_helpers import (HW_NOISE_A, HW_NOISE_B, HW_NOISE_MAX, LOG2_LN2, LOG2E,
-                               assert_close, bf16_bits, f32, fp32_key_floor, sbar_of, say)
+                               assert_close, bf16_bits, f32, fp32_key_floor, sbar_of, say,
+                               soft_product_exact)
 
 pytestmark = pytest.mark.gpu
 
@@ -1196,6 +1197,7 @@ def test_soft_forward(dev, case):
     Wh, S2, idx2 = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True)
     torch.cuda.synchronize()
     assert torch.equal(idx, idx2) and torch.equal(S.view(torch.int32), S2.view(torch.int32))
+    soft_product_exact(bf16_bits(W), f32(S), bf16_bits(Ws), "W_soft against the kernel's S")
     tau32, lam32 = float(np.float32(tau)), float(np.float32(lam))
     _, S_o, idx_o = oracle.mask_fwd(bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
     assert np.array_equal(idx.cpu().numpy(), idx_o)
@@ -1226,11 +1228,12 @@ def test_soft_forward_alone(dev, case):
     Ws, S, idx = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=False,
                               want_idx=False, soft_forward=True)
     assert S is None and idx is None
-    We, _, _ = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True,
-                            soft_forward=True)
+    We, Se, _ = roi.mask_fwd(W, L, n, m, tau, lam, seed, step, off, want_soft=True,
+                             soft_forward=True)
     torch.cuda.synchronize()
     assert torch.equal(Ws.view(torch.int16), We.view(torch.int16)), \
         "the soft forward alone differs from the soft forward with S"
+    soft_product_exact(bf16_bits(W), f32(Se), bf16_bits(Ws), "W_soft against the kernel's S")
     tau32, lam32 = float(np.float32(tau)), float(np.float32(lam))
     _, S_o, _ = oracle.mask_fwd(bf16_bits(W), f32(L), n, m, tau32, lam32, seed, step, off)
     wf = (bf16_bits(W).astype(np.uint32) << 16).view(np.float32).astype(np.float64).reshape(-1)
