@@ -316,53 +316,102 @@ __global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_fwd_kernel
     }
 }
 
-template <int M, int N>
-__global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_bwd_kernel(CatArgs a)
+// The keys from the logits and the noise ng = -g of a group's candidates,
+// kappa = fl(fl(alpha / lambda) + g); lambda = 1 is a wave-uniform branch
+// without the division.
+template <int C>
+__device__ __forceinline__ void cat_keys_from_noise(const float (&alpha)[C], const float (&ng)[C],
+                                                    float lambda, float (&k)[C])
+{
+    if (__builtin_amdgcn_readfirstlane(__float_as_uint(lambda)) == 0x3F800000u) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) k[c] = alpha[c] - ng[c];
+    } else {
+#pragma unroll
+        for (int c = 0; c < C; ++c) k[c] = alpha[c] / lambda - ng[c];
+    }
+}
+
+// One chunk of B groups of the categorical backward.  The loads go out first:
+// the group's W and dL/dW_masked, its logits (per lane, or for the staged
+// tile this thread's share of the block's contiguous logits), and the log
+// cells.  With up to 8 candidates the noise -- C Philox words and 2C
+// logarithms per group, most of the arithmetic -- needs none of them and runs
+// while they are in flight; with more, the C noise values and the tile share
+// would not fit in registers beside each other, and each key is formed as its
+// noise is drawn, after the loads.  kFull: all B groups are inside the
+// array, so no per-lane condition makes the compiler wait for every load at
+// a join.
+template <int M, int N, bool kFull>
+__device__ __forceinline__ void cat_bwd_chunk(const CatArgs& a, float* tile, float2* tab,
+                                              int64_t base)
 {
     constexpr int C = Candidates<M, N>::C;
     constexpr int B = cat_block(C);
     constexpr bool kStage = cat_staged_bwd(C);
-    __shared__ float tile[kStage ? B * C : 2];
-    // Every group takes the exact keys: each wave keeps its own copy of the
-    // log cells in LDS (noise.hpp).
-    __shared__ float4 wave_tabs[B / 64][kLogCells / 2];
-    const float2* tab = reinterpret_cast<const float2*>(wave_tabs[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)]);
-    // The loop bound is uniform over the block (the tile copies are cooperative).
-    for (int64_t base = (int64_t)blockIdx.x * B; base < a.ngroups; base += (int64_t)gridDim.x * B) {
-        const int here = (int)(a.ngroups - base < B ? a.ngroups - base : B);
-        const int64_t q = base + threadIdx.x;
-        const bool live = (int)threadIdx.x < here;
-        const float4 cells = log_cells_of_lane();
-        float alpha[C];
-        if constexpr (kStage) {
-            tile_in<B>(a.alpha + base * C, tile, here * C);
-            __syncthreads();
-            if (live) {
+    constexpr bool kNoiseFirst = C <= 8;
+    constexpr int kShare = kStage && kNoiseFirst ? C / 2 : 1; // 8-byte tile pieces per thread
+    const int here = kFull ? B : (int)(a.ngroups - base);
+    const int64_t q = base + threadIdx.x;
+    const bool live = kFull || (int)threadIdx.x < here;
+    uint32_t w[M / 2], g[M / 2];
+    float alpha[C];
+    f32x2v share[kShare];
+    if (live) {
+        load_bf16_pairs<M>(a.W + q * M, w);
+        load_bf16_pairs<M>(a.G + q * M, g);
+    }
+    if constexpr (kStage) {
+        if constexpr (kFull && kNoiseFirst) {
+            const f32x2v* src = reinterpret_cast<const f32x2v*>(a.alpha + base * C);
 #pragma unroll
-                for (int c = 0; c < C; ++c) alpha[c] = tile[threadIdx.x * C + c];
-            }
-            __syncthreads(); // the gradients go into the same tile
-        } else if (live) {
-            load_cat_logits<C>(a.alpha + q * C, alpha);
+            for (int i = 0; i < kShare; ++i) share[i] = stream_load(src + threadIdx.x + i * B);
         }
-        float d[C];
-        uint32_t w[M], g[M];
-        if (live) {
-            load_bf16<M>(a.W + q * M, w);
-            load_bf16<M>(a.G + q * M, g);
+    } else if (live) {
+        load_cat_logits<C>(a.alpha + q * C, alpha);
+    }
+    const float4 cells = log_cells_of_lane();
+    __builtin_amdgcn_sched_barrier(0);
+    float ng[kNoiseFirst ? C : 1];
+    uint32_t x[C];
+    cat_words<C>(a.group0 + (uint64_t)q, a.key, x);
+    publish_log_table(tab, cells);
+    if constexpr (kNoiseFirst) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) ng[c] = neg_gumbel_from_word(x[c], tab);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (kStage) {
+        if constexpr (kFull && kNoiseFirst) {
+            f32x2v* dst = reinterpret_cast<f32x2v*>(tile);
+#pragma unroll
+            for (int i = 0; i < kShare; ++i) dst[threadIdx.x + i * B] = share[i];
+        } else {
+            tile_in<B>(a.alpha + base * C, tile, here * C);
         }
-        publish_wave_log_table(const_cast<float2*>(tab), cells);
+        __syncthreads();
         if (live) {
-        uint32_t x[C];
-        cat_words<C>(a.group0 + (uint64_t)q, a.key, x);
-        // the keys the forward sampled: kappa = fl(fl(alpha / lambda) + g)
+#pragma unroll
+            for (int c = 0; c < C; ++c) alpha[c] = tile[threadIdx.x * C + c];
+        }
+        __syncthreads(); // the gradients go into the same tile
+    }
+    float d[C];
+    if (live) {
+        // the keys the forward sampled, and their softmax
         float y[C];
-        cat_exact_keys<C>(alpha, x, a.lambda, tab, y);
+        if constexpr (kNoiseFirst)
+            cat_keys_from_noise<C>(alpha, ng, a.lambda, y);
+        else
+            cat_exact_keys<C>(alpha, x, a.lambda, tab, y);
         cat_softmax<C>(y, kLog2e * a.inv_tau);
         // Straight-through: dL/dS = dL/dW_masked (.) W; ybar_c = sum_{j in c} sbar_j.
         float sbar[M];
 #pragma unroll
-        for (int j = 0; j < M; ++j) sbar[j] = bf16_bits_to_float(g[j]) * bf16_bits_to_float(w[j]);
+        for (int i = 0; i < M / 2; ++i) {
+            sbar[2 * i] = bf16_bits_to_float(g[i] & 0xFFFFu) * bf16_bits_to_float(w[i] & 0xFFFFu);
+            sbar[2 * i + 1] = bf16_bits_to_float(g[i] >> 16) * bf16_bits_to_float(w[i] >> 16);
+        }
         float ybar[C], dot = 0.0f;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
@@ -376,18 +425,37 @@ __global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_bwd_kernel
         const float s = a.inv_tau * a.inv_lambda;
 #pragma unroll
         for (int c = 0; c < C; ++c) d[c] = y[c] * (ybar[c] - dot) * s;
-        }
-        if constexpr (kStage) {
-            if (live) {
+    }
+    if constexpr (kStage) {
+        if (live) {
 #pragma unroll
-                for (int c = 0; c < C; ++c) tile[threadIdx.x * C + c] = d[c];
-            }
-            __syncthreads();
-            tile_out<B>(tile, a.dalpha + base * C, here * C);
-            __syncthreads(); // before the next tile overwrites it
-        } else if (live) {
-            store_cat<C>(a.dalpha + q * C, d);
+            for (int c = 0; c < C; ++c) tile[threadIdx.x * C + c] = d[c];
         }
+        __syncthreads();
+        tile_out<B>(tile, a.dalpha + base * C, here * C);
+        __syncthreads(); // before the next chunk overwrites the tile
+    } else if (live) {
+        store_cat<C>(a.dalpha + q * C, d);
+    }
+}
+
+template <int M, int N>
+__global__ __launch_bounds__(cat_block(Candidates<M, N>::C)) void cat_bwd_kernel(CatArgs a)
+{
+    constexpr int C = Candidates<M, N>::C;
+    constexpr int B = cat_block(C);
+    __shared__ float tile[cat_staged_bwd(C) ? B * C : 2];
+    // Every group takes the exact keys; the block's waves share one copy of
+    // the log cells in LDS (noise.hpp).
+    __shared__ float4 tab4[kLogCells / 2];
+    float2* tab = reinterpret_cast<float2*>(tab4);
+    // The loop bound and the full / partial choice are uniform over the block
+    // (the tile copies are cooperative).
+    for (int64_t base = (int64_t)blockIdx.x * B; base < a.ngroups; base += (int64_t)gridDim.x * B) {
+        if (base + B <= a.ngroups)
+            cat_bwd_chunk<M, N, true>(a, tile, tab, base);
+        else
+            cat_bwd_chunk<M, N, false>(a, tile, tab, base);
     }
 }
 
