@@ -718,7 +718,9 @@ def test_export_feeds_sparse_mfma(dev, case):
 CAT = [(37, 36, 2, 4, 1.0, 1.0, 0), (64, 96, 2, 4, 0.3, 0.6, 5), (33, 64, 1, 4, 0.7, 1.0, 3),
        (33, 64, 3, 4, 1.3, 1.0, 1), (21, 64, 4, 4, 1.0, 1.0, 0), (61, 88, 2, 8, 0.5, 1.0, 7),
        (61, 88, 4, 8, 1.0, 2.0, 2 ** 33 + 5), (25, 64, 1, 8, 0.4, 1.0, 11),
-       (25, 64, 7, 8, 1.0, 1.0, 0), (19, 96, 3, 8, 0.8, 1.0, 2 ** 40)]
+       (25, 64, 7, 8, 1.0, 1.0, 0), (19, 96, 3, 8, 0.8, 1.0, 2 ** 40),
+       # 8 candidates over several full 256-group chunks and a ragged one
+       (70, 64, 1, 8, 0.6, 1.0, 9), (67, 48, 7, 8, 1.0, 0.8, 2 ** 32 - 100)]
 
 
 def cat_fp32_floor(alpha, G_bits, W_bits, n, m, tau, lam, seed, step, goff):
