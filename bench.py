@@ -823,8 +823,8 @@ def main() -> int:
         t = args.traffic_summary
         return traffic_summary(t[0:3], t[3:6], int(t[6]), work.numel, work.n, work.m)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the sampler needs no collectives, and this build "
-              "runs and reports a single MI355X (pass --gpus 1).", file=sys.stderr)
+        print("bench.py measures one GPU only: the sampler needs no collectives, and the "
+              "benchmark runs and reports a single MI355X (pass --gpus 1).", file=sys.stderr)
         return 2
 
     if args.mode == "soft":
