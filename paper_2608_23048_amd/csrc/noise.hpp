@@ -138,14 +138,14 @@ __device__ __forceinline__ void fill_log_table(float2* tab)
     if (i < kLogCells) tab[i] = kLogCellTable.cell[i];
 }
 
-// A wave's own copy of the cells in LDS, for kernels in which every group
-// takes the exact keys.  Lane l holds cells 2l and 2l + 1 (16 bytes): it loads
-// them with log_cells_of_lane() and stores them into the wave's 1 KiB copy
-// with publish_wave_log_table().  The wave reads only its own copy, so no
-// block barrier is needed: its LDS writes are complete (lgkmcnt 0) before any
-// of its lanes reads.  Every lane of the wave must take part.  The load is
-// issued ahead of the kernel's HBM streams so that waiting for it (a cached
-// read) does not wait for them.
+// The cells in LDS for kernels in which every group takes the exact keys:
+// one 1 KiB copy per block.  Lane l holds cells 2l and 2l + 1 (16 bytes),
+// loaded with log_cells_of_lane() ahead of the kernel's HBM streams, so that
+// waiting for this cached read does not wait for them.  Every wave then
+// stores the whole table with publish_log_table(): the same values at the
+// same addresses, so a wave whose own writes have completed (lgkmcnt 0) sees
+// the cells whatever the other waves do, and no wave waits for another (no
+// block barrier).  Every lane of the wave must take part.
 __device__ __forceinline__ float4 log_cells_of_lane()
 {
     // The empty asm keeps the load where it is written (inside the caller's
@@ -156,21 +156,11 @@ __device__ __forceinline__ float4 log_cells_of_lane()
     return reinterpret_cast<const float4*>(kLogCellTable.cell)[lane];
 }
 
-__device__ __forceinline__ void publish_wave_log_table(float2* wave_tab, float4 cells)
-{
-    reinterpret_cast<float4*>(wave_tab)[threadIdx.x & 63] = cells;
-    __builtin_amdgcn_s_waitcnt(0xC07F); // lgkmcnt(0); vmcnt and expcnt not waited for
-    __builtin_amdgcn_wave_barrier();
-}
-
-// The same with one copy shared by the block's waves: each wave writes all of
-// it (the same values at the same addresses, so a wave that reads after its
-// own writes have completed sees the cells whatever the other waves do), and
-// no wave waits for another.  The copy is the block's only LDS array, so its
-// address is a constant and a lookup needs no base register.
 __device__ __forceinline__ void publish_log_table(float2* tab, float4 cells)
 {
-    publish_wave_log_table(tab, cells);
+    reinterpret_cast<float4*>(tab)[threadIdx.x & 63] = cells;
+    __builtin_amdgcn_s_waitcnt(0xC07F); // lgkmcnt(0); vmcnt and expcnt not waited for
+    __builtin_amdgcn_wave_barrier();
 }
 
 // ln of the float whose bit pattern is ix.  With t = ix - kLogZBaseBits the
