@@ -708,8 +708,9 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // How the exp-domain recursion raises omega to 1 / tau: 1 or 2 when 1 / tau
 // is that integer (by multiplication), else 0 (exp2 and log2).
 // -1 where the exp-domain form is off (q = 1 / tau above 2.25, see
-// exp_span_limit): the backward then has a log-domain-only variant.  The
-// forwards treat -1 as 0 (their exp-domain branch is never taken there).
+// exp_span_limit): the backward and the soft forward alone then have a
+// log-domain-only variant.  The other forwards treat -1 as 0 (their
+// exp-domain branch is never taken there).
 int tau_mode(float tau)
 {
     if (tau == 1.0f) return 1;
